@@ -1,0 +1,203 @@
+/*
+ * dmoe.h -- C ABI of the block-routed MoE layer forward for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * One MoE layer forward of a block-diffusion decode step, split into the
+ * steps of the routing procedure of "dMoE: dLLMs with Learnable Block
+ * Experts" (Sec. 4.2 and Alg. 1) followed by expert execution:
+ *
+ *   dmoe_router_logits         token scores s_i = Router(t_i)  (Sec. 4.2)
+ *   dmoe_block_aggregate_topk  block scores S_block = mean_i s_i, coreset
+ *                              C = top-k(S_block), per-token weights
+ *                              (Sec. 4.2 aggregation; Alg. 1 with |C| = k)
+ *   dmoe_token_topk            token-level top-k (the "Original" routing of
+ *                              Sec. 5.1, the baseline)
+ *   dmoe_build_expert_schedule unique experts of the forward and the rows
+ *                              (token, slot) that use each one (the unique
+ *                              expert count of Sec. 3 is its n_unique)
+ *   dmoe_expert_ffn            SwiGLU FFN of every unique expert over its
+ *                              rows, plus the always-on shared expert
+ *   dmoe_combine               y_t = sum_j w[t,j] * FFN_{e_tj}(x_t) + FFN_s(x_t)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every pointer argument is a DEVICE pointer (memory the caller allocated on
+ *    the GPU, e.g. with hipMalloc or a torch CUDA tensor) unless the comment
+ *    says otherwise.  The caller owns all memory.  The library allocates
+ *    nothing and keeps no state between calls.
+ *  - All arrays are dense and row-major.  Matrices are indexed [row][col] with
+ *    the last index contiguous.
+ *  - Tokens are block-major: block b of a forward is rows
+ *    [b*block_size, (b+1)*block_size) of the hidden states.
+ *  - stream is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *    entry point only enqueues work on it and returns without synchronising;
+ *    a fault inside a kernel surfaces at the caller's next synchronisation.
+ *  - Ordering of a top-k: indices by (score descending, expert id ascending),
+ *    so an exact tie goes to the lower expert id.
+ *  - Errors: arguments are validated on the host before anything is launched.
+ *      DMOE_ERR_INVALID_ARG  a required pointer is NULL, a size is out of range,
+ *                            or a pointer is not aligned as documented;
+ *      DMOE_ERR_UNSUPPORTED  valid arguments with no kernel (a shape outside
+ *                            the documented limits);
+ *      DMOE_ERR_HIP          a kernel launch failed.
+ *    On a non-OK status nothing was enqueued (except for DMOE_ERR_HIP) and
+ *    dmoe_last_error() describes the cause.
+ *  - Element types: dmoe_dtype gives the storage type of hidden states,
+ *    weights and the layer output.  Router logits, probabilities, block
+ *    scores, combine weights and gaps are always float32; expert indices and
+ *    schedules are int32.  Accumulation is float32 throughout.
+ *  - Alignment: every pointer must be 16-byte aligned.
+ */
+#ifndef DMOE_H
+#define DMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dmoe_status {
+  DMOE_OK = 0,
+  DMOE_ERR_INVALID_ARG = -1,
+  DMOE_ERR_UNSUPPORTED = -2,
+  DMOE_ERR_HIP = -3
+} dmoe_status;
+
+typedef enum dmoe_dtype {
+  DMOE_F32 = 0,  /* IEEE binary32 */
+  DMOE_BF16 = 1  /* bfloat16 (upper half of a binary32) */
+} dmoe_dtype;
+
+/*
+ * Unique-expert schedule of one forward (device arrays, caller-allocated).
+ * Written by dmoe_build_expert_schedule, read by dmoe_expert_ffn.
+ *   n_unique [1]        number of distinct experts selected in the forward
+ *   unique   [E]        their ids, ascending, in unique[0 .. n_unique)
+ *   offsets  [E + 1]    rows of unique[u] are rows offsets[u] .. offsets[u+1]
+ *                       of row_token / row_slot; offsets[n_unique] = n_rows
+ *   row_token[n_rows]   token of each row (n_rows = n_groups*group_size*k)
+ *   row_slot [n_rows]   slot j in 0..k-1 of the token's expert list
+ * Within one expert, rows are ordered by token.
+ */
+typedef struct dmoe_schedule {
+  int32_t* n_unique;
+  int32_t* unique;
+  int32_t* offsets;
+  int32_t* row_token;
+  int32_t* row_slot;
+} dmoe_schedule;
+
+/*
+ * Router scores (Sec. 4.2, s_i = Router(t_i)): linear router and softmax.
+ *   logits[t][e] = sum_h x[t][h] * w_router[e][h] + bias[e]
+ *   probs[t][:]  = softmax(logits[t][:]) over all E experts (max-subtracted)
+ * x [T][H] and w_router [E][H] of type dt; bias [E] float32 or NULL (no bias);
+ * logits [T][E] float32 or NULL (not stored); probs [T][E] float32.
+ * Limits: T >= 1; 1 <= E <= 4096; H >= 1.  For DMOE_BF16: H % 128 == 0 and
+ * E % 32 == 0 (matrix-core tiles); DMOE_F32 has no further limit.
+ */
+dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
+                               dmoe_dtype dt, int T, int H, int E,
+                               float* logits, float* probs, void* stream);
+
+/*
+ * Block-level routing (Sec. 4.2 aggregation, Alg. 1 with a coreset of size k).
+ * For each block b of block_size consecutive tokens:
+ *   S[b][e]     = (1/block_size) * sum_{t in b} probs[t][e]   (token order)
+ *   C_b         = top-k of S[b][:]                       -> block_experts[b][0..k)
+ *   gap[b]      = S_(k) - S_(k+1)  (k-th minus (k+1)-th largest; +inf if k == E)
+ *   w[t][j]     = probs[t][C_b[j]] / sum_j' probs[t][C_b[j']]   for t in b
+ * probs [n_blocks*block_size][E]; block_scores [n_blocks][E] or NULL;
+ * block_experts [n_blocks][k] int32; combine_w [n_blocks*block_size][k];
+ * gap [n_blocks] or NULL.
+ * Limits: n_blocks >= 1; 1 <= block_size <= 4096; 1 <= k <= min(E, 64);
+ * E <= 4096.
+ */
+dmoe_status dmoe_block_aggregate_topk(const float* probs, int n_blocks, int block_size, int E,
+                                      int k, float* block_scores, int32_t* block_experts,
+                                      float* combine_w, float* gap, void* stream);
+
+/*
+ * Token-level top-k routing (the baseline): for each token t
+ *   R_t = top-k of probs[t][:] -> token_experts[t][0..k)
+ *   gap[t] = p_(k) - p_(k+1) (+inf if k == E)
+ *   w[t][j] = probs[t][R_t[j]] / sum_j' probs[t][R_t[j']]
+ * probs [T][E]; token_experts [T][k] int32; combine_w [T][k]; gap [T] or NULL.
+ * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 4096.
+ */
+dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* token_experts,
+                            float* combine_w, float* gap, void* stream);
+
+/*
+ * Unique-expert schedule.  experts [n_groups][k] int32 holds one expert list
+ * per group; group g covers tokens [g*group_size, (g+1)*group_size).  Block
+ * routing passes block_experts with group_size = block_size; token routing
+ * passes token_experts with group_size = 1.  The lists of a group must hold k
+ * distinct ids in [0, E) (what the two top-k entry points produce); a
+ * violation is not detected and yields an undefined schedule.
+ * Writes every array of sched (see dmoe_schedule).
+ * Limits: n_groups >= 1; group_size >= 1; 1 <= k <= min(E, 64); E <= 512;
+ * n_groups*group_size*k < 2^31.
+ */
+dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int group_size,
+                                       int k, int E, dmoe_schedule sched, void* stream);
+
+/*
+ * Bytes of workspace dmoe_expert_ffn needs for these sizes (the SwiGLU
+ * activations of every routed row and every shared-expert row).
+ * Returns 0 on invalid sizes.
+ */
+size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
+
+/*
+ * Expert execution: for every unique expert e = sched.unique[u] and each of
+ * its rows (t, j):
+ *   h = silu(w_gate[e] x_t) * (w_up[e] x_t)          (SwiGLU, silu(a) = a/(1+e^-a))
+ *   slot_out[t][j][:] = w_down[e] h
+ * and, when the shared expert is present (ws_gate != NULL), for every token t:
+ *   shared_out[t][:] = ws_down (silu(ws_gate x_t) * (ws_up x_t))
+ * Each selected expert's weights are streamed once per call.
+ * x [T][H]; w_gate, w_up [E][I][H]; w_down [E][H][I]; ws_gate, ws_up [I_s][H];
+ * ws_down [H][I_s] (all type dt; the three shared pointers are all NULL with
+ * I_s == 0, or all set with I_s > 0).
+ * sched: written by dmoe_build_expert_schedule for these T and k.
+ * max_unique: an upper bound of sched.n_unique known on the host (the grid is
+ * sized for it): min(E, n_groups*k).
+ * slot_out [T][k][H] float32 (every (t, j) is written); shared_out [T][H]
+ * float32 (NULL iff no shared expert).
+ * workspace: device scratch of at least dmoe_ffn_workspace_size(...) bytes,
+ * ws_bytes its size.  Its contents on entry do not matter.
+ * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 512; 1 <= max_unique <= E.
+ * DMOE_BF16: H % 128 == 0, I % 128 == 0, I_s % 128 == 0 (matrix-core tiles).
+ * DMOE_F32: any H, I, I_s >= 1.
+ */
+dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up,
+                            const void* w_down, const void* ws_gate, const void* ws_up,
+                            const void* ws_down, dmoe_dtype dt, int T, int H, int E, int I,
+                            int I_s, int k, int max_unique, dmoe_schedule sched, float* slot_out,
+                            float* shared_out, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Weighted combine:
+ *   y[t][h] = sum_{j=0..k-1} combine_w[t][j] * slot_out[t][j][h]  (+ shared_out[t][h])
+ * summed in slot order in float32, stored as dt.
+ * slot_out [T][k][H] float32; combine_w [T][k] float32; shared_out [T][H]
+ * float32 or NULL; y [T][H] of type dt.
+ * Limits: T >= 1; 1 <= k <= 64; H >= 1; H % 4 == 0.
+ */
+dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const float* shared_out,
+                         dmoe_dtype dt, int T, int H, int k, void* y, void* stream);
+
+/* Message describing the last non-OK status returned on this thread ("" if none). */
+const char* dmoe_last_error(void);
+
+/* Library version, e.g. "0.1.0" (host string, owned by the library). */
+const char* dmoe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DMOE_H */

@@ -1,0 +1,206 @@
+// C ABI of libdmoe: argument validation on the host, then the kernel
+// launchers.  Validation touches no GPU state, so every error path can be
+// exercised on a machine without a GPU.
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "dmoe_common.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dmoe_status fail(dmoe_status st, const char* fn, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = std::string(fn) + ": " + buf;
+  return st;
+}
+
+dmoe_status ok() {
+  g_last_error.clear();
+  return DMOE_OK;
+}
+
+dmoe_status hip_status(hipError_t err, const char* fn) {
+  if (err == hipSuccess) return ok();
+  return fail(DMOE_ERR_HIP, fn, "kernel launch failed: %s", hipGetErrorString(err));
+}
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+bool valid_dtype(dmoe_dtype dt) { return dt == DMOE_F32 || dt == DMOE_BF16; }
+
+constexpr int kMaxE = 4096;
+constexpr int kMaxScheduleE = 512;
+constexpr int kMaxK = 64;
+constexpr long kIntLimit = 0x7fffffffL;
+
+#define REQUIRE(cond, ...)                                  \
+  do {                                                      \
+    if (!(cond)) return fail(DMOE_ERR_INVALID_ARG, __func__, __VA_ARGS__); \
+  } while (0)
+#define SUPPORT(cond, ...)                                  \
+  do {                                                      \
+    if (!(cond)) return fail(DMOE_ERR_UNSUPPORTED, __func__, __VA_ARGS__); \
+  } while (0)
+#define ALIGNED(p) REQUIRE(!misaligned(p), #p " is not 16-byte aligned")
+
+}  // namespace
+
+extern "C" {
+
+const char* dmoe_last_error(void) { return g_last_error.c_str(); }
+
+const char* dmoe_version(void) { return "0.1.0"; }
+
+dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
+                               dmoe_dtype dt, int T, int H, int E, float* logits, float* probs,
+                               void* stream) {
+  REQUIRE(x && w_router && probs, "x, w_router and probs must not be NULL");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(static_cast<long>(T) * E <= kIntLimit && static_cast<long>(T) * H <= kIntLimit,
+          "T*E and T*H must fit in int32");
+  ALIGNED(x);
+  ALIGNED(w_router);
+  ALIGNED(bias);
+  ALIGNED(logits);
+  ALIGNED(probs);
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
+    SUPPORT(E % 32 == 0, "bf16 router needs E %% 32 == 0 (E=%d)", E);
+  }
+  return hip_status(dmoe::launch_router(x, w_router, bias, dt, T, H, E, logits, probs,
+                                        static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
+dmoe_status dmoe_block_aggregate_topk(const float* probs, int n_blocks, int block_size, int E,
+                                      int k, float* block_scores, int32_t* block_experts,
+                                      float* combine_w, float* gap, void* stream) {
+  REQUIRE(probs && block_experts && combine_w, "probs, block_experts and combine_w must not be NULL");
+  REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
+  REQUIRE(block_size >= 1 && block_size <= 4096, "block_size=%d must be in [1, 4096]", block_size);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(static_cast<long>(n_blocks) * block_size * E <= kIntLimit, "T*E must fit in int32");
+  ALIGNED(probs);
+  ALIGNED(block_scores);
+  ALIGNED(block_experts);
+  ALIGNED(combine_w);
+  ALIGNED(gap);
+  return hip_status(dmoe::launch_block_topk(probs, n_blocks, block_size, E, k, block_scores,
+                                            block_experts, combine_w, gap,
+                                            static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
+dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* token_experts,
+                            float* combine_w, float* gap, void* stream) {
+  REQUIRE(probs && token_experts && combine_w, "probs, token_experts and combine_w must not be NULL");
+  REQUIRE(T >= 1, "T=%d must be >= 1", T);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(static_cast<long>(T) * E <= kIntLimit, "T*E must fit in int32");
+  ALIGNED(probs);
+  ALIGNED(token_experts);
+  ALIGNED(combine_w);
+  ALIGNED(gap);
+  return hip_status(dmoe::launch_token_topk(probs, T, E, k, token_experts, combine_w, gap,
+                                            static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
+dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int group_size, int k,
+                                       int E, dmoe_schedule sched, void* stream) {
+  REQUIRE(experts, "experts must not be NULL");
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+          "every schedule array must be set");
+  REQUIRE(n_groups >= 1 && group_size >= 1, "n_groups=%d and group_size=%d must be >= 1", n_groups,
+          group_size);
+  REQUIRE(E >= 1, "E=%d must be >= 1", E);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(static_cast<long>(n_groups) * group_size * k < kIntLimit, "n_groups*group_size*k must fit in int32");
+  SUPPORT(E <= kMaxScheduleE, "the schedule supports E <= %d (E=%d)", kMaxScheduleE, E);
+  ALIGNED(experts);
+  ALIGNED(sched.n_unique);
+  ALIGNED(sched.unique);
+  ALIGNED(sched.offsets);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
+  return hip_status(dmoe::launch_schedule(experts, n_groups, group_size, k, E, sched,
+                                          static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
+size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
+  if (T < 1 || I < 1 || I_s < 0 || k < 1 || !valid_dtype(dt)) return 0;
+  return dmoe::ffn_hbuf_bytes(T, I, I_s, k, dt);
+}
+
+dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up, const void* w_down,
+                            const void* ws_gate, const void* ws_up, const void* ws_down,
+                            dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
+                            int max_unique, dmoe_schedule sched, float* slot_out,
+                            float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
+  REQUIRE(x && w_gate && w_up && w_down && slot_out && workspace,
+          "x, w_gate, w_up, w_down, slot_out and workspace must not be NULL");
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+          "every schedule array must be set");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1 && I >= 1 && I_s >= 0, "T=%d, H=%d, I=%d must be >= 1 and I_s=%d >= 0",
+          T, H, I, I_s);
+  REQUIRE(E >= 1, "E=%d must be >= 1", E);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(max_unique >= 1 && max_unique <= E, "max_unique=%d must be in [1, E]", max_unique);
+  const bool shared = I_s > 0;
+  REQUIRE(shared == (ws_gate != nullptr) && shared == (ws_up != nullptr) &&
+              shared == (ws_down != nullptr) && shared == (shared_out != nullptr),
+          "ws_gate, ws_up, ws_down and shared_out must all be set iff I_s > 0");
+  REQUIRE(static_cast<long>(T) * k * H <= kIntLimit * 4L && static_cast<long>(T) * (k + 1) < kIntLimit,
+          "T*k*H is too large");
+  const size_t need = dmoe::ffn_hbuf_bytes(T, I, I_s, k, dt);
+  REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
+  ALIGNED(x);
+  ALIGNED(w_gate);
+  ALIGNED(w_up);
+  ALIGNED(w_down);
+  ALIGNED(ws_gate);
+  ALIGNED(ws_up);
+  ALIGNED(ws_down);
+  ALIGNED(slot_out);
+  ALIGNED(shared_out);
+  ALIGNED(workspace);
+  SUPPORT(E <= kMaxScheduleE, "E <= %d is supported (E=%d)", kMaxScheduleE, E);
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
+            "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
+  }
+  dmoe::FfnArgs a{x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, T, H, E, I, I_s, k, max_unique,
+                  sched, slot_out, shared_out, workspace};
+  return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
+}
+
+dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const float* shared_out,
+                         dmoe_dtype dt, int T, int H, int k, void* y, void* stream) {
+  REQUIRE(slot_out && combine_w && y, "slot_out, combine_w and y must not be NULL");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
+  REQUIRE(H % 4 == 0, "H=%d must be a multiple of 4", H);
+  REQUIRE(k >= 1 && k <= kMaxK, "k=%d must be in [1, %d]", k, kMaxK);
+  ALIGNED(slot_out);
+  ALIGNED(combine_w);
+  ALIGNED(shared_out);
+  ALIGNED(y);
+  return hip_status(dmoe::launch_combine(slot_out, combine_w, shared_out, dt, T, H, k, y,
+                                         static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
+}  // extern "C"

@@ -1,0 +1,88 @@
+// Internal declarations shared by the host validation layer and the gfx950
+// kernels of libdmoe.  Not part of the public ABI (see include/dmoe.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "dmoe.h"
+
+namespace dmoe {
+
+// ---------------------------------------------------------------------------
+// Element types
+// ---------------------------------------------------------------------------
+typedef uint16_t bf16_t;  // bfloat16 storage: the upper 16 bits of a binary32
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v) << 16);
+}
+
+// Round-to-nearest-even binary32 -> bfloat16 (NaN stays a quiet NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return static_cast<bf16_t>((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float load_as_f32(const T* p);
+template <>
+__device__ __forceinline__ float load_as_f32<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_as_f32<bf16_t>(const bf16_t* p) { return bf16_to_f32(*p); }
+
+template <typename T>
+__device__ __forceinline__ void store_from_f32(T* p, float v);
+template <>
+__device__ __forceinline__ void store_from_f32<float>(float* p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void store_from_f32<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+
+// 16-byte load of eight bfloat16 values as an MFMA operand.
+__device__ __forceinline__ bf16x8 ld_bf16x8(const bf16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(p));
+}
+
+__device__ __forceinline__ float silu_f32(float a) { return a / (1.0f + expf(-a)); }
+
+constexpr int kWave = 64;  // CDNA wavefront width
+
+// ---------------------------------------------------------------------------
+// Host-side launchers (one per kernel family; arguments already validated)
+// ---------------------------------------------------------------------------
+hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
+                         int H, int E, float* logits, float* probs, hipStream_t s);
+hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, float* scores,
+                             int32_t* experts, float* w, float* gap, hipStream_t s);
+hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* experts, float* w,
+                             float* gap, hipStream_t s);
+hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, int E,
+                           dmoe_schedule sched, hipStream_t s);
+
+struct FfnArgs {
+  const void* x;
+  const void* wg;
+  const void* wu;
+  const void* wd;
+  const void* wsg;
+  const void* wsu;
+  const void* wsd;
+  int T, H, E, I, I_s, k, max_unique;
+  dmoe_schedule sched;
+  float* slot_out;
+  float* shared_out;
+  void* hbuf;  // SwiGLU activations [T*k + T][max(I, I_s)] of the storage type
+};
+hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
+size_t ffn_hbuf_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
+
+hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
+                          dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);
+
+}  // namespace dmoe

@@ -1,0 +1,82 @@
+"""One MoE layer forward as the chain of libdmoe entry points.
+
+:class:`MoELayer` owns the device buffers of one layer shape and enqueues
+
+    dmoe_router_logits -> dmoe_block_aggregate_topk | dmoe_token_topk
+    -> dmoe_build_expert_schedule -> dmoe_expert_ffn -> dmoe_combine
+
+on the current stream.  It allocates only in its constructor, so a forward
+can be captured in a HIP graph.  Nothing is computed on the host.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import lib
+
+
+class MoELayer:
+    def __init__(self, H: int, E: int, I: int, I_s: int, k: int, n_blocks: int, block_size: int,
+                 dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False):
+        self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
+        self.NB, self.bs = n_blocks, block_size
+        self.T = T = n_blocks * block_size
+        self.dtype = dtype
+        f32 = dict(dtype=torch.float32, device=device)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.logits = torch.empty((T, E), **f32) if keep_logits else None
+        self.probs = torch.empty((T, E), **f32)
+        self.block_scores = torch.empty((n_blocks, E), **f32)
+        self.block_experts = torch.empty((n_blocks, k), **i32)
+        self.block_gap = torch.empty((n_blocks,), **f32)
+        self.token_experts = torch.empty((T, k), **i32)
+        self.token_gap = torch.empty((T,), **f32)
+        self.combine_w = torch.empty((T, k), **f32)
+        self.sched = lib.Schedule.empty(E, T * k, device)
+        self.slot_out = torch.empty((T, k, H), **f32)
+        self.shared_out = torch.empty((T, H), **f32) if I_s > 0 else None
+        dt = lib.DMOE_F32 if dtype == torch.float32 else lib.DMOE_BF16
+        nbytes = lib.dmoe_ffn_workspace_size(T, I, I_s, k, dt)
+        self.workspace = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=device)
+        self.y = torch.empty((T, H), dtype=dtype, device=device)
+
+    def max_unique(self, routing: str) -> int:
+        groups = self.NB if routing == "block" else self.T
+        return min(self.E, groups * self.k)
+
+    def route(self, x, w_router, bias=None, routing: str = "block", stream=None):
+        T, H, E, k = self.T, self.H, self.E, self.k
+        lib.dmoe_router_logits(x, w_router, bias, T, H, E, self.logits, self.probs, stream)
+        if routing == "block":
+            lib.dmoe_block_aggregate_topk(self.probs, self.NB, self.bs, E, k, self.block_scores,
+                                          self.block_experts, self.combine_w, self.block_gap, stream)
+            lib.dmoe_build_expert_schedule(self.block_experts, self.NB, self.bs, k, E, self.sched, stream)
+        elif routing == "token":
+            lib.dmoe_token_topk(self.probs, T, E, k, self.token_experts, self.combine_w, self.token_gap,
+                                stream)
+            lib.dmoe_build_expert_schedule(self.token_experts, T, 1, k, E, self.sched, stream)
+        else:
+            raise ValueError(f"routing must be 'block' or 'token', not {routing!r}")
+
+    def experts_ffn(self, x, w: dict, routing: str = "block", stream=None):
+        lib.dmoe_expert_ffn(x, w["w_gate"], w["w_up"], w["w_down"], w.get("ws_gate"), w.get("ws_up"),
+                            w.get("ws_down"), self.T, self.H, self.E, self.I, self.I_s, self.k,
+                            self.max_unique(routing), self.sched, self.slot_out, self.shared_out,
+                            self.workspace, stream)
+
+    def combine(self, stream=None):
+        lib.dmoe_combine(self.slot_out, self.combine_w, self.shared_out, self.T, self.H, self.k, self.y,
+                         stream)
+
+    def forward(self, x, w: dict, routing: str = "block", stream=None) -> torch.Tensor:
+        """Whole layer on hidden states x[T, H]; returns (a view of) y[T, H]."""
+        self.route(x, w["w_router"], w.get("bias"), routing, stream)
+        self.experts_ffn(x, w, routing, stream)
+        self.combine(stream)
+        return self.y
+
+    def experts(self, routing: str) -> torch.Tensor:
+        return self.block_experts if routing == "block" else self.token_experts
+
+    def gaps(self, routing: str) -> torch.Tensor:
+        return self.block_gap if routing == "block" else self.token_gap

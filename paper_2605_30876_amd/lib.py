@@ -1,0 +1,171 @@
+"""Thin ctypes binding of libdmoe (include/dmoe.h).
+
+Each ``dmoe_*`` function here has the name and argument order of the C entry
+point it wraps.  It only marshals arguments: torch tensors become device
+pointers, the current torch stream becomes the hipStream_t, and a non-OK
+status raises :class:`DmoeError`.  Every step of the MoE layer runs in the
+library's HIP kernels; torch only provides device memory and streams.
+
+The library is loaded from this package directory (built by
+``python -m paper_2605_30876_amd.build``).  There is no fallback: when the
+library is missing, :func:`load` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdmoe.so")
+
+DMOE_OK, DMOE_ERR_INVALID_ARG, DMOE_ERR_UNSUPPORTED, DMOE_ERR_HIP = 0, -1, -2, -3
+DMOE_F32, DMOE_BF16 = 0, 1
+
+STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG",
+                DMOE_ERR_UNSUPPORTED: "DMOE_ERR_UNSUPPORTED", DMOE_ERR_HIP: "DMOE_ERR_HIP"}
+
+# Every symbol include/dmoe.h declares.
+EXPORTS = ("dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
+           "dmoe_build_expert_schedule", "dmoe_ffn_workspace_size", "dmoe_expert_ffn",
+           "dmoe_combine", "dmoe_last_error", "dmoe_version")
+
+
+class DmoeError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class dmoe_schedule(ctypes.Structure):
+    _fields_ = [("n_unique", ctypes.c_void_p), ("unique", ctypes.c_void_p),
+                ("offsets", ctypes.c_void_p), ("row_token", ctypes.c_void_p),
+                ("row_slot", ctypes.c_void_p)]
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_S = ctypes.c_size_t
+_SIGS = {
+    "dmoe_router_logits": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
+    "dmoe_block_aggregate_topk": ([_P, _I, _I, _I, _I, _P, _P, _P, _P, _P], _I),
+    "dmoe_token_topk": ([_P, _I, _I, _I, _P, _P, _P, _P], _I),
+    "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
+    "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
+    "dmoe_expert_ffn": ([_P] * 7 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
+    "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
+    "dmoe_last_error": ([], ctypes.c_char_p),
+    "dmoe_version": ([], ctypes.c_char_p),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libdmoe (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libdmoe is not built ({path} is missing); run "
+                           f"'python -m paper_2605_30876_amd.build' first")
+    lib = ctypes.CDLL(path)
+    for name, (args, res) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != DMOE_OK:
+        raise DmoeError(status, load().dmoe_last_error().decode())
+
+
+def ptr(t) -> int | None:
+    """Device pointer of a tensor (None for None)."""
+    return None if t is None else t.data_ptr()
+
+
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return DMOE_F32
+    if t.dtype == torch.bfloat16:
+        return DMOE_BF16
+    raise TypeError(f"unsupported element type {t.dtype}")
+
+
+def stream_handle(stream=None) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# Entry points (same names and argument order as include/dmoe.h)
+# ---------------------------------------------------------------------------
+
+
+def dmoe_router_logits(x, w_router, bias, T, H, E, logits, probs, stream=None):
+    _check(load().dmoe_router_logits(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), T, H, E,
+                                     ptr(logits), ptr(probs), stream_handle(stream)))
+
+
+def dmoe_block_aggregate_topk(probs, n_blocks, block_size, E, k, block_scores, block_experts,
+                              combine_w, gap, stream=None):
+    _check(load().dmoe_block_aggregate_topk(ptr(probs), n_blocks, block_size, E, k, ptr(block_scores),
+                                            ptr(block_experts), ptr(combine_w), ptr(gap),
+                                            stream_handle(stream)))
+
+
+def dmoe_token_topk(probs, T, E, k, token_experts, combine_w, gap, stream=None):
+    _check(load().dmoe_token_topk(ptr(probs), T, E, k, ptr(token_experts), ptr(combine_w), ptr(gap),
+                                  stream_handle(stream)))
+
+
+@dataclass
+class Schedule:
+    """Device arrays of a dmoe_schedule (int32 torch tensors)."""
+    n_unique: torch.Tensor
+    unique: torch.Tensor
+    offsets: torch.Tensor
+    row_token: torch.Tensor
+    row_slot: torch.Tensor
+
+    @staticmethod
+    def empty(E: int, n_rows: int, device) -> "Schedule":
+        z = lambda n: torch.zeros(max(n, 4), dtype=torch.int32, device=device)  # noqa: E731
+        return Schedule(z(1), z(E), z(E + 1), z(n_rows), z(n_rows))
+
+    def as_c(self) -> dmoe_schedule:
+        return dmoe_schedule(ptr(self.n_unique), ptr(self.unique), ptr(self.offsets),
+                             ptr(self.row_token), ptr(self.row_slot))
+
+
+def dmoe_build_expert_schedule(experts, n_groups, group_size, k, E, sched: Schedule, stream=None):
+    _check(load().dmoe_build_expert_schedule(ptr(experts), n_groups, group_size, k, E, sched.as_c(),
+                                             stream_handle(stream)))
+
+
+def dmoe_ffn_workspace_size(T, I, I_s, k, dt) -> int:
+    return int(load().dmoe_ffn_workspace_size(T, I, I_s, k, dt))
+
+
+def dmoe_expert_ffn(x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, T, H, E, I, I_s, k,
+                    max_unique, sched: Schedule, slot_out, shared_out, workspace, stream=None):
+    _check(load().dmoe_expert_ffn(ptr(x), ptr(w_gate), ptr(w_up), ptr(w_down), ptr(ws_gate),
+                                  ptr(ws_up), ptr(ws_down), dtype_code(x), T, H, E, I, I_s, k,
+                                  max_unique, sched.as_c(), ptr(slot_out), ptr(shared_out),
+                                  ptr(workspace), workspace.numel() * workspace.element_size(),
+                                  stream_handle(stream)))
+
+
+def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):
+    _check(load().dmoe_combine(ptr(slot_out), ptr(combine_w), ptr(shared_out), dtype_code(y), T, H,
+                               k, ptr(y), stream_handle(stream)))
+
+
+def dmoe_version() -> str:
+    return load().dmoe_version().decode()

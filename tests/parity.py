@@ -1,0 +1,140 @@
+"""Parity helpers: run the HIP path and the oracle on the same seeded inputs
+and compare them.
+
+Expected values come from the oracle only.  Where a routing decision is a
+near-tie (the oracle's gap below ``NEAR_TIE``), several expert sets are
+correct; the oracle enumerates them, the GPU's set must be one of them, and
+the expected weights, schedule and output use that oracle-enumerated set.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import oracle as O
+
+BF16_TOL = 2e-2   # max|y - y_ref| <= 2e-2 * RMS(y_ref) for bf16 weights
+F32_TOL = 1e-4    # ... <= 1e-4 * RMS(y_ref) for the fp32 layer
+PROB_TOL = 1e-6   # router probabilities, combine weights, block scores, gaps (absolute)
+
+
+def tol_for(cfg) -> float:
+    return F32_TOL if cfg.dtype == "f32" else BF16_TOL
+
+
+def cpu(t):
+    return None if t is None else t.detach().to("cpu")
+
+
+def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: list, what: str):
+    """Per group: the oracle's own top-k list, or (near-tie) the oracle-valid
+    set that the GPU picked, ranked by the oracle's scores."""
+    out = np.zeros((scores.shape[0], k), dtype=np.int32)
+    for g in range(scores.shape[0]):
+        idx, gap = O.topk(scores[g], k)
+        if gap >= O.NEAR_TIE:
+            assert set(gpu_sel[g].tolist()) == set(idx.tolist()), (
+                f"{what} group {g}: GPU set {sorted(gpu_sel[g].tolist())} != oracle {sorted(idx.tolist())}"
+                f" (gap {gap:.3g})")
+            out[g] = idx
+        else:
+            cands = O.valid_topk_sets(scores[g], k)
+            gs = frozenset(gpu_sel[g].tolist())
+            assert gs in cands, f"{what} group {g}: near-tie but GPU set {sorted(gs)} is not a valid top-{k}"
+            order = O.ranked(scores[g])
+            out[g] = [e for e in order if e in gs][:k]
+            log.append({"what": what, "group": g, "gap": float(gap), "oracle": sorted(idx.tolist()),
+                        "gpu": sorted(gs)})
+    return out
+
+
+def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, check_determinism=True):
+    """Run the GPU forward on d_gpu, compare with the oracle, return a report."""
+    x = d_gpu["x"]
+    y = layer.forward(x, d_gpu, routing).clone()
+    torch.cuda.synchronize()
+    report = {"near_ties": []}
+
+    # ---- routing --------------------------------------------------------
+    z = O.router_logits(x, d_gpu["w_router"], d_gpu.get("bias"))
+    p = O.softmax_rows(z)
+    p_gpu = cpu(layer.probs).numpy()
+    perr = float(np.max(np.abs(p_gpu - p)))
+    assert perr <= PROB_TOL, f"router probabilities differ by {perr:.3g}"
+    report["prob_err"] = perr
+
+    k = cfg.k
+    sel_gpu = cpu(layer.experts(routing)).numpy()
+    gap_gpu = cpu(layer.gaps(routing)).numpy()
+    w_gpu = cpu(layer.combine_w).numpy()
+    if routing == "block":
+        S = O.block_scores(p, cfg.bs)
+        S_gpu = cpu(layer.block_scores).numpy()
+        serr = float(np.max(np.abs(S_gpu - S)))
+        assert serr <= PROB_TOL, f"block scores differ by {serr:.3g}"
+        scores = S
+        sel = accepted_selection(S, sel_gpu, k, report["near_ties"], "block")
+        ept = O.expand_block_experts(sel, cfg.bs)
+        gs = cfg.bs
+    else:
+        scores = p
+        sel = accepted_selection(p, sel_gpu, k, report["near_ties"], "token")
+        ept = sel
+        gs = 1
+    # gaps (groups that are not near-ties)
+    for g in range(scores.shape[0]):
+        _, gap = O.topk(scores[g], k)
+        if gap >= O.NEAR_TIE and math.isfinite(gap):
+            assert abs(gap_gpu[g] - gap) <= PROB_TOL, f"gap of group {g}: {gap_gpu[g]} vs {gap}"
+        elif not math.isfinite(gap):
+            assert not math.isfinite(gap_gpu[g])
+    # GPU lists are in (score desc) order of the oracle scores, up to near-ties
+    for g in range(sel_gpu.shape[0]):
+        sc = scores[g][sel_gpu[g]]
+        assert np.all(sc[:-1] >= sc[1:] - O.NEAR_TIE), f"group {g} not in descending score order"
+    # combine weights, compared per (token, expert)
+    werr = 0.0
+    ept_gpu = O.expand_block_experts(sel_gpu, gs) if routing == "block" else sel_gpu
+    for t in range(cfg.T):
+        w_ref = O.renormalised_weights(p[t], ept[t])
+        ref = dict(zip(ept[t].tolist(), w_ref.tolist()))
+        got = dict(zip(ept_gpu[t].tolist(), w_gpu[t].tolist()))
+        assert ref.keys() == got.keys()
+        werr = max(werr, max(abs(ref[e] - got[e]) for e in ref))
+    assert werr <= PROB_TOL, f"combine weights differ by {werr:.3g}"
+    report["w_err"] = werr
+
+    # ---- schedule -------------------------------------------------------
+    uniq = O.unique_experts(sel)
+    n_u = int(cpu(layer.sched.n_unique)[0])
+    assert n_u == uniq.size, f"n_unique {n_u} != {uniq.size}"
+    assert cpu(layer.sched.unique)[:n_u].numpy().tolist() == uniq.tolist()
+    offs = cpu(layer.sched.offsets).numpy()
+    rt = cpu(layer.sched.row_token).numpy()
+    rs = cpu(layer.sched.row_slot).numpy()
+    rows = O.expert_rows(sel, gs)
+    for u, e in enumerate(uniq.tolist()):
+        got = list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist()))
+        assert got == rows[e], f"rows of expert {e} differ"
+    assert offs[n_u] == cfg.T * k
+    report["n_unique"] = n_u
+
+    # ---- layer output ---------------------------------------------------
+    w_acc = np.stack([O.renormalised_weights(p[t], ept[t]) for t in range(cfg.T)])
+    toks = None if sample_tokens is None else np.asarray(sample_tokens)
+    y_ref = O.combine(x, ept, w_acc, d_gpu["w_gate"], d_gpu["w_up"], d_gpu["w_down"],
+                      d_gpu.get("ws_gate"), d_gpu.get("ws_up"), d_gpu.get("ws_down"), tokens=toks)
+    y_got = cpu(y).float().numpy().astype(np.float64)
+    if toks is not None:
+        y_got = y_got[toks]
+    err = O.max_rel_err(y_got, y_ref)
+    report["y_err_rms"] = err
+    assert err <= tol_for(cfg), f"max|y - y_ref| = {err:.3g} * RMS(y_ref) > {tol_for(cfg)}"
+
+    if check_determinism:
+        y2 = layer.forward(x, d_gpu, routing).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2), "two runs differ bitwise"
+    return report

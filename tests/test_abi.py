@@ -1,0 +1,166 @@
+"""CPU checks of the C ABI: the library loads, exports every function
+include/dmoe.h declares, and rejects invalid arguments on the host with the
+documented status before launching anything."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2605_30876_amd import lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dmoe.h")
+
+# These calls pass host addresses as "device" pointers; validation must reject
+# them before any launch.  Never run them where a GPU could execute a launch.
+pytestmark = pytest.mark.skipif(torch.cuda.is_available(), reason="host-validation tests run without a GPU")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(dmoe_[a-z_0-9]+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = lib.load()
+    out = subprocess.run(["nm", "-D", "--defined-only", lib.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\sT\s(dmoe_[a-z_0-9]+)$", out, flags=re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(L, name) is not None
+    assert lib.dmoe_version() == "0.1.0"
+
+
+@pytest.fixture(scope="module")
+def L():
+    return lib.load()
+
+
+@pytest.fixture(scope="module")
+def buf():
+    # 16-byte aligned host buffer standing in for device memory (never dereferenced)
+    a = np.zeros(4096, dtype=np.float32)
+    base = a.ctypes.data
+    assert base % 16 == 0
+    return a, base
+
+
+def status(L, name, *args):
+    st = getattr(L, name)(*args)
+    return st, L.dmoe_last_error().decode()
+
+
+def test_router_validation(L, buf):
+    _, p = buf
+    st, msg = status(L, "dmoe_router_logits", None, p, None, 1, 32, 2048, 256, None, p, None)
+    assert st == lib.DMOE_ERR_INVALID_ARG and "must not be NULL" in msg
+    assert status(L, "dmoe_router_logits", p, p, None, 7, 32, 2048, 256, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 0, 2048, 256, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 5000, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p + 4, p, None, 1, 32, 2048, 256, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    st, msg = status(L, "dmoe_router_logits", p, p, None, 1, 32, 2000, 256, None, p, None)
+    assert st == lib.DMOE_ERR_UNSUPPORTED and "H % 128" in msg
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 250, None, p, None)[0] == lib.DMOE_ERR_UNSUPPORTED
+
+
+def test_topk_validation(L, buf):
+    _, p = buf
+    bt = "dmoe_block_aggregate_topk"
+    # k > E, k > 64, k < 1, bad block size, NULL output
+    assert status(L, bt, p, 1, 32, 8, 9, None, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, bt, p, 1, 32, 256, 65, None, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, bt, p, 1, 32, 256, 0, None, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, bt, p, 1, 0, 256, 8, None, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, bt, p, 0, 32, 256, 8, None, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, bt, p, 1, 32, 256, 8, None, None, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, bt, p, 1, 32, 256, 8, p + 8, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    tt = "dmoe_token_topk"
+    assert status(L, tt, p, 32, 256, 0, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, tt, p, 0, 256, 8, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, tt, p, 32, 4, 8, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, tt, None, 32, 256, 8, p, p, None, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, tt, p, 32, 256, 8, p, p, p + 4, None)[0] == lib.DMOE_ERR_INVALID_ARG
+
+
+def _sched(p, bad=None):
+    s = lib.dmoe_schedule(p, p, p, p, p)
+    if bad:
+        setattr(s, bad, None)
+    return s
+
+
+def test_schedule_validation(L, buf):
+    _, p = buf
+    f = "dmoe_build_expert_schedule"
+    for field in ("n_unique", "unique", "offsets", "row_token", "row_slot"):
+        assert status(L, f, p, 1, 32, 8, 256, _sched(p, field), None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, None, 1, 32, 8, 256, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, 0, 32, 8, 256, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, 1, 0, 8, 256, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, 1, 32, 9, 8, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, 2**20, 2**10, 8, 256, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
+    st, msg = status(L, f, p, 1, 32, 8, 1024, _sched(p), None)
+    assert st == lib.DMOE_ERR_UNSUPPORTED and "E <= 512" in msg
+
+
+def _ffn(L, p, **over):
+    a = dict(x=p, wg=p, wu=p, wd=p, wsg=p, wsu=p, wsd=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512,
+             I_s=512, k=8, max_unique=8, sched=lib.dmoe_schedule(p, p, p, p, p), slot=p, shared=p, ws=p,
+             ws_bytes=1 << 30)
+    a.update(over)
+    return status(L, "dmoe_expert_ffn", a["x"], a["wg"], a["wu"], a["wd"], a["wsg"], a["wsu"], a["wsd"],
+                  a["dt"], a["T"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_unique"], a["sched"],
+                  a["slot"], a["shared"], a["ws"], a["ws_bytes"], None)
+
+
+def test_ffn_validation(L, buf):
+    _, p = buf
+    INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    assert _ffn(L, p, x=None)[0] == INV
+    assert _ffn(L, p, ws=None)[0] == INV
+    assert _ffn(L, p, dt=5)[0] == INV
+    assert _ffn(L, p, k=0)[0] == INV
+    assert _ffn(L, p, max_unique=0)[0] == INV
+    assert _ffn(L, p, max_unique=257)[0] == INV
+    assert _ffn(L, p, wsd=None)[0] == INV            # shared triple inconsistent
+    assert _ffn(L, p, shared=None)[0] == INV
+    assert _ffn(L, p, I_s=0)[0] == INV               # shared pointers set without a shared expert
+    st, msg = _ffn(L, p, ws_bytes=100)
+    assert st == INV and "workspace" in msg
+    assert _ffn(L, p, slot=p + 4)[0] == INV
+    assert _ffn(L, p, sched=lib.dmoe_schedule(p, None, p, p, p))[0] == INV
+    assert _ffn(L, p, H=2000)[0] == UNS
+    assert _ffn(L, p, I=500)[0] == UNS
+    assert _ffn(L, p, E=1024, max_unique=8)[0] == UNS
+
+
+def test_combine_validation(L, buf):
+    _, p = buf
+    f = "dmoe_combine"
+    assert status(L, f, None, p, None, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, p, None, 1, 32, 2046, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, p, None, 1, 32, 2048, 65, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, p, None, 9, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, p, p + 4, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+
+
+def test_workspace_size():
+    assert lib.dmoe_ffn_workspace_size(32, 512, 512, 8, lib.DMOE_BF16) == (32 * 8 + 32) * 512 * 2
+    assert lib.dmoe_ffn_workspace_size(8, 128, 0, 2, lib.DMOE_F32) == 8 * 2 * 128 * 4
+    assert lib.dmoe_ffn_workspace_size(0, 128, 0, 2, lib.DMOE_F32) == 0
+    assert lib.dmoe_ffn_workspace_size(8, 128, 0, 2, 7) == 0
+
+
+def test_last_error_cleared_per_thread(L, buf):
+    _, p = buf
+    L.dmoe_combine(None, p, None, 1, 32, 2048, 8, p, None)
+    assert L.dmoe_last_error().decode().startswith("dmoe_combine")

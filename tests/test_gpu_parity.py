@@ -1,0 +1,137 @@
+"""GPU parity of the whole layer forward (block and token routing) against
+the CPU oracle, through the C ABI.  Marked ``gpu``."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from dmoe_synth import get_config, make_inputs
+from paper_2605_30876_amd import lib
+from paper_2605_30876_amd.layer import MoELayer
+from parity import run_and_check
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer(cfg):
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    return MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt, device="cuda")
+
+
+def _to_gpu(d):
+    return {k: (None if v is None else v.cuda()) for k, v in d.items()}
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+SMALL = ["tiny_f32", "small_f32", "small_bf16", "small_bf16_zipf", "small_bf16_corr"]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("name", SMALL)
+def test_small_layer_parity(gpu_lib, name, routing, seed):
+    cfg = get_config(name)
+    _say("case", name, routing, seed)
+    d = _to_gpu(make_inputs(cfg, seed))
+    rep = run_and_check(cfg, d, routing, _layer(cfg))
+    _say("  ", rep)
+
+
+# Full-size layers: routing and schedule are checked on every token, the
+# output on a sample of tokens the oracle computes one by one.
+FULL = {"decode_b1": None, "decode_b16": [0, 1, 31, 32, 250, 511], "large_zipf_b8": [0, 77, 255],
+        "corr_b64x64": [0, 63, 64, 2047, 4095]}
+
+
+@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("name", list(FULL))
+def test_full_size_parity(gpu_lib, name, routing):
+    cfg = get_config(name)
+    _say("case", name, routing)
+    d = make_inputs(cfg, seed=0, device="cuda")
+    rep = run_and_check(cfg, d, routing, _layer(cfg), sample_tokens=FULL[name],
+                        check_determinism=(name == "decode_b1"))
+    _say("  ", {k: v for k, v in rep.items() if k != "near_ties"}, "near_ties:", len(rep["near_ties"]))
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "small_f32"])
+def test_block_size_one_equals_token_routing(gpu_lib, name):
+    base = get_config(name)
+    cfg = base.with_(name=base.name + "_bs1", NB=base.T if base.T <= 64 else 37, bs=1)
+    d = _to_gpu(make_inputs(cfg, seed=5))
+    layer = _layer(cfg)
+    yb = layer.forward(d["x"], d, "block").clone()
+    eb = layer.block_experts.clone()
+    yt = layer.forward(d["x"], d, "token").clone()
+    torch.cuda.synchronize()
+    assert torch.equal(eb, layer.token_experts)
+    assert torch.equal(yb, yt)
+    run_and_check(cfg, d, "block", layer)
+
+
+@pytest.mark.parametrize("routing", ["block", "token"])
+def test_k_equals_E(gpu_lib, routing):
+    cfg = get_config("small_bf16").with_(name="kE", E=32, k=32, NB=2, bs=24)
+    d = _to_gpu(make_inputs(cfg, seed=1))
+    rep = run_and_check(cfg, d, routing, _layer(cfg))
+    assert rep["n_unique"] == 32
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_single_token(gpu_lib, dtype):
+    base = get_config("small_bf16" if dtype == "bf16" else "small_f32")
+    cfg = base.with_(name=base.name + "_t1", NB=1, bs=1)
+    d = _to_gpu(make_inputs(cfg, seed=2))
+    for routing in ("block", "token"):
+        run_and_check(cfg, d, routing, _layer(cfg))
+
+
+def test_single_expert_f32(gpu_lib):
+    cfg = get_config("small_f32").with_(name="e1", E=1, k=1)
+    d = _to_gpu(make_inputs(cfg, seed=3))
+    rep = run_and_check(cfg, d, "block", _layer(cfg))
+    assert rep["n_unique"] == 1
+
+
+def test_k_one_bf16(gpu_lib):
+    cfg = get_config("small_bf16").with_(name="k1", k=1)
+    d = _to_gpu(make_inputs(cfg, seed=4))
+    for routing in ("block", "token"):
+        run_and_check(cfg, d, routing, _layer(cfg))
+
+
+@pytest.mark.parametrize("n_groups,gs,k,E", [(1, 32, 8, 256), (16, 32, 8, 256), (4096, 1, 8, 256),
+                                             (64, 64, 8, 256), (3, 5, 3, 7), (300, 1, 4, 512),
+                                             (40, 2, 1, 1)])
+def test_schedule_against_oracle(gpu_lib, n_groups, gs, k, E):
+    rng = np.random.default_rng(n_groups * 7 + k)
+    # a skewed draw so that some experts are shared by many groups
+    pop = rng.zipf(1.3, size=E).astype(np.float64)
+    pop /= pop.sum()
+    ex = np.stack([rng.choice(E, size=k, replace=False, p=pop) for _ in range(n_groups)]).astype(np.int32)
+    sched = lib.Schedule.empty(E, n_groups * gs * k, "cuda")
+    lib.dmoe_build_expert_schedule(torch.from_numpy(ex).cuda(), n_groups, gs, k, E, sched)
+    torch.cuda.synchronize()
+    uniq = O.unique_experts(ex)
+    rows = O.expert_rows(ex, gs)
+    n = int(sched.n_unique[0])
+    assert n == uniq.size
+    assert sched.unique[:n].cpu().tolist() == uniq.tolist()
+    offs = sched.offsets.cpu().numpy()
+    rt, rs = sched.row_token.cpu().numpy(), sched.row_slot.cpu().numpy()
+    for u, e in enumerate(uniq.tolist()):
+        assert list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist())) == rows[e]
+    assert offs[n] == n_groups * gs * k
+
+
+def test_error_status_on_gpu(gpu_lib):
+    cfg = get_config("small_bf16")
+    layer = _layer(cfg)
+    with pytest.raises(lib.DmoeError) as ei:
+        lib.dmoe_token_topk(layer.probs, cfg.T, cfg.E, cfg.E + 1, layer.token_experts, layer.combine_w, None)
+    assert ei.value.status == lib.DMOE_ERR_INVALID_ARG
