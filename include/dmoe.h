@@ -95,8 +95,8 @@ typedef struct dmoe_schedule {
  *   probs[t][:]  = softmax(logits[t][:]) over all E experts (max-subtracted)
  * x [T][H] and w_router [E][H] of type dt; bias [E] float32 or NULL (no bias);
  * logits [T][E] float32 or NULL (not stored); probs [T][E] float32.
- * Limits: T >= 1; 1 <= E <= 4096; H >= 1.  For DMOE_BF16: H % 128 == 0 and
- * E % 32 == 0 (matrix-core tiles); DMOE_F32 has no further limit.
+ * Limits: T >= 1; 1 <= E <= 4096; H >= 1.  For DMOE_BF16: H % 128 == 0
+ * (matrix-core tiles); DMOE_F32 has no further limit.
  */
 dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
                                dmoe_dtype dt, int T, int H, int E,

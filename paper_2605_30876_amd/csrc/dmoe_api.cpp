@@ -74,7 +74,6 @@ dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float*
   ALIGNED(probs);
   if (dt == DMOE_BF16) {
     SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
-    SUPPORT(E % 32 == 0, "bf16 router needs E %% 32 == 0 (E=%d)", E);
   }
   return hip_status(dmoe::launch_router(x, w_router, bias, dt, T, H, E, logits, probs,
                                         static_cast<hipStream_t>(stream)),

@@ -32,9 +32,11 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
   const bf16_t* pb[2];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    int t = min(t0 + r * 16 + c, T - 1);  // ragged token tail: clamp reads, skip writes
+    // ragged token / expert tails: clamp the rows read, skip the writes
+    const int t = min(t0 + r * 16 + c, T - 1);
+    const int e = min(e0 + r * 16 + c, E - 1);
     pa[r] = x + static_cast<size_t>(t) * H + kbeg + q * 8;
-    pb[r] = w + static_cast<size_t>(e0 + r * 16 + c) * H + kbeg + q * 8;
+    pb[r] = w + static_cast<size_t>(e) * H + kbeg + q * 8;
   }
   f32x4 acc[2][2];
 #pragma unroll
@@ -68,6 +70,7 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
 #pragma unroll
       for (int ww = 0; ww < 3; ++ww) v += red[ww][r * 2 + s][lane];
       const int e = e0 + s * 16 + c;
+      if (e >= E) continue;
       const float b = bias ? bias[e] : 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -125,7 +128,7 @@ hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_d
                          int H, int E, float* logits, float* probs, hipStream_t s) {
   float* z = logits ? logits : probs;
   if (dt == DMOE_BF16) {
-    dim3 grid((T + kRouterTile - 1) / kRouterTile, E / kRouterTile);
+    dim3 grid((T + kRouterTile - 1) / kRouterTile, (E + kRouterTile - 1) / kRouterTile);
     router_logits_bf16_kernel<<<grid, 256, 0, s>>>(static_cast<const bf16_t*>(x),
                                                     static_cast<const bf16_t*>(w), bias, T, H, E, z);
   } else {

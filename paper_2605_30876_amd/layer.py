@@ -17,7 +17,8 @@ from . import lib
 
 class MoELayer:
     def __init__(self, H: int, E: int, I: int, I_s: int, k: int, n_blocks: int, block_size: int,
-                 dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False):
+                 dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False,
+                 out_dtype: torch.dtype = torch.float32):
         self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
         self.NB, self.bs = n_blocks, block_size
         self.T = T = n_blocks * block_size
@@ -38,7 +39,8 @@ class MoELayer:
         dt = lib.DMOE_F32 if dtype == torch.float32 else lib.DMOE_BF16
         nbytes = lib.dmoe_ffn_workspace_size(T, I, I_s, k, dt)
         self.workspace = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=device)
-        self.y = torch.empty((T, H), dtype=dtype, device=device)
+        # The layer output is accumulated in fp32; it is stored as out_dtype.
+        self.y = torch.empty((T, H), dtype=out_dtype, device=device)
 
     def max_unique(self, routing: str) -> int:
         groups = self.NB if routing == "block" else self.T

@@ -129,6 +129,21 @@ def test_schedule_against_oracle(gpu_lib, n_groups, gs, k, E):
     assert offs[n] == n_groups * gs * k
 
 
+@pytest.mark.parametrize("name", ["small_bf16", "decode_b1"])
+def test_bf16_output_is_rounded_fp32_output(gpu_lib, name):
+    """Storing the layer output as bf16 rounds the fp32 result once (RNE)."""
+    cfg = get_config(name)
+    d = make_inputs(cfg, seed=0, device="cuda")
+    l32 = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, out_dtype=torch.float32)
+    l16 = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, out_dtype=torch.bfloat16)
+    for routing in ("block", "token"):
+        y32 = l32.forward(d["x"], d, routing).clone()
+        y16 = l16.forward(d["x"], d, routing).clone()
+        torch.cuda.synchronize()
+        assert y16.dtype == torch.bfloat16
+        assert torch.equal(y16, y32.to(torch.bfloat16))
+
+
 def test_error_status_on_gpu(gpu_lib):
     cfg = get_config("small_bf16")
     layer = _layer(cfg)
