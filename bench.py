@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of the MoE layer forward of a block-diffusion decode step,
+block routing vs token routing, on one MI355X.
+
+One step = one whole MoE layer forward (router -> top-k -> unique-expert
+schedule -> expert FFN -> combine) over one batch of tokens.  Steps rotate
+through ``--layers`` layers with distinct weights and hidden states, so that
+the experts a step streams were last touched more than a GiB of traffic
+earlier and cannot be served from the 256 MB Infinity Cache.
+
+Prints ONE JSON line.  ``value`` is the block-routed MoE-layer time per decode
+step in microseconds; the token-routed baseline, unique expert counts, HBM
+bandwidth and the expert-FFN roofline are reported beside it, with the CPU
+oracle timed on a bounded sample as ``cpu_baseline``.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config decode_b1]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer µs/decode step + achieved HBM GB/s (% peak), block vs token routing"
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E peak (AMD specification)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2048, help="timed steps per routing mode")
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--config", default="decode_b1")
+    ap.add_argument("--layers", type=int, default=0, help="distinct layers to rotate through (0: auto)")
+    ap.add_argument("--routing", choices=["both", "block", "token"], default="both")
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle timing per mode")
+    ap.add_argument("--ffn-only", action="store_true",
+                    help="only replay the expert FFN (for hardware-counter runs)")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("ffn.hip", "dmoe_common.h"):
+        with open(os.path.join(ROOT, "paper_2605_30876_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from dmoe_synth import get_config, make_inputs
+    from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes
+    from paper_2605_30876_amd import lib
+    from paper_2605_30876_amd.layer import MoELayer
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lib.load()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    cfg = get_config(args.config)
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    eb = element_bytes(cfg)
+    B_e, B_s = expert_bytes(cfg), shared_bytes(cfg)
+
+    # Enough layers that one rotation streams >= 1.5 GiB of distinct selected
+    # experts (block routing streams k experts per block at most).
+    if args.layers <= 0:
+        per_step = min(cfg.E, cfg.NB * cfg.k) * B_e + B_s
+        layer_bytes = cfg.E * B_e + B_s
+        free = torch.cuda.mem_get_info()[0]
+        args.layers = max(2, min(64, -(-int(1.5 * 2**30) // per_step), int(0.5 * free // layer_bytes)))
+    NL = args.layers
+    steps = -(-args.steps // NL) * NL  # whole rotations
+    log(f"[bench] config {cfg.name}: T={cfg.T} H={cfg.H} E={cfg.E} I={cfg.I} I_s={cfg.I_s} k={cfg.k}; "
+        f"{NL} layers ({NL * (cfg.E * B_e + B_s) / 2**30:.1f} GiB of weights), {steps} steps per mode")
+
+    t0 = time.time()
+    layers = []
+    for l in range(NL):
+        d = make_inputs(cfg, seed=args.seed, layer=l, device=dev)
+        layers.append((d, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
+                                   device=dev, out_dtype=dt)))
+    torch.cuda.synchronize()
+    log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
+
+    modes = ["block", "token"] if args.routing == "both" else [args.routing]
+    results = {}
+    for routing in modes:
+        def step(l, routing=routing):
+            d, m = layers[l]
+            m.forward(d["x"], d, routing)
+
+        def ffn(l, routing=routing):
+            d, m = layers[l]
+            m.experts_ffn(d["x"], d, routing)
+
+        for i in range(max(args.warmup, NL)):
+            step(i % NL)
+        torch.cuda.synchronize()
+        n_unique = [int(m.sched.n_unique[0]) for _, m in layers]
+
+        graph = ffn_graph = None
+        if not args.no_graph:
+            stream = torch.cuda.Stream()
+            stream.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(stream):
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph, stream=stream):
+                    for l in range(NL):
+                        step(l)
+                ffn_graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(ffn_graph, stream=stream):
+                    for l in range(NL):
+                        ffn(l)
+            torch.cuda.current_stream().wait_stream(stream)
+            for _ in range(2):
+                graph.replay()
+                ffn_graph.replay()
+            torch.cuda.synchronize()
+
+        def run(n_steps, fn_graph, fn_eager):
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            w0 = time.perf_counter()
+            ev0.record()
+            if fn_graph is not None:
+                for _ in range(n_steps // NL):
+                    fn_graph.replay()
+            else:
+                for i in range(n_steps):
+                    fn_eager(i % NL)
+            ev1.record()
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - w0
+            return wall, ev0.elapsed_time(ev1) / 1e3
+
+        if args.ffn_only:
+            wall, gpu_s = run(steps, ffn_graph, ffn)
+            results[routing] = {"ffn_us": gpu_s / steps * 1e6, "n_unique": n_unique}
+            log(f"[bench] {routing}: expert FFN {gpu_s / steps * 1e6:.2f} us/launch")
+            continue
+
+        wall, gpu_s = run(steps, graph, step)
+        wall_f, ffn_s = run(steps, ffn_graph, ffn)
+        U = statistics.mean(n_unique)
+        us = wall / steps * 1e6
+        layer_bytes = U * B_e + B_s + cfg.E * cfg.H * eb + cfg.T * cfg.H * eb + cfg.T * cfg.H * eb
+        ffn_bytes = U * B_e + B_s
+        ffn_us = ffn_s / steps * 1e6
+        results[routing] = {
+            "us_per_step": round(us, 3),
+            "gpu_event_us_per_step": round(gpu_s / steps * 1e6, 3),
+            "tokens_per_s": round(cfg.T / (us * 1e-6), 1),
+            "unique_experts_per_forward": round(U, 2),
+            "hbm_bytes_per_step": int(layer_bytes),
+            "hbm_gbps": round(layer_bytes / (us * 1e-6) / 1e9, 1),
+            "frac_peak": round(layer_bytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+            "expert_ffn_us": round(ffn_us, 3),
+            "expert_ffn_gbps": round(ffn_bytes / (ffn_us * 1e-6) / 1e9, 1),
+            "expert_ffn_bytes": int(ffn_bytes),
+        }
+        log(f"[bench] {routing}: {us:.2f} us/step (events {gpu_s / steps * 1e6:.2f}), U={U:.1f}, "
+            f"{results[routing]['hbm_gbps']} GB/s layer; expert FFN {ffn_us:.2f} us = "
+            f"{results[routing]['expert_ffn_gbps']} GB/s")
+        del graph, ffn_graph
+
+    if args.ffn_only:
+        print(json.dumps({"ffn_only": results, "config": cfg.name, "layers": NL, "steps": steps}))
+        return 0
+
+    main_mode = "block" if "block" in results else modes[0]
+    r = results[main_mode]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as fh:
+            tr = json.load(fh)
+        if tr.get("source_hash") == source_hash() and tr.get("config") == cfg.name:
+            traffic = tr.get("hbm_bytes_per_launch", {}).get(main_mode)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, layers[0][0], main_mode, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": r["us_per_step"],
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": max(args.warmup, NL),
+        "ms_per_step": round(r["us_per_step"] / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) hidden states, N(0,0.02^2) weights)",
+        "config": {"workload": f"{cfg.name}: one MoE layer, hidden {cfg.H}, {cfg.E} routed experts of "
+                               f"SwiGLU intermediate {cfg.I} + shared {cfg.I_s}, top-{cfg.k}, "
+                               f"{cfg.NB} sequence(s) x block {cfg.bs} = {cfg.T} tokens per forward",
+                   "routing": main_mode, "layers_rotated": NL, "graph": not args.no_graph},
+        "roofline": {"bound": "hbm", "kernel": "expert FFN (gate/up+SwiGLU and down launches)",
+                     "achieved": r["expert_ffn_gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(r["expert_ffn_gbps"] / PEAK_HBM_GBPS, 4), "traffic": traffic},
+        "cpu_baseline": cpu,
+        "block_routing": results.get("block"),
+        "token_routing": results.get("token"),
+    }
+    if "block" in results and "token" in results:
+        out["token_over_block_time"] = round(results["token"]["us_per_step"] / results["block"]["us_per_step"], 3)
+    print(json.dumps(out))
+    return 0
+
+
+def cpu_baseline(cfg, d_gpu, routing, budget_s):
+    """The CPU oracle, as it stands, timed on the host on one layer's inputs."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # threadpoolctl missing: numpy BLAS uses the visible cores
+        threads = os.cpu_count()
+    d = {k: (None if v is None else v.to("cpu")) for k, v in d_gpu.items()}
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while time.perf_counter() < t_end or not times:
+        t0 = time.perf_counter()
+        O.moe_forward(d, cfg.k, cfg.bs, routing)
+        times.append(time.perf_counter() - t0)
+        if len(times) >= 50:
+            break
+    us = float(np.median(times)) * 1e6
+    log(f"[bench] cpu oracle ({routing}): {us:.0f} us/step over {len(times)} forwards, {threads} threads")
+    del torch
+    return {"value": round(us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+            "sample": f"{len(times)} {routing}-routed forwards of one {cfg.name} layer "
+                      f"({cfg.T} tokens), median; inputs already in host memory"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())
