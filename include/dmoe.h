@@ -168,7 +168,8 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  * slot_out [T][k][H] float32 (every (t, j) is written); shared_out [T][H]
  * float32 (NULL iff no shared expert).
  * workspace: device scratch of at least dmoe_ffn_workspace_size(...) bytes,
- * ws_bytes its size.  Its contents on entry do not matter.
+ * ws_bytes its size.  Its contents on entry do not matter; calls that share
+ * one workspace must not overlap in time (use one stream).
  * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 512; 1 <= max_unique <= E.
  * DMOE_BF16: H % 128 == 0, I % 128 == 0, I_s % 128 == 0 (matrix-core tiles).
  * DMOE_F32: any H, I, I_s >= 1.

@@ -140,7 +140,7 @@ dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int
 
 size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
   if (T < 1 || I < 1 || I_s < 0 || k < 1 || !valid_dtype(dt)) return 0;
-  return dmoe::ffn_hbuf_bytes(T, I, I_s, k, dt);
+  return dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
 }
 
 dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up, const void* w_down,
@@ -164,7 +164,7 @@ dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up,
           "ws_gate, ws_up, ws_down and shared_out must all be set iff I_s > 0");
   REQUIRE(static_cast<long>(T) * k * H <= kIntLimit * 4L && static_cast<long>(T) * (k + 1) < kIntLimit,
           "T*k*H is too large");
-  const size_t need = dmoe::ffn_hbuf_bytes(T, I, I_s, k, dt);
+  const size_t need = dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
   REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
   ALIGNED(x);
   ALIGNED(w_gate);

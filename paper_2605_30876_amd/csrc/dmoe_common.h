@@ -77,10 +77,10 @@ struct FfnArgs {
   dmoe_schedule sched;
   float* slot_out;
   float* shared_out;
-  void* hbuf;  // SwiGLU activations [T*k + T][max(I, I_s)] of the storage type
+  void* workspace;  // SwiGLU activations [T*k + T][max(I, I_s)] of the storage type
 };
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
-size_t ffn_hbuf_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
+size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
 
 hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
                           dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);

@@ -63,11 +63,16 @@ _SIGS = {
 _lib = None
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libdmoe (once).  Raises if it has not been built."""
+def load(path: str | None = None) -> ctypes.CDLL:
+    """Load libdmoe (once).  Raises if it has not been built.
+
+    ``path`` (or the DMOE_LIB environment variable) selects another build of
+    the library, e.g. a variant under test; the default is the in-tree build.
+    """
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("DMOE_LIB") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"libdmoe is not built ({path} is missing); run "
                            f"'python -m paper_2605_30876_amd.build' first")

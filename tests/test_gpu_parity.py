@@ -59,6 +59,22 @@ def test_full_size_parity(gpu_lib, name, routing):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name", ["decode_b1", "small_bf16_zipf"])
+def test_workspace_reuse_across_inputs(gpu_lib, name):
+    """Forwards on different inputs through one layer (one workspace, one h
+    buffer): each later forward matches the oracle, so nothing stale is read."""
+    cfg = get_config(name)
+    layer = _layer(cfg)
+    dev = "cuda"
+    inputs = [make_inputs(cfg, seed=s, device=dev) for s in (0, 7)]
+    for routing in ("block", "token", "block"):
+        layer.forward(inputs[0]["x"], inputs[0], routing)
+        rep = run_and_check(cfg, inputs[1], routing, layer, sample_tokens=[0, 5, cfg.T - 1],
+                            check_determinism=False)
+        _say("  ", routing, {k: v for k, v in rep.items() if k != "near_ties"})
+        inputs.reverse()
+
+
 @pytest.mark.parametrize("name", ["small_bf16", "small_f32"])
 def test_block_size_one_equals_token_routing(gpu_lib, name):
     base = get_config(name)
