@@ -90,17 +90,27 @@ typedef struct dmoe_schedule {
 } dmoe_schedule;
 
 /*
+ * Bytes of optional workspace that let dmoe_router_logits split the hidden
+ * dimension over several workgroups (worth it when T is small: a decode
+ * step).  0 when no split is used for these sizes.
+ */
+size_t dmoe_router_workspace_size(int T, int H, int E, dmoe_dtype dt);
+
+/*
  * Router scores (Sec. 4.2, s_i = Router(t_i)): linear router and softmax.
  *   logits[t][e] = sum_h x[t][h] * w_router[e][h] + bias[e]
  *   probs[t][:]  = softmax(logits[t][:]) over all E experts (max-subtracted)
  * x [T][H] and w_router [E][H] of type dt; bias [E] float32 or NULL (no bias);
  * logits [T][E] float32 or NULL (not stored); probs [T][E] float32.
+ * workspace: NULL, or device scratch of ws_bytes >= dmoe_router_workspace_size
+ * bytes (contents on entry do not matter; results do not depend on whether
+ * it is given).  Calls sharing a workspace must not overlap in time.
  * Limits: T >= 1; 1 <= E <= 4096; H >= 1.  For DMOE_BF16: H % 128 == 0
  * (matrix-core tiles); DMOE_F32 has no further limit.
  */
 dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
-                               dmoe_dtype dt, int T, int H, int E,
-                               float* logits, float* probs, void* stream);
+                               dmoe_dtype dt, int T, int H, int E, float* logits, float* probs,
+                               void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Block-level routing (Sec. 4.2 aggregation, Alg. 1 with a coreset of size k).

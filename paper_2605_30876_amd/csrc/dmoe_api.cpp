@@ -58,9 +58,14 @@ const char* dmoe_last_error(void) { return g_last_error.c_str(); }
 
 const char* dmoe_version(void) { return "0.1.0"; }
 
+size_t dmoe_router_workspace_size(int T, int H, int E, dmoe_dtype dt) {
+  if (T < 1 || H < 1 || E < 1 || E > kMaxE || !valid_dtype(dt)) return 0;
+  return dmoe::router_workspace_bytes(T, H, E, dt);
+}
+
 dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
                                dmoe_dtype dt, int T, int H, int E, float* logits, float* probs,
-                               void* stream) {
+                               void* workspace, size_t ws_bytes, void* stream) {
   REQUIRE(x && w_router && probs, "x, w_router and probs must not be NULL");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
   REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
@@ -72,11 +77,12 @@ dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float*
   ALIGNED(bias);
   ALIGNED(logits);
   ALIGNED(probs);
+  ALIGNED(workspace);
   if (dt == DMOE_BF16) {
     SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
   }
-  return hip_status(dmoe::launch_router(x, w_router, bias, dt, T, H, E, logits, probs,
-                                        static_cast<hipStream_t>(stream)),
+  return hip_status(dmoe::launch_router(x, w_router, bias, dt, T, H, E, logits, probs, workspace,
+                                        workspace ? ws_bytes : 0, static_cast<hipStream_t>(stream)),
                     __func__);
 }
 

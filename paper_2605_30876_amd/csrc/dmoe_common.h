@@ -57,7 +57,9 @@ constexpr int kWave = 64;  // CDNA wavefront width
 // Host-side launchers (one per kernel family; arguments already validated)
 // ---------------------------------------------------------------------------
 hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
-                         int H, int E, float* logits, float* probs, hipStream_t s);
+                         int H, int E, float* logits, float* probs, void* workspace,
+                         size_t ws_bytes, hipStream_t s);
+size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt);
 hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, float* scores,
                              int32_t* experts, float* w, float* gap, hipStream_t s);
 hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* experts, float* w,

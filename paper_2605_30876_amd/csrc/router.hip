@@ -3,30 +3,93 @@
 //
 // bf16: logits = x Wr^T on the matrix cores (v_mfma_f32_16x16x32_bf16, fp32
 // accumulation; a bf16 x bf16 product is exact in fp32).  A workgroup owns a
-// 32-token x 32-expert tile; its four waves split the hidden dimension in
-// quarters and the partial tiles are summed in wave order through LDS, so the
-// result does not depend on scheduling.
+// 32-token x 32-expert tile of one of S slices of the hidden dimension; its
+// four waves split the slice in quarters and issue all their operand loads
+// at once, and the partial tiles are summed in wave order through LDS.  With
+// few tokens (a decode step) the hidden dimension is split over S <= 4
+// workgroups so that more CUs share the router matrix; the S partial logits
+// go to the workspace and the softmax sums them in slice order, so the result
+// does not depend on scheduling.
 // f32: one thread per (token, expert) dot product.
-// Softmax: one wave per token row, max-subtracted, in place when the caller
-// does not keep the logits.
+// Softmax: one wave per token row; all partial loads of a pass are issued
+// together and the row is staged in LDS (one read pass, one write pass).
+#include <algorithm>
+
 #include "dmoe_common.h"
 
 namespace dmoe {
 namespace {
 
 constexpr int kRouterTile = 32;
+constexpr int kRouterSteps = 8;  // K steps of 32 per load burst
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+  return v;
+}
+
+constexpr int kMaxSplits = 4;
+
+// Softmax of one token row from S partial planes (slice order) + bias; z is
+// the wave's LDS row of E floats.  A lane handles 4 elements (e = lane + 64*u)
+// per pass and issues all their partial loads together.
+__device__ void softmax_row(const float* pr, size_t plane, int S, const float* bias, int E,
+                            float* z, float* out, float* lo) {
+  const int lane = threadIdx.x & 63;
+  float m = -INFINITY;
+  for (int e0 = 0; e0 < E; e0 += 4 * kWave) {
+    float p[4][kMaxSplits];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = e0 + u * kWave + lane;
+#pragma unroll
+      for (int s = 0; s < kMaxSplits; ++s)
+        if (s < S && e < E) p[u][s] = pr[s * plane + e];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = e0 + u * kWave + lane;
+      if (e >= E) continue;
+      float v = p[u][0];
+#pragma unroll
+      for (int s = 1; s < kMaxSplits; ++s)
+        if (s < S) v += p[u][s];
+      if (bias) v += bias[e];
+      z[e] = v;
+      m = fmaxf(m, v);
+    }
+  }
+  m = wave_max(m);
+  float sum = 0.f;
+  for (int e = lane; e < E; e += kWave) sum += expf(z[e] - m);
+  sum = wave_sum(sum);
+  for (int e = lane; e < E; e += kWave) {
+    const float v = z[e];
+    out[e] = expf(v - m) / sum;
+    if (lo) lo[e] = v;
+  }
+}
 
 __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
-    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, const float* __restrict__ bias,
-    int T, int H, int E, float* __restrict__ logits) {
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, int T, int H, int E, int S,
+    float* __restrict__ part) {
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int q = lane >> 4;   // k-group of the MFMA operand / row group of the result
   const int c = lane & 15;   // row of A (token) / column of B (expert)
   const int t0 = blockIdx.x * kRouterTile;
   const int e0 = blockIdx.y * kRouterTile;
-  const int kw = H >> 2;
-  const int kbeg = wave * kw;
+  const int slice = H / S;
+  const int kw = slice >> 2;
+  const int kbeg = blockIdx.z * slice + wave * kw;
+  const int steps = kw >> 5;
 
   const bf16_t* pa[2];
   const bf16_t* pb[2];
@@ -44,13 +107,25 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
 #pragma unroll
     for (int s = 0; s < 2; ++s) acc[r][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = 0; k0 < kw; k0 += 32) {
-    bf16x8 a0 = ld_bf16x8(pa[0] + k0), a1 = ld_bf16x8(pa[1] + k0);
-    bf16x8 b0 = ld_bf16x8(pb[0] + k0), b1 = ld_bf16x8(pb[1] + k0);
-    acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc[0][0], 0, 0, 0);
-    acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b1, acc[0][1], 0, 0, 0);
-    acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b0, acc[1][0], 0, 0, 0);
-    acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc[1][1], 0, 0, 0);
+  for (int sc = 0; sc < steps; sc += kRouterSteps) {
+    const int ns = min(kRouterSteps, steps - sc);
+    bf16x8 a[kRouterSteps][2], b[kRouterSteps][2];
+#pragma unroll
+    for (int s = 0; s < kRouterSteps; ++s)
+      if (s < ns)
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          a[s][r] = ld_bf16x8(pa[r] + (sc + s) * 32);
+          b[s][r] = ld_bf16x8(pb[r] + (sc + s) * 32);
+        }
+#pragma unroll
+    for (int s = 0; s < kRouterSteps; ++s)
+      if (s < ns)
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            acc[r][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s][r], b[s][u], acc[r][u], 0, 0, 0);
   }
 
   __shared__ f32x4 red[3][4][kWave];
@@ -62,6 +137,7 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
   }
   __syncthreads();
   if (wave != 0) return;
+  float* out = part + static_cast<size_t>(blockIdx.z) * T * E;
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
 #pragma unroll
@@ -71,19 +147,18 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
       for (int ww = 0; ww < 3; ++ww) v += red[ww][r * 2 + s][lane];
       const int e = e0 + s * 16 + c;
       if (e >= E) continue;
-      const float b = bias ? bias[e] : 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = t0 + r * 16 + q * 4 + i;
-        if (t < T) logits[static_cast<size_t>(t) * E + e] = v[i] + b;
+        if (t < T) out[static_cast<size_t>(t) * E + e] = v[i];
       }
     }
   }
 }
 
 __global__ __launch_bounds__(256) void router_logits_f32_kernel(
-    const float* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
-    int T, int H, int E, float* __restrict__ logits) {
+    const float* __restrict__ x, const float* __restrict__ w, int T, int H, int E,
+    float* __restrict__ part) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   const int t = blockIdx.y;
   if (e >= E) return;
@@ -91,54 +166,65 @@ __global__ __launch_bounds__(256) void router_logits_f32_kernel(
   const float* wr = w + static_cast<size_t>(e) * H;
   float acc = 0.f;
   for (int h = 0; h < H; ++h) acc = fmaf(xr[h], wr[h], acc);
-  logits[static_cast<size_t>(t) * E + e] = acc + (bias ? bias[e] : 0.f);
+  part[static_cast<size_t>(t) * E + e] = acc;
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-  return v;
-}
-
-// One wave per token row; z and p may alias (in-place softmax).
-__global__ __launch_bounds__(256) void softmax_rows_kernel(const float* z, int T, int E, float* p) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+// One wave per token row, four rows per workgroup; dynamic LDS: 4*E floats.
+// part may alias probs (S == 1): the row is read to LDS before it is written.
+__global__ __launch_bounds__(256) void softmax_rows_kernel(const float* part, int S,
+                                                           const float* __restrict__ bias, int T,
+                                                           int E, float* probs, float* logits) {
+  extern __shared__ float zrow[];
+  const int wave = threadIdx.x >> 6;
+  const int t = blockIdx.x * 4 + wave;
   if (t >= T) return;
-  const float* zr = z + static_cast<size_t>(t) * E;
-  float* pr = p + static_cast<size_t>(t) * E;
-  float m = -INFINITY;
-  for (int e = lane; e < E; e += kWave) m = fmaxf(m, zr[e]);
-  m = wave_max(m);
-  float s = 0.f;
-  for (int e = lane; e < E; e += kWave) s += expf(zr[e] - m);
-  s = wave_sum(s);
-  for (int e = lane; e < E; e += kWave) pr[e] = expf(zr[e] - m) / s;
+  softmax_row(part + static_cast<size_t>(t) * E, static_cast<size_t>(T) * E, S, bias, E,
+              zrow + static_cast<size_t>(wave) * E, probs + static_cast<size_t>(t) * E,
+              logits ? logits + static_cast<size_t>(t) * E : nullptr);
 }
+
+// Slices of the hidden dimension: enough router workgroups to spread the
+// router matrix over about half the CUs, each slice a multiple of 128.
+int router_splits(int T, int H, int E) {
+  const long tiles = static_cast<long>((T + kRouterTile - 1) / kRouterTile) * ((E + kRouterTile - 1) / kRouterTile);
+  int S = 1;
+  while (S < kMaxSplits && tiles * S < 128 && (H / 128) % (2 * S) == 0) S *= 2;
+  return S;
+}
+
+
 
 }  // namespace
 
+size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt) {
+  if (dt != DMOE_BF16) return 0;
+  const int S = router_splits(T, H, E);
+  return S > 1 ? static_cast<size_t>(S) * T * E * sizeof(float) : 0;
+}
+
 hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
-                         int H, int E, float* logits, float* probs, hipStream_t s) {
-  float* z = logits ? logits : probs;
+                         int H, int E, float* logits, float* probs, void* workspace,
+                         size_t ws_bytes, hipStream_t s) {
+  int S = 1;
+  float* part = probs;  // S == 1: the softmax reads the logits in place
+  const size_t lds = static_cast<size_t>(4) * E * sizeof(float);
   if (dt == DMOE_BF16) {
-    dim3 grid((T + kRouterTile - 1) / kRouterTile, (E + kRouterTile - 1) / kRouterTile);
+    const size_t need = router_workspace_bytes(T, H, E, dt);
+    if (need > 0 && workspace && ws_bytes >= need) {
+      S = router_splits(T, H, E);
+      part = static_cast<float*>(workspace);
+    }
+    dim3 grid((T + kRouterTile - 1) / kRouterTile, (E + kRouterTile - 1) / kRouterTile, S);
     router_logits_bf16_kernel<<<grid, 256, 0, s>>>(static_cast<const bf16_t*>(x),
-                                                    static_cast<const bf16_t*>(w), bias, T, H, E, z);
+                                                    static_cast<const bf16_t*>(w), T, H, E, S, part);
   } else {
     dim3 grid((E + 255) / 256, T);
     router_logits_f32_kernel<<<grid, 256, 0, s>>>(static_cast<const float*>(x),
-                                                   static_cast<const float*>(w), bias, T, H, E, z);
+                                                   static_cast<const float*>(w), T, H, E, part);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  softmax_rows_kernel<<<(T + 3) / 4, 256, 0, s>>>(z, T, E, probs);
+  softmax_rows_kernel<<<(T + 3) / 4, 256, lds, s>>>(part, S, bias, T, E, probs, logits);
   return hipGetLastError();
 }
 

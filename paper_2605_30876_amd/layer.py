@@ -37,6 +37,8 @@ class MoELayer:
         self.slot_out = torch.empty((T, k, H), **f32)
         self.shared_out = torch.empty((T, H), **f32) if I_s > 0 else None
         dt = lib.DMOE_F32 if dtype == torch.float32 else lib.DMOE_BF16
+        rbytes = lib.dmoe_router_workspace_size(T, H, E, dt)
+        self.router_ws = torch.empty((rbytes,), dtype=torch.uint8, device=device) if rbytes else None
         nbytes = lib.dmoe_ffn_workspace_size(T, I, I_s, k, dt)
         self.workspace = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=device)
         # The layer output is accumulated in fp32; it is stored as out_dtype.
@@ -48,7 +50,7 @@ class MoELayer:
 
     def route(self, x, w_router, bias=None, routing: str = "block", stream=None):
         T, H, E, k = self.T, self.H, self.E, self.k
-        lib.dmoe_router_logits(x, w_router, bias, T, H, E, self.logits, self.probs, stream)
+        lib.dmoe_router_logits(x, w_router, bias, T, H, E, self.logits, self.probs, self.router_ws, stream)
         if routing == "block":
             lib.dmoe_block_aggregate_topk(self.probs, self.NB, self.bs, E, k, self.block_scores,
                                           self.block_experts, self.combine_w, self.block_gap, stream)

@@ -28,7 +28,7 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
                 DMOE_ERR_UNSUPPORTED: "DMOE_ERR_UNSUPPORTED", DMOE_ERR_HIP: "DMOE_ERR_HIP"}
 
 # Every symbol include/dmoe.h declares.
-EXPORTS = ("dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
+EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
            "dmoe_build_expert_schedule", "dmoe_ffn_workspace_size", "dmoe_expert_ffn",
            "dmoe_combine", "dmoe_last_error", "dmoe_version")
 
@@ -49,7 +49,8 @@ _P = ctypes.c_void_p
 _I = ctypes.c_int
 _S = ctypes.c_size_t
 _SIGS = {
-    "dmoe_router_logits": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
+    "dmoe_router_workspace_size": ([_I, _I, _I, _I], _S),
+    "dmoe_router_logits": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _S, _P], _I),
     "dmoe_block_aggregate_topk": ([_P, _I, _I, _I, _I, _P, _P, _P, _P, _P], _I),
     "dmoe_token_topk": ([_P, _I, _I, _I, _P, _P, _P, _P], _I),
     "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
@@ -113,9 +114,15 @@ def stream_handle(stream=None) -> int:
 # ---------------------------------------------------------------------------
 
 
-def dmoe_router_logits(x, w_router, bias, T, H, E, logits, probs, stream=None):
+def dmoe_router_workspace_size(T, H, E, dt) -> int:
+    return int(load().dmoe_router_workspace_size(T, H, E, dt))
+
+
+def dmoe_router_logits(x, w_router, bias, T, H, E, logits, probs, workspace=None, stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().dmoe_router_logits(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), T, H, E,
-                                     ptr(logits), ptr(probs), stream_handle(stream)))
+                                     ptr(logits), ptr(probs), ptr(workspace), nbytes,
+                                     stream_handle(stream)))
 
 
 def dmoe_block_aggregate_topk(probs, n_blocks, block_size, E, k, block_scores, block_experts,

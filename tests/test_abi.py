@@ -61,13 +61,14 @@ def status(L, name, *args):
 
 def test_router_validation(L, buf):
     _, p = buf
-    st, msg = status(L, "dmoe_router_logits", None, p, None, 1, 32, 2048, 256, None, p, None)
+    st, msg = status(L, "dmoe_router_logits", None, p, None, 1, 32, 2048, 256, None, p, None, 0, None)
     assert st == lib.DMOE_ERR_INVALID_ARG and "must not be NULL" in msg
-    assert status(L, "dmoe_router_logits", p, p, None, 7, 32, 2048, 256, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p, p, None, 1, 0, 2048, 256, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 5000, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p + 4, p, None, 1, 32, 2048, 256, None, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    st, msg = status(L, "dmoe_router_logits", p, p, None, 1, 32, 2000, 256, None, p, None)
+    assert status(L, "dmoe_router_logits", p, p, None, 7, 32, 2048, 256, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 0, 2048, 256, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 5000, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p + 4, p, None, 1, 32, 2048, 256, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 256, None, p, p + 8, 64, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    st, msg = status(L, "dmoe_router_logits", p, p, None, 1, 32, 2000, 256, None, p, None, 0, None)
     assert st == lib.DMOE_ERR_UNSUPPORTED and "H % 128" in msg
 
 
@@ -150,6 +151,15 @@ def test_combine_validation(L, buf):
     assert status(L, f, p, p, None, 1, 32, 2048, 65, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
     assert status(L, f, p, p, None, 9, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
     assert status(L, f, p, p, p + 4, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+
+
+def test_router_workspace_size():
+    # decode step: the hidden dimension is split, one fp32 partial plane per slice
+    n = lib.dmoe_router_workspace_size(32, 2048, 256, lib.DMOE_BF16)
+    assert n == 4 * 32 * 256 * 4  # 4 partial logit planes
+    assert lib.dmoe_router_workspace_size(4096, 2048, 256, lib.DMOE_BF16) == 0
+    assert lib.dmoe_router_workspace_size(8, 256, 16, lib.DMOE_F32) == 0
+    assert lib.dmoe_router_workspace_size(0, 2048, 256, lib.DMOE_BF16) == 0
 
 
 def test_workspace_size():
