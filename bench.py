@@ -57,7 +57,7 @@ def log(*a):
 
 def source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("ffn.hip", "dmoe_common.h"):
+    for f in ("ffn.hip", "pack.hip", "dmoe_common.h"):
         with open(os.path.join(ROOT, "paper_2605_30876_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -76,7 +76,7 @@ def main():
     from dmoe_synth import get_config, make_inputs
     from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes
     from paper_2605_30876_amd import lib
-    from paper_2605_30876_amd.layer import MoELayer
+    from paper_2605_30876_amd.layer import MoELayer, pack_weights
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lib.load()
@@ -103,8 +103,12 @@ def main():
     layers = []
     for l in range(NL):
         d = make_inputs(cfg, seed=args.seed, layer=l, device=dev)
-        layers.append((d, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
-                                   device=dev, out_dtype=dt)))
+        if l == 0 and not args.no_cpu_baseline:
+            d0_host = {k: (None if v is None else v.to("cpu")) for k, v in d.items()}
+        w = pack_weights(d)  # the layer keeps only the packed expert weights
+        layers.append((d["x"], w, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
+                                           device=dev, out_dtype=dt)))
+        del d
     torch.cuda.synchronize()
     log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
 
@@ -112,17 +116,17 @@ def main():
     results = {}
     for routing in modes:
         def step(l, routing=routing):
-            d, m = layers[l]
-            m.forward(d["x"], d, routing)
+            x, w, m = layers[l]
+            m.forward(x, w, routing)
 
         def ffn(l, routing=routing):
-            d, m = layers[l]
-            m.experts_ffn(d["x"], d, routing)
+            _, w, m = layers[l]
+            m.experts_ffn(w, routing)
 
         for i in range(max(args.warmup, NL)):
             step(i % NL)
         torch.cuda.synchronize()
-        n_unique = [int(m.sched.n_unique[0]) for _, m in layers]
+        n_unique = [int(m.sched.n_unique[0]) for _, _, m in layers]
 
         graph = ffn_graph = None
         if not args.no_graph:
@@ -204,7 +208,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, layers[0][0], main_mode, args.cpu_seconds)
+        cpu = cpu_baseline(cfg, d0_host, main_mode, args.cpu_seconds)
 
     out = {
         "metric": METRIC,
@@ -236,10 +240,10 @@ def main():
     return 0
 
 
-def cpu_baseline(cfg, d_gpu, routing, budget_s):
-    """The CPU oracle, as it stands, timed on the host on one layer's inputs."""
+def cpu_baseline(cfg, d, routing, budget_s):
+    """The CPU oracle, as it stands, timed on the host on one layer's inputs
+    (host copies of the tensors the GPU runs on)."""
     import numpy as np
-    import torch
 
     import oracle as O
 
@@ -248,7 +252,6 @@ def cpu_baseline(cfg, d_gpu, routing, budget_s):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: numpy BLAS uses the visible cores
         threads = os.cpu_count()
-    d = {k: (None if v is None else v.to("cpu")) for k, v in d_gpu.items()}
     times = []
     t_end = time.perf_counter() + budget_s
     while time.perf_counter() < t_end or not times:
@@ -259,7 +262,6 @@ def cpu_baseline(cfg, d_gpu, routing, budget_s):
             break
     us = float(np.median(times)) * 1e6
     log(f"[bench] cpu oracle ({routing}): {us:.0f} us/step over {len(times)} forwards, {threads} threads")
-    del torch
     return {"value": round(us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
             "sample": f"{len(times)} {routing}-routed forwards of one {cfg.name} layer "
                       f"({cfg.T} tokens), median; inputs already in host memory"}

@@ -19,6 +19,20 @@
  *                              rows, plus the always-on shared expert
  *   dmoe_combine               y_t = sum_j w[t,j] * FFN_{e_tj}(x_t) + FFN_s(x_t)
  *
+ * and two layout conversions for the expert FFN's operands:
+ *
+ *   dmoe_pack_expert_weights   expert weights -> the FFN's packed layout
+ *                              (once, when the model is loaded)
+ *   dmoe_pack_activations      hidden states -> chunk-major layout (also a
+ *                              by-product of dmoe_router_logits)
+ *
+ * Chunk-major activations
+ * -----------------------
+ * The expert FFN reads hidden states as 16-byte chunks of c consecutive
+ * features (c = 8 for DMOE_BF16, 4 for DMOE_F32), chunk-major:
+ *   x_chunked[(j * T + t) * c + i] = x[t][j * c + i],   j < H/c, i < c
+ * so that the same chunk of consecutive tokens is contiguous in memory.
+ *
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Every pointer argument is a DEVICE pointer (memory the caller allocated on
@@ -102,6 +116,9 @@ size_t dmoe_router_workspace_size(int T, int H, int E, dmoe_dtype dt);
  *   probs[t][:]  = softmax(logits[t][:]) over all E experts (max-subtracted)
  * x [T][H] and w_router [E][H] of type dt; bias [E] float32 or NULL (no bias);
  * logits [T][E] float32 or NULL (not stored); probs [T][E] float32.
+ * x_chunked: NULL, or T*H elements of type dt that receive x in the
+ * chunk-major layout (see above; H must be a multiple of c), ready for
+ * dmoe_expert_ffn; the router reads every chunk of x anyway.
  * workspace: NULL, or device scratch of ws_bytes >= dmoe_router_workspace_size
  * bytes (contents on entry do not matter; results do not depend on whether
  * it is given).  Calls sharing a workspace must not overlap in time.
@@ -110,7 +127,7 @@ size_t dmoe_router_workspace_size(int T, int H, int E, dmoe_dtype dt);
  */
 dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
                                dmoe_dtype dt, int T, int H, int E, float* logits, float* probs,
-                               void* workspace, size_t ws_bytes, void* stream);
+                               void* x_chunked, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Block-level routing (Sec. 4.2 aggregation, Alg. 1 with a coreset of size k).
@@ -155,6 +172,37 @@ dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int
                                        int k, int E, dmoe_schedule sched, void* stream);
 
 /*
+ * Hidden states x [T][H] (row-major, type dt) -> x_chunked [T*H] in the
+ * chunk-major layout above.  For callers that do not run dmoe_router_logits
+ * with its x_chunked output.  x and x_chunked must not overlap.
+ * Limits: T, H >= 1; H % c == 0; T*H < 2^31.
+ */
+dmoe_status dmoe_pack_activations(const void* x, dmoe_dtype dt, int T, int H, void* x_chunked,
+                                  void* stream);
+
+/*
+ * Expert weights in the layout dmoe_expert_ffn streams (call once when the
+ * model is loaded; the FFN reads only the packed copies).
+ * Inputs: w_gate, w_up [n_experts][I][H]; w_down [n_experts][H][I], type dt.
+ * Outputs: w13 (2*n_experts*I*H elements) and w2 (n_experts*H*I elements) of
+ * type dt; neither may overlap an input or the other.
+ *   DMOE_BF16: matrix-core fragment order.  w13 holds, per expert, tiles of
+ *     16 rows x 32 columns, index [it][ks] with it < I/8, ks < H/32; tile row
+ *     r (r < 16) is the gate row (r%4 < 2) or the up row (r%4 >= 2) of
+ *     intermediate unit 8*it + 2*(r/4) + r%2, columns 32*ks .. 32*ks+31.  w2
+ *     holds, per expert, tiles [jt][ks] with jt < H/16, ks < I/32, tile row r
+ *     being w_down row 16*jt + r, columns 32*ks .. 32*ks+31.  A tile is stored
+ *     as 64 pieces of 8 elements; piece p = 16*g + r holds row r, columns
+ *     8g .. 8g+7 of the tile.
+ *   DMOE_F32: w13[e] = w_gate[e] followed by w_up[e]; w2 = w_down.
+ * The shared expert is packed by a second call with n_experts = 1, I = I_s.
+ * Limits: n_experts, H, I >= 1; DMOE_BF16: H % 128 == 0 and I % 128 == 0.
+ */
+dmoe_status dmoe_pack_expert_weights(const void* w_gate, const void* w_up, const void* w_down,
+                                     dmoe_dtype dt, int n_experts, int H, int I, void* w13, void* w2,
+                                     void* stream);
+
+/*
  * Bytes of workspace dmoe_expert_ffn needs for these sizes (the SwiGLU
  * activations of every routed row and every shared-expert row).
  * Returns 0 on invalid sizes.
@@ -164,14 +212,15 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
 /*
  * Expert execution: for every unique expert e = sched.unique[u] and each of
  * its rows (t, j):
- *   h = silu(w_gate[e] x_t) * (w_up[e] x_t)          (SwiGLU, silu(a) = a/(1+e^-a))
- *   slot_out[t][j][:] = w_down[e] h
- * and, when the shared expert is present (ws_gate != NULL), for every token t:
- *   shared_out[t][:] = ws_down (silu(ws_gate x_t) * (ws_up x_t))
+ *   h = silu(W_gate[e] x_t) * (W_up[e] x_t)          (SwiGLU, silu(a) = a/(1+e^-a))
+ *   slot_out[t][j][:] = W_down[e] h
+ * and, when the shared expert is present (ws13 != NULL), for every token t:
+ *   shared_out[t][:] = Ws_down (silu(Ws_gate x_t) * (Ws_up x_t))
  * Each selected expert's weights are streamed once per call.
- * x [T][H]; w_gate, w_up [E][I][H]; w_down [E][H][I]; ws_gate, ws_up [I_s][H];
- * ws_down [H][I_s] (all type dt; the three shared pointers are all NULL with
- * I_s == 0, or all set with I_s > 0).
+ * x_chunked: the hidden states x [T][H] in the chunk-major layout above.
+ * w13, w2: all E routed experts packed by dmoe_pack_expert_weights (I);
+ * ws13, ws2: the shared expert packed the same way (n_experts = 1, I = I_s),
+ * both NULL with I_s == 0 or both set with I_s > 0.  All of type dt.
  * sched: written by dmoe_build_expert_schedule for these T and k.
  * max_unique: an upper bound of sched.n_unique known on the host (the grid is
  * sized for it): min(E, n_groups*k).
@@ -180,15 +229,15 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  * workspace: device scratch of at least dmoe_ffn_workspace_size(...) bytes,
  * ws_bytes its size.  Its contents on entry do not matter; calls that share
  * one workspace must not overlap in time (use one stream).
- * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 512; 1 <= max_unique <= E.
+ * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 512; 1 <= max_unique <= E;
+ * H % c == 0; (T*k + T) * max(I, I_s) < 2^31.
  * DMOE_BF16: H % 128 == 0, I % 128 == 0, I_s % 128 == 0 (matrix-core tiles).
- * DMOE_F32: any H, I, I_s >= 1.
+ * DMOE_F32: any I, I_s >= 1.
  */
-dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up,
-                            const void* w_down, const void* ws_gate, const void* ws_up,
-                            const void* ws_down, dmoe_dtype dt, int T, int H, int E, int I,
-                            int I_s, int k, int max_unique, dmoe_schedule sched, float* slot_out,
-                            float* shared_out, void* workspace, size_t ws_bytes, void* stream);
+dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* w2, const void* ws13,
+                            const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
+                            int max_unique, dmoe_schedule sched, float* slot_out, float* shared_out,
+                            void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Weighted combine:

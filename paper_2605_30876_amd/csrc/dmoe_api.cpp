@@ -65,7 +65,7 @@ size_t dmoe_router_workspace_size(int T, int H, int E, dmoe_dtype dt) {
 
 dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float* bias,
                                dmoe_dtype dt, int T, int H, int E, float* logits, float* probs,
-                               void* workspace, size_t ws_bytes, void* stream) {
+                               void* x_chunked, void* workspace, size_t ws_bytes, void* stream) {
   REQUIRE(x && w_router && probs, "x, w_router and probs must not be NULL");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
   REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
@@ -78,11 +78,16 @@ dmoe_status dmoe_router_logits(const void* x, const void* w_router, const float*
   ALIGNED(logits);
   ALIGNED(probs);
   ALIGNED(workspace);
+  ALIGNED(x_chunked);
+  if (x_chunked) {
+    REQUIRE(H % dmoe::chunk_elems(dt) == 0, "x_chunked needs H %% %d == 0 (H=%d)", dmoe::chunk_elems(dt), H);
+  }
   if (dt == DMOE_BF16) {
     SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
   }
-  return hip_status(dmoe::launch_router(x, w_router, bias, dt, T, H, E, logits, probs, workspace,
-                                        workspace ? ws_bytes : 0, static_cast<hipStream_t>(stream)),
+  return hip_status(dmoe::launch_router(x, w_router, bias, dt, T, H, E, logits, probs, x_chunked,
+                                        workspace, workspace ? ws_bytes : 0,
+                                        static_cast<hipStream_t>(stream)),
                     __func__);
 }
 
@@ -144,18 +149,54 @@ dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int
                     __func__);
 }
 
+dmoe_status dmoe_pack_activations(const void* x, dmoe_dtype dt, int T, int H, void* x_chunked,
+                                  void* stream) {
+  REQUIRE(x && x_chunked, "x and x_chunked must not be NULL");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
+  REQUIRE(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
+  REQUIRE(static_cast<long>(T) * H <= kIntLimit, "T*H must fit in int32");
+  REQUIRE(x != x_chunked, "x and x_chunked must not alias");
+  ALIGNED(x);
+  ALIGNED(x_chunked);
+  return hip_status(dmoe::launch_pack_activations(x, dt, T, H, x_chunked, static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
+dmoe_status dmoe_pack_expert_weights(const void* w_gate, const void* w_up, const void* w_down,
+                                     dmoe_dtype dt, int n_experts, int H, int I, void* w13, void* w2,
+                                     void* stream) {
+  REQUIRE(w_gate && w_up && w_down && w13 && w2, "no pointer may be NULL");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(n_experts >= 1 && H >= 1 && I >= 1, "n_experts=%d, H=%d and I=%d must be >= 1", n_experts, H, I);
+  REQUIRE(w13 != w_gate && w13 != w_up && w13 != w_down && w2 != w_gate && w2 != w_up && w2 != w_down &&
+              w13 != w2,
+          "outputs must not alias the inputs or each other");
+  ALIGNED(w_gate);
+  ALIGNED(w_up);
+  ALIGNED(w_down);
+  ALIGNED(w13);
+  ALIGNED(w2);
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0 && I % 128 == 0, "bf16 experts need H and I to be multiples of 128 (H=%d, I=%d)",
+            H, I);
+  }
+  return hip_status(dmoe::launch_pack_weights(w_gate, w_up, w_down, dt, n_experts, H, I, w13, w2,
+                                              static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
 size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
   if (T < 1 || I < 1 || I_s < 0 || k < 1 || !valid_dtype(dt)) return 0;
   return dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
 }
 
-dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up, const void* w_down,
-                            const void* ws_gate, const void* ws_up, const void* ws_down,
-                            dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
-                            int max_unique, dmoe_schedule sched, float* slot_out,
-                            float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
-  REQUIRE(x && w_gate && w_up && w_down && slot_out && workspace,
-          "x, w_gate, w_up, w_down, slot_out and workspace must not be NULL");
+dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* w2, const void* ws13,
+                            const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
+                            int max_unique, dmoe_schedule sched, float* slot_out, float* shared_out,
+                            void* workspace, size_t ws_bytes, void* stream) {
+  REQUIRE(x_chunked && w13 && w2 && slot_out && workspace,
+          "x_chunked, w13, w2, slot_out and workspace must not be NULL");
   REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
           "every schedule array must be set");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
@@ -164,21 +205,21 @@ dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up,
   REQUIRE(E >= 1, "E=%d must be >= 1", E);
   REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
   REQUIRE(max_unique >= 1 && max_unique <= E, "max_unique=%d must be in [1, E]", max_unique);
+  REQUIRE(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
   const bool shared = I_s > 0;
-  REQUIRE(shared == (ws_gate != nullptr) && shared == (ws_up != nullptr) &&
-              shared == (ws_down != nullptr) && shared == (shared_out != nullptr),
-          "ws_gate, ws_up, ws_down and shared_out must all be set iff I_s > 0");
-  REQUIRE(static_cast<long>(T) * k * H <= kIntLimit * 4L && static_cast<long>(T) * (k + 1) < kIntLimit,
-          "T*k*H is too large");
+  REQUIRE(shared == (ws13 != nullptr) && shared == (ws2 != nullptr) && shared == (shared_out != nullptr),
+          "ws13, ws2 and shared_out must all be set iff I_s > 0");
+  const long rows = static_cast<long>(T) * k + (shared ? T : 0);
+  REQUIRE(rows < kIntLimit && rows * (I > I_s ? I : I_s) <= kIntLimit && static_cast<long>(T) * H <= kIntLimit &&
+              static_cast<long>(T) * k * H <= kIntLimit * 4L,
+          "T*k*H, T*H or the SwiGLU buffer is too large");
   const size_t need = dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
   REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
-  ALIGNED(x);
-  ALIGNED(w_gate);
-  ALIGNED(w_up);
-  ALIGNED(w_down);
-  ALIGNED(ws_gate);
-  ALIGNED(ws_up);
-  ALIGNED(ws_down);
+  ALIGNED(x_chunked);
+  ALIGNED(w13);
+  ALIGNED(w2);
+  ALIGNED(ws13);
+  ALIGNED(ws2);
   ALIGNED(slot_out);
   ALIGNED(shared_out);
   ALIGNED(workspace);
@@ -187,7 +228,7 @@ dmoe_status dmoe_expert_ffn(const void* x, const void* w_gate, const void* w_up,
     SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
             "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
   }
-  dmoe::FfnArgs a{x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, T, H, E, I, I_s, k, max_unique,
+  dmoe::FfnArgs a{x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_unique,
                   sched, slot_out, shared_out, workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }

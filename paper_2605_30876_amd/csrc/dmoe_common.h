@@ -57,8 +57,8 @@ constexpr int kWave = 64;  // CDNA wavefront width
 // Host-side launchers (one per kernel family; arguments already validated)
 // ---------------------------------------------------------------------------
 hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
-                         int H, int E, float* logits, float* probs, void* workspace,
-                         size_t ws_bytes, hipStream_t s);
+                         int H, int E, float* logits, float* probs, void* x_chunked,
+                         void* workspace, size_t ws_bytes, hipStream_t s);
 size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt);
 hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, float* scores,
                              int32_t* experts, float* w, float* gap, hipStream_t s);
@@ -67,19 +67,25 @@ hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* e
 hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, int E,
                            dmoe_schedule sched, hipStream_t s);
 
+// 16-byte chunks: elements of one chunk of the chunk-major activation layout.
+inline int chunk_elems(dmoe_dtype dt) { return dt == DMOE_F32 ? 4 : 8; }
+
+hipError_t launch_pack_weights(const void* wg, const void* wu, const void* wd, dmoe_dtype dt, int E,
+                               int H, int I, void* w13, void* w2, hipStream_t s);
+hipError_t launch_pack_activations(const void* x, dmoe_dtype dt, int T, int H, void* x_chunked,
+                                   hipStream_t s);
+
 struct FfnArgs {
-  const void* x;
-  const void* wg;
-  const void* wu;
-  const void* wd;
-  const void* wsg;
-  const void* wsu;
-  const void* wsd;
+  const void* x;     // activations, chunk-major [H/c][T][c]
+  const void* w13;   // packed routed gate/up weights
+  const void* w2;    // packed routed down weights
+  const void* ws13;  // packed shared-expert gate/up (or nullptr)
+  const void* ws2;   // packed shared-expert down (or nullptr)
   int T, H, E, I, I_s, k, max_unique;
   dmoe_schedule sched;
   float* slot_out;
   float* shared_out;
-  void* workspace;  // SwiGLU activations [T*k + T][max(I, I_s)] of the storage type
+  void* workspace;  // SwiGLU activations of T*k (+ T) rows, max(I, I_s) wide, storage type
 };
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);

@@ -25,9 +25,13 @@
 //    KMAX 32-wide K steps), with the token operand double-buffered in chunks
 //    behind it; partial tiles are summed in wave order through LDS, so
 //    results do not depend on scheduling.
-//  * A lane's 8-element K group is the same index set in A and B, which is all
-//    the matrix instruction needs; the four lane groups of a 16-byte load
-//    cover 64 contiguous bytes of a row.
+//  * Operand layouts are chosen so that consecutive lanes read consecutive
+//    memory: weights are pre-packed in fragment order (a wave's load of one
+//    16 x 32 tile is 1 KiB contiguous, its burst a contiguous run), and token
+//    rows (x, and the h rows between the two kernels) are chunk-major
+//    [K/8][rows][8], so 16 consecutive rows read 256 contiguous bytes per
+//    8-element chunk.  Lane (q, c) of a K-step holds chunk 4*step + q of its
+//    row in both operands, which is all the matrix instruction needs.
 // f32 path: plain per-thread dot products (small fp32 layers).
 #include <algorithm>
 
@@ -66,23 +70,23 @@ __device__ __forceinline__ bool decode_group(int gidx, int max_unique, const int
 // ---- bf16 kernels ----------------------------------------------------------
 
 struct FfnParams {
-  const bf16_t* x;
-  const bf16_t* wg;
-  const bf16_t* wu;
-  const bf16_t* wd;
-  const bf16_t* wsg;
-  const bf16_t* wsu;
-  const bf16_t* wsd;
+  const bf16_t* xk;    // activations, chunk-major [H/8][T][8]
+  const bf16_t* w13;   // routed gate/up, fragment-packed
+  const bf16_t* w2;    // routed down, fragment-packed
+  const bf16_t* ws13;  // shared gate/up, fragment-packed
+  const bf16_t* ws2;   // shared down, fragment-packed
   const int* n_unique;
   const int* unique;
   const int* offsets;
   const int* row_token;
   const int* row_slot;
-  int T, H, I, I_s, k, Tk, ldh, max_unique;
-  bf16_t* hbuf;
+  int T, H, I, I_s, k, Tk, R, max_unique;  // R: rows of the h buffer
+  bf16_t* hk;                              // SwiGLU activations, chunk-major [ldh/8][R][8]
   float* slot_out;
   float* shared_out;
 };
+
+constexpr int kFrag = 512;  // bf16 elements of one packed 16 x 32 weight tile (1 KiB)
 
 // Operands of one wave for up to KMAX K-steps (32 each) of its K-slice.
 // A: one 16-row weight tile, all steps issued at once; B: NT 16-column token
@@ -95,29 +99,32 @@ struct WaveOps {
   bf16x8 b[2][kBChunk][NT];
 };
 
+// A: packed tiles, step s at pa + s*kFrag (one contiguous burst per wave).
 template <int NT, int KMAX>
-__device__ __forceinline__ void issue_a(WaveOps<NT, KMAX>& w, const bf16_t* pa, int k0, int ns) {
+__device__ __forceinline__ void issue_a(WaveOps<NT, KMAX>& w, const bf16_t* pa, int ns) {
 #pragma unroll
   for (int s = 0; s < KMAX; ++s)
-    if (s < ns) w.a[s] = ld_bf16x8(pa + k0 + s * 32);
+    if (s < ns) w.a[s] = ld_bf16x8(pa + s * kFrag);
 }
 
+// B: chunk-major rows, step s at pb[ct] + s*bstep.
 template <int BUF, int NT, int KMAX>
-__device__ __forceinline__ void issue_b(WaveOps<NT, KMAX>& w, const bf16_t* const* pb, int k0, int chunk, int ns) {
+__device__ __forceinline__ void issue_b(WaveOps<NT, KMAX>& w, const bf16_t* const* pb, int bstep, int chunk,
+                                        int ns) {
 #pragma unroll
   for (int s = 0; s < kBChunk; ++s)
     if (chunk * kBChunk + s < ns)
 #pragma unroll
-      for (int ct = 0; ct < NT; ++ct) w.b[BUF][s][ct] = ld_bf16x8(pb[ct] + k0 + (chunk * kBChunk + s) * 32);
+      for (int ct = 0; ct < NT; ++ct) w.b[BUF][s][ct] = ld_bf16x8(pb[ct] + (chunk * kBChunk + s) * bstep);
 }
 
 template <int C, int NT, int KMAX>
-__device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX>& w, const bf16_t* const* pb, int k0, int ns,
+__device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX>& w, const bf16_t* const* pb, int bstep, int ns,
                                           f32x4 (&acc)[NT]) {
   constexpr int NCH = KMAX / kBChunk;
   if constexpr (C < NCH) {
     if (C * kBChunk < ns) {
-      if constexpr (C + 1 < NCH) issue_b<(C + 1) & 1>(w, pb, k0, C + 1, ns);
+      if constexpr (C + 1 < NCH) issue_b<(C + 1) & 1>(w, pb, bstep, C + 1, ns);
       __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads where they are
 #pragma unroll
       for (int s = 0; s < kBChunk; ++s)
@@ -126,23 +133,26 @@ __device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX>& w, const bf16_t* co
           for (int ct = 0; ct < NT; ++ct)
             acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.a[C * kBChunk + s], w.b[C & 1][s][ct],
                                                               acc[ct], 0, 0, 0);
-      mma_chunk<C + 1>(w, pb, k0, ns, acc);
+      mma_chunk<C + 1>(w, pb, bstep, ns, acc);
     }
   }
 }
 
-// acc[ct] += A[k0 .. k0 + 32*steps) . B_ct[same]^T for this wave's slice, in
-// bursts of KMAX steps: token chunk 0, the weight burst, then the chunks.
+// acc[ct] += A . B_ct^T over this wave's `steps` K-steps, in bursts of KMAX
+// steps: token chunk 0, the weight burst, then the remaining token chunks.
 template <int NT, int KMAX>
-__device__ __forceinline__ void wave_dot(const bf16_t* pa, const bf16_t* const* pb, int steps,
+__device__ __forceinline__ void wave_dot(const bf16_t* pa, const bf16_t* const* pb, int bstep, int steps,
                                          f32x4 (&acc)[NT]) {
   WaveOps<NT, KMAX> w;
   for (int sc = 0; sc < steps; sc += KMAX) {
     const int ns = min(KMAX, steps - sc);
-    issue_b<0>(w, pb, sc * 32, 0, ns);
-    issue_a(w, pa, sc * 32, ns);
+    const bf16_t* pbs[NT];
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) pbs[ct] = pb[ct] + sc * bstep;
+    issue_b<0>(w, pbs, bstep, 0, ns);
+    issue_a(w, pa + sc * kFrag, ns);
     __builtin_amdgcn_sched_barrier(0);
-    mma_chunk<0>(w, pb, sc * 32, ns, acc);
+    mma_chunk<0>(w, pbs, bstep, ns, acc);
   }
 }
 
@@ -168,24 +178,25 @@ __device__ __forceinline__ void zero(f32x4 (&acc)[NT]) {
   for (int ct = 0; ct < NT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
-// grid (ldh / 8, groups): tile of 8 intermediate units (16 A rows).
+// grid (ldh / 8, groups): packed gate/up tile `it` = 8 intermediate units.
+// Wave w reduces over hidden chunks [w*H/32, (w+1)*H/32) (K-steps
+// [w*H/128, (w+1)*H/128)).
 template <int NT, int KMAX>
 __global__ __launch_bounds__(kThreads) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
     return;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
-  const int i0 = blockIdx.x * 8;
-  if (i0 >= Iw) return;
+  const int it = blockIdx.x;
+  if (it * 8 >= Iw) return;
   const int H = p.H;
-  const bf16_t* Wg = g.expert >= 0 ? p.wg + static_cast<size_t>(g.expert) * p.I * H : p.wsg;
-  const bf16_t* Wu = g.expert >= 0 ? p.wu + static_cast<size_t>(g.expert) * p.I * H : p.wsu;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = lane >> 4, c = lane & 15;
-  const int kw = H >> 2, kbeg = wave * kw, steps = kw >> 5;
-  // A-row c: gate (c%4 < 2) or up row of intermediate unit i0 + 2*(c/4) + c%2.
-  const int i = i0 + 2 * (c >> 2) + (c & 1);
-  const bf16_t* pa = ((c & 2) ? Wu : Wg) + static_cast<size_t>(i) * H + kbeg + q * 8;
+  const int ksteps = H >> 5, steps = ksteps >> 2;
+  const bf16_t* W = g.expert >= 0 ? p.w13 + static_cast<size_t>(g.expert) * 2 * p.I * H : p.ws13;
+  const bf16_t* pa = W + (static_cast<size_t>(it) * ksteps + wave * steps) * kFrag + lane * 8;
+  const int bstep = 32 * p.T;  // 4 chunks of T tokens per K-step
+  const int chunk0 = wave * steps * 4 + q;
 
   __shared__ f32x4 red[3][NT][kWave];
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
@@ -194,21 +205,22 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_bf16_kernel(FfnParams p) 
     for (int ct = 0; ct < NT; ++ct) {
       const int col = min(p0 + ct * 16 + c, g.n - 1);
       const int tok = g.tok ? g.tok[col] : col;
-      pb[ct] = p.x + static_cast<size_t>(tok) * H + kbeg + q * 8;
+      pb[ct] = p.xk + (static_cast<size_t>(chunk0) * p.T + tok) * 8;
     }
     f32x4 acc[NT];
     zero(acc);
-    wave_dot<NT, KMAX>(pa, pb, steps, acc);
+    wave_dot<NT, KMAX>(pa, pb, bstep, steps, acc);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
       for (int ct = 0; ct < NT; ++ct) {
         const int col = p0 + ct * 16 + c;
         if (col < g.n) {
+          // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*it + 2q
           const f32x4 v = acc[ct];
           const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
           const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3]);
-          bf16_t* dst = p.hbuf + static_cast<size_t>(g.r0 + col) * p.ldh + i0 + 2 * q;
+          bf16_t* dst = p.hk + (static_cast<size_t>(it) * p.R + g.r0 + col) * 8 + 2 * q;
           *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
         }
       }
@@ -217,7 +229,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_bf16_kernel(FfnParams p) 
   }
 }
 
-// grid (H / 16, groups): tile of 16 output features.
+// grid (H / 16, groups): packed down tile `jt` = 16 output features.
 template <int NT, int KMAX>
 __global__ __launch_bounds__(kThreads) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
@@ -225,12 +237,14 @@ __global__ __launch_bounds__(kThreads) void ffn_down_bf16_kernel(FfnParams p) {
     return;
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
-  const bf16_t* Wd = g.expert >= 0 ? p.wd + static_cast<size_t>(g.expert) * H * p.I : p.wsd;
-  const int j0 = blockIdx.x * 16;
+  const int jt = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = lane >> 4, c = lane & 15;
-  const int kw = Kd >> 2, kbeg = wave * kw, steps = kw >> 5;
-  const bf16_t* pa = Wd + static_cast<size_t>(j0 + c) * Kd + kbeg + q * 8;
+  const int ksteps = Kd >> 5, steps = ksteps >> 2;
+  const bf16_t* W = g.expert >= 0 ? p.w2 + static_cast<size_t>(g.expert) * H * p.I : p.ws2;
+  const bf16_t* pa = W + (static_cast<size_t>(jt) * ksteps + wave * steps) * kFrag + lane * 8;
+  const int bstep = 32 * p.R;
+  const int chunk0 = wave * steps * 4 + q;
 
   __shared__ f32x4 red[3][NT][kWave];
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
@@ -238,18 +252,18 @@ __global__ __launch_bounds__(kThreads) void ffn_down_bf16_kernel(FfnParams p) {
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
       const int col = min(p0 + ct * 16 + c, g.n - 1);
-      pb[ct] = p.hbuf + static_cast<size_t>(g.r0 + col) * p.ldh + kbeg + q * 8;
+      pb[ct] = p.hk + (static_cast<size_t>(chunk0) * p.R + g.r0 + col) * 8;
     }
     f32x4 acc[NT];
     zero(acc);
-    wave_dot<NT, KMAX>(pa, pb, steps, acc);
+    wave_dot<NT, KMAX>(pa, pb, bstep, steps, acc);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
       for (int ct = 0; ct < NT; ++ct) {
         const int col = p0 + ct * 16 + c;
         if (col < g.n) {
-          const int j = j0 + 4 * q;
+          const int j = jt * 16 + 4 * q;
           float* dst;
           if (g.tok) {
             const int r = g.r0 + col;
@@ -268,32 +282,33 @@ __global__ __launch_bounds__(kThreads) void ffn_down_bf16_kernel(FfnParams p) {
 // ---- f32 path -------------------------------------------------------------
 
 __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
-    const float* __restrict__ x, const float* __restrict__ wg, const float* __restrict__ wu,
-    const float* __restrict__ wsg, const float* __restrict__ wsu, const int* __restrict__ n_unique,
-    const int* __restrict__ unique, const int* __restrict__ offsets,
-    const int* __restrict__ row_token, int T, int H, int I, int I_s, int Tk, int max_unique,
-    int ldh, float* __restrict__ hbuf) {
+    const float* __restrict__ xk, const float* __restrict__ w13, const float* __restrict__ ws13,
+    const int* __restrict__ n_unique, const int* __restrict__ unique, const int* __restrict__ offsets,
+    const int* __restrict__ row_token, int T, int H, int I, int I_s, int Tk, int max_unique, int ldh,
+    float* __restrict__ hbuf) {
   Group g;
   if (!decode_group(blockIdx.y, max_unique, n_unique, unique, offsets, row_token, T, Tk, g)) return;
   const int Iw = g.expert >= 0 ? I : I_s;
   const int i = blockIdx.x * kThreads + threadIdx.x;
   if (i >= Iw) return;
-  const float* wgr = (g.expert >= 0 ? wg + static_cast<size_t>(g.expert) * I * H : wsg) + static_cast<size_t>(i) * H;
-  const float* wur = (g.expert >= 0 ? wu + static_cast<size_t>(g.expert) * I * H : wsu) + static_cast<size_t>(i) * H;
+  // stacked weights: [2][Iw][H], gate then up
+  const float* W = g.expert >= 0 ? w13 + static_cast<size_t>(g.expert) * 2 * I * H : ws13;
+  const float* wgr = W + static_cast<size_t>(i) * H;
+  const float* wur = W + (static_cast<size_t>(Iw) + i) * H;
   for (int col = 0; col < g.n; ++col) {
     const int tok = g.tok ? g.tok[col] : col;
-    const float* xr = x + static_cast<size_t>(tok) * H;
     float a = 0.f, b = 0.f;
     for (int h = 0; h < H; ++h) {
-      a = fmaf(xr[h], wgr[h], a);
-      b = fmaf(xr[h], wur[h], b);
+      const float xv = xk[(static_cast<size_t>(h >> 2) * T + tok) * 4 + (h & 3)];
+      a = fmaf(xv, wgr[h], a);
+      b = fmaf(xv, wur[h], b);
     }
     hbuf[static_cast<size_t>(g.r0 + col) * ldh + i] = silu_f32(a) * b;
   }
 }
 
 __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
-    const float* __restrict__ wd, const float* __restrict__ wsd, const int* __restrict__ n_unique,
+    const float* __restrict__ w2, const float* __restrict__ ws2, const int* __restrict__ n_unique,
     const int* __restrict__ unique, const int* __restrict__ offsets,
     const int* __restrict__ row_token, const int* __restrict__ row_slot, int T, int H, int I,
     int I_s, int k, int Tk, int max_unique, int ldh, const float* __restrict__ hbuf,
@@ -303,7 +318,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
   const int Kd = g.expert >= 0 ? I : I_s;
   const int j = blockIdx.x * kThreads + threadIdx.x;
   if (j >= H) return;
-  const float* wr = (g.expert >= 0 ? wd + static_cast<size_t>(g.expert) * H * I : wsd) + static_cast<size_t>(j) * Kd;
+  const float* wr = (g.expert >= 0 ? w2 + static_cast<size_t>(g.expert) * H * I : ws2) + static_cast<size_t>(j) * Kd;
   for (int col = 0; col < g.n; ++col) {
     const float* hr = hbuf + static_cast<size_t>(g.r0 + col) * ldh;
     float acc = 0.f;
@@ -327,9 +342,9 @@ int pick_ntiles(int T, int k, int max_unique) {
 }
 
 template <int NT>
-hipError_t launch_bf16(const FfnParams& p, int groups, hipStream_t s) {
+hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   constexpr int KMAX = NT <= 2 ? 16 : 8;
-  ffn_gateup_bf16_kernel<NT, KMAX><<<dim3(p.ldh / 8, groups), kThreads, 0, s>>>(p);
+  ffn_gateup_bf16_kernel<NT, KMAX><<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_down_bf16_kernel<NT, 8><<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
@@ -346,34 +361,33 @@ size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt) {
 
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
   const int Tk = a.T * a.k;
+  const int R = Tk + (a.I_s > 0 ? a.T : 0);
   const int ldh = std::max(a.I, a.I_s);
   const int groups = a.max_unique + (a.I_s > 0 ? 1 : 0);
   if (dt == DMOE_BF16) {
-    FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.wg),
-                static_cast<const bf16_t*>(a.wu), static_cast<const bf16_t*>(a.wd),
-                static_cast<const bf16_t*>(a.wsg), static_cast<const bf16_t*>(a.wsu),
-                static_cast<const bf16_t*>(a.wsd), a.sched.n_unique, a.sched.unique,
+    FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w13),
+                static_cast<const bf16_t*>(a.w2), static_cast<const bf16_t*>(a.ws13),
+                static_cast<const bf16_t*>(a.ws2), a.sched.n_unique, a.sched.unique,
                 a.sched.offsets, a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k,
-                Tk, ldh, a.max_unique, static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
+                Tk, R, a.max_unique, static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
     switch (pick_ntiles(a.T, a.k, a.max_unique)) {
-      case 1: return launch_bf16<1>(p, groups, s);
-      case 2: return launch_bf16<2>(p, groups, s);
-      default: return launch_bf16<4>(p, groups, s);
+      case 1: return launch_bf16<1>(p, ldh, groups, s);
+      case 2: return launch_bf16<2>(p, ldh, groups, s);
+      default: return launch_bf16<4>(p, ldh, groups, s);
     }
   }
-  void* hbuf = a.workspace;
+  float* hbuf = static_cast<float*>(a.workspace);
   dim3 g_gu((ldh + kThreads - 1) / kThreads, groups), g_dn((a.H + kThreads - 1) / kThreads, groups);
   ffn_gateup_f32_kernel<<<g_gu, kThreads, 0, s>>>(
-      static_cast<const float*>(a.x), static_cast<const float*>(a.wg), static_cast<const float*>(a.wu),
-      static_cast<const float*>(a.wsg), static_cast<const float*>(a.wsu), a.sched.n_unique,
-      a.sched.unique, a.sched.offsets, a.sched.row_token, a.T, a.H, a.I, a.I_s, Tk, a.max_unique, ldh,
-      static_cast<float*>(hbuf));
+      static_cast<const float*>(a.x), static_cast<const float*>(a.w13), static_cast<const float*>(a.ws13),
+      a.sched.n_unique, a.sched.unique, a.sched.offsets, a.sched.row_token, a.T, a.H, a.I, a.I_s, Tk,
+      a.max_unique, ldh, hbuf);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_down_f32_kernel<<<g_dn, kThreads, 0, s>>>(
-      static_cast<const float*>(a.wd), static_cast<const float*>(a.wsd), a.sched.n_unique,
+      static_cast<const float*>(a.w2), static_cast<const float*>(a.ws2), a.sched.n_unique,
       a.sched.unique, a.sched.offsets, a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s,
-      a.k, Tk, a.max_unique, ldh, static_cast<const float*>(hbuf), a.slot_out, a.shared_out);
+      a.k, Tk, a.max_unique, ldh, hbuf, a.slot_out, a.shared_out);
   return hipGetLastError();
 }
 

@@ -13,6 +13,9 @@
 // f32: one thread per (token, expert) dot product.
 // Softmax: one wave per token row; all partial loads of a pass are issued
 // together and the row is staged in LDS (one read pass, one write pass).
+// Optionally the kernel also stores x in the chunk-major layout the expert
+// FFN reads ([H/c][T][c], c elements per 16-byte chunk): the workgroups of the
+// first expert tile already hold every 16-byte chunk of x in registers.
 #include <algorithm>
 
 #include "dmoe_common.h"
@@ -79,7 +82,7 @@ __device__ void softmax_row(const float* pr, size_t plane, int S, const float* b
 
 __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, int T, int H, int E, int S,
-    float* __restrict__ part) {
+    float* __restrict__ part, bf16_t* __restrict__ xk) {
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int q = lane >> 4;   // k-group of the MFMA operand / row group of the result
@@ -126,6 +129,19 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
 #pragma unroll
           for (int u = 0; u < 2; ++u)
             acc[r][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s][r], b[s][u], acc[r][u], 0, 0, 0);
+    if (xk && blockIdx.y == 0) {
+      // chunk (kbeg + 32*(sc+s))/8 + q of token t0 + 16r + c
+#pragma unroll
+      for (int s = 0; s < kRouterSteps; ++s)
+        if (s < ns)
+#pragma unroll
+          for (int r = 0; r < 2; ++r) {
+            const int t = t0 + r * 16 + c;
+            const int j = ((kbeg + (sc + s) * 32) >> 3) + q;
+            if (t < T)
+              *reinterpret_cast<bf16x8*>(xk + (static_cast<size_t>(j) * T + t) * 8) = a[s][r];
+          }
+    }
   }
 
   __shared__ f32x4 red[3][4][kWave];
@@ -158,11 +174,13 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
 
 __global__ __launch_bounds__(256) void router_logits_f32_kernel(
     const float* __restrict__ x, const float* __restrict__ w, int T, int H, int E,
-    float* __restrict__ part) {
+    float* __restrict__ part, float* __restrict__ xk) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   const int t = blockIdx.y;
-  if (e >= E) return;
   const float* xr = x + static_cast<size_t>(t) * H;
+  if (xk && blockIdx.x == 0)
+    for (int h = threadIdx.x; h < H; h += blockDim.x) xk[(static_cast<size_t>(h >> 2) * T + t) * 4 + (h & 3)] = xr[h];
+  if (e >= E) return;
   const float* wr = w + static_cast<size_t>(e) * H;
   float acc = 0.f;
   for (int h = 0; h < H; ++h) acc = fmaf(xr[h], wr[h], acc);
@@ -191,9 +209,6 @@ int router_splits(int T, int H, int E) {
   while (S < kMaxSplits && tiles * S < 128 && (H / 128) % (2 * S) == 0) S *= 2;
   return S;
 }
-
-
-
 }  // namespace
 
 size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt) {
@@ -203,8 +218,8 @@ size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt) {
 }
 
 hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
-                         int H, int E, float* logits, float* probs, void* workspace,
-                         size_t ws_bytes, hipStream_t s) {
+                         int H, int E, float* logits, float* probs, void* x_chunked,
+                         void* workspace, size_t ws_bytes, hipStream_t s) {
   int S = 1;
   float* part = probs;  // S == 1: the softmax reads the logits in place
   const size_t lds = static_cast<size_t>(4) * E * sizeof(float);
@@ -216,11 +231,13 @@ hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_d
     }
     dim3 grid((T + kRouterTile - 1) / kRouterTile, (E + kRouterTile - 1) / kRouterTile, S);
     router_logits_bf16_kernel<<<grid, 256, 0, s>>>(static_cast<const bf16_t*>(x),
-                                                    static_cast<const bf16_t*>(w), T, H, E, S, part);
+                                                    static_cast<const bf16_t*>(w), T, H, E, S, part,
+                                                    static_cast<bf16_t*>(x_chunked));
   } else {
     dim3 grid((E + 255) / 256, T);
     router_logits_f32_kernel<<<grid, 256, 0, s>>>(static_cast<const float*>(x),
-                                                   static_cast<const float*>(w), T, H, E, part);
+                                                   static_cast<const float*>(w), T, H, E, part,
+                                                   static_cast<float*>(x_chunked));
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

@@ -7,12 +7,38 @@
 
 on the current stream.  It allocates only in its constructor, so a forward
 can be captured in a HIP graph.  Nothing is computed on the host.
+
+Expert weights are used in the library's packed layout: :func:`pack_weights`
+converts a layer's weights once (dmoe_pack_expert_weights).
 """
 from __future__ import annotations
 
 import torch
 
 from . import lib
+
+
+def pack_weights(w: dict, keep_unpacked: bool = False) -> dict:
+    """Weights of one layer for :meth:`MoELayer.forward`: the router weights
+    and bias as given, the routed and shared experts packed by the library.
+
+    ``w`` holds w_router, bias (or None), w_gate/w_up [E][I][H], w_down
+    [E][H][I] and optionally ws_gate/ws_up [I_s][H], ws_down [H][I_s].
+    """
+    out = {"w_router": w["w_router"], "bias": w.get("bias")}
+    E, I, H = w["w_gate"].shape
+    out["w13"] = torch.empty((2 * E * I * H,), dtype=w["w_gate"].dtype, device=w["w_gate"].device)
+    out["w2"] = torch.empty((E * H * I,), dtype=w["w_gate"].dtype, device=w["w_gate"].device)
+    lib.dmoe_pack_expert_weights(w["w_gate"], w["w_up"], w["w_down"], E, H, I, out["w13"], out["w2"])
+    if w.get("ws_gate") is not None:
+        I_s = w["ws_gate"].shape[0]
+        out["ws13"] = torch.empty((2 * I_s * H,), dtype=w["ws_gate"].dtype, device=w["ws_gate"].device)
+        out["ws2"] = torch.empty((H * I_s,), dtype=w["ws_gate"].dtype, device=w["ws_gate"].device)
+        lib.dmoe_pack_expert_weights(w["ws_gate"], w["ws_up"], w["ws_down"], 1, H, I_s, out["ws13"],
+                                     out["ws2"])
+    if keep_unpacked:
+        out.update({k: v for k, v in w.items() if k not in out})
+    return out
 
 
 class MoELayer:
@@ -26,6 +52,8 @@ class MoELayer:
         f32 = dict(dtype=torch.float32, device=device)
         i32 = dict(dtype=torch.int32, device=device)
         self.logits = torch.empty((T, E), **f32) if keep_logits else None
+        # x in the chunk-major layout the expert FFN reads (written by the router)
+        self.x_chunked = torch.empty((T * H,), dtype=dtype, device=device)
         self.probs = torch.empty((T, E), **f32)
         self.block_scores = torch.empty((n_blocks, E), **f32)
         self.block_experts = torch.empty((n_blocks, k), **i32)
@@ -50,7 +78,8 @@ class MoELayer:
 
     def route(self, x, w_router, bias=None, routing: str = "block", stream=None):
         T, H, E, k = self.T, self.H, self.E, self.k
-        lib.dmoe_router_logits(x, w_router, bias, T, H, E, self.logits, self.probs, self.router_ws, stream)
+        lib.dmoe_router_logits(x, w_router, bias, T, H, E, self.logits, self.probs, self.x_chunked,
+                               self.router_ws, stream)
         if routing == "block":
             lib.dmoe_block_aggregate_topk(self.probs, self.NB, self.bs, E, k, self.block_scores,
                                           self.block_experts, self.combine_w, self.block_gap, stream)
@@ -62,20 +91,21 @@ class MoELayer:
         else:
             raise ValueError(f"routing must be 'block' or 'token', not {routing!r}")
 
-    def experts_ffn(self, x, w: dict, routing: str = "block", stream=None):
-        lib.dmoe_expert_ffn(x, w["w_gate"], w["w_up"], w["w_down"], w.get("ws_gate"), w.get("ws_up"),
-                            w.get("ws_down"), self.T, self.H, self.E, self.I, self.I_s, self.k,
-                            self.max_unique(routing), self.sched, self.slot_out, self.shared_out,
-                            self.workspace, stream)
+    def experts_ffn(self, w: dict, routing: str = "block", stream=None):
+        """Expert FFN on the chunk-major copy of x that :meth:`route` stored."""
+        lib.dmoe_expert_ffn(self.x_chunked, w["w13"], w["w2"], w.get("ws13"), w.get("ws2"), self.T, self.H,
+                            self.E, self.I, self.I_s, self.k, self.max_unique(routing), self.sched,
+                            self.slot_out, self.shared_out, self.workspace, stream)
 
     def combine(self, stream=None):
         lib.dmoe_combine(self.slot_out, self.combine_w, self.shared_out, self.T, self.H, self.k, self.y,
                          stream)
 
     def forward(self, x, w: dict, routing: str = "block", stream=None) -> torch.Tensor:
-        """Whole layer on hidden states x[T, H]; returns (a view of) y[T, H]."""
+        """Whole layer on hidden states x[T, H] with weights from
+        :func:`pack_weights`; returns (a view of) y[T, H]."""
         self.route(x, w["w_router"], w.get("bias"), routing, stream)
-        self.experts_ffn(x, w, routing, stream)
+        self.experts_ffn(w, routing, stream)
         self.combine(stream)
         return self.y
 

@@ -29,8 +29,8 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 
 # Every symbol include/dmoe.h declares.
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
-           "dmoe_build_expert_schedule", "dmoe_ffn_workspace_size", "dmoe_expert_ffn",
-           "dmoe_combine", "dmoe_last_error", "dmoe_version")
+           "dmoe_build_expert_schedule", "dmoe_pack_activations", "dmoe_pack_expert_weights",
+           "dmoe_ffn_workspace_size", "dmoe_expert_ffn", "dmoe_combine", "dmoe_last_error", "dmoe_version")
 
 
 class DmoeError(RuntimeError):
@@ -50,12 +50,14 @@ _I = ctypes.c_int
 _S = ctypes.c_size_t
 _SIGS = {
     "dmoe_router_workspace_size": ([_I, _I, _I, _I], _S),
-    "dmoe_router_logits": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _S, _P], _I),
+    "dmoe_router_logits": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P], _I),
     "dmoe_block_aggregate_topk": ([_P, _I, _I, _I, _I, _P, _P, _P, _P, _P], _I),
     "dmoe_token_topk": ([_P, _I, _I, _I, _P, _P, _P, _P], _I),
     "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
+    "dmoe_pack_activations": ([_P, _I, _I, _I, _P, _P], _I),
+    "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
-    "dmoe_expert_ffn": ([_P] * 7 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
+    "dmoe_expert_ffn": ([_P] * 5 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
     "dmoe_last_error": ([], ctypes.c_char_p),
     "dmoe_version": ([], ctypes.c_char_p),
@@ -118,10 +120,11 @@ def dmoe_router_workspace_size(T, H, E, dt) -> int:
     return int(load().dmoe_router_workspace_size(T, H, E, dt))
 
 
-def dmoe_router_logits(x, w_router, bias, T, H, E, logits, probs, workspace=None, stream=None):
+def dmoe_router_logits(x, w_router, bias, T, H, E, logits, probs, x_chunked=None, workspace=None,
+                       stream=None):
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().dmoe_router_logits(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), T, H, E,
-                                     ptr(logits), ptr(probs), ptr(workspace), nbytes,
+                                     ptr(logits), ptr(probs), ptr(x_chunked), ptr(workspace), nbytes,
                                      stream_handle(stream)))
 
 
@@ -161,17 +164,25 @@ def dmoe_build_expert_schedule(experts, n_groups, group_size, k, E, sched: Sched
                                              stream_handle(stream)))
 
 
+def dmoe_pack_activations(x, T, H, x_chunked, stream=None):
+    _check(load().dmoe_pack_activations(ptr(x), dtype_code(x), T, H, ptr(x_chunked), stream_handle(stream)))
+
+
+def dmoe_pack_expert_weights(w_gate, w_up, w_down, n_experts, H, I, w13, w2, stream=None):
+    _check(load().dmoe_pack_expert_weights(ptr(w_gate), ptr(w_up), ptr(w_down), dtype_code(w_gate),
+                                           n_experts, H, I, ptr(w13), ptr(w2), stream_handle(stream)))
+
+
 def dmoe_ffn_workspace_size(T, I, I_s, k, dt) -> int:
     return int(load().dmoe_ffn_workspace_size(T, I, I_s, k, dt))
 
 
-def dmoe_expert_ffn(x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, T, H, E, I, I_s, k,
-                    max_unique, sched: Schedule, slot_out, shared_out, workspace, stream=None):
-    _check(load().dmoe_expert_ffn(ptr(x), ptr(w_gate), ptr(w_up), ptr(w_down), ptr(ws_gate),
-                                  ptr(ws_up), ptr(ws_down), dtype_code(x), T, H, E, I, I_s, k,
-                                  max_unique, sched.as_c(), ptr(slot_out), ptr(shared_out),
-                                  ptr(workspace), workspace.numel() * workspace.element_size(),
-                                  stream_handle(stream)))
+def dmoe_expert_ffn(x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_unique, sched: Schedule,
+                    slot_out, shared_out, workspace, stream=None):
+    _check(load().dmoe_expert_ffn(ptr(x_chunked), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
+                                  dtype_code(x_chunked), T, H, E, I, I_s, k, max_unique, sched.as_c(),
+                                  ptr(slot_out), ptr(shared_out), ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), stream_handle(stream)))
 
 
 def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):

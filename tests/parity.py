@@ -14,6 +14,7 @@ import numpy as np
 import torch
 
 import oracle as O
+from paper_2605_30876_amd.layer import pack_weights
 
 BF16_TOL = 2e-2   # max|y - y_ref| <= 2e-2 * RMS(y_ref) for bf16 weights
 F32_TOL = 1e-4    # ... <= 1e-4 * RMS(y_ref) for the fp32 layer
@@ -50,10 +51,15 @@ def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: lis
     return out
 
 
-def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, check_determinism=True):
-    """Run the GPU forward on d_gpu, compare with the oracle, return a report."""
+def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, check_determinism=True,
+                  packed=None):
+    """Run the GPU forward on d_gpu, compare with the oracle, return a report.
+
+    The GPU runs on the library's packed copy of the weights (``packed``, or
+    packed here); the oracle on the unpacked tensors of d_gpu."""
     x = d_gpu["x"]
-    y = layer.forward(x, d_gpu, routing).clone()
+    wp = packed if packed is not None else pack_weights(d_gpu)
+    y = layer.forward(x, wp, routing).clone()
     torch.cuda.synchronize()
     report = {"near_ties": []}
 
@@ -134,7 +140,7 @@ def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, che
     assert err <= tol_for(cfg), f"max|y - y_ref| = {err:.3g} * RMS(y_ref) > {tol_for(cfg)}"
 
     if check_determinism:
-        y2 = layer.forward(x, d_gpu, routing).clone()
+        y2 = layer.forward(x, wp, routing).clone()
         torch.cuda.synchronize()
         assert torch.equal(y, y2), "two runs differ bitwise"
     return report

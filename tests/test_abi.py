@@ -61,14 +61,14 @@ def status(L, name, *args):
 
 def test_router_validation(L, buf):
     _, p = buf
-    st, msg = status(L, "dmoe_router_logits", None, p, None, 1, 32, 2048, 256, None, p, None, 0, None)
+    st, msg = status(L, "dmoe_router_logits", None, p, None, 1, 32, 2048, 256, None, p, None, None, 0, None)
     assert st == lib.DMOE_ERR_INVALID_ARG and "must not be NULL" in msg
-    assert status(L, "dmoe_router_logits", p, p, None, 7, 32, 2048, 256, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p, p, None, 1, 0, 2048, 256, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 5000, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p + 4, p, None, 1, 32, 2048, 256, None, p, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 256, None, p, p + 8, 64, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    st, msg = status(L, "dmoe_router_logits", p, p, None, 1, 32, 2000, 256, None, p, None, 0, None)
+    assert status(L, "dmoe_router_logits", p, p, None, 7, 32, 2048, 256, None, p, None, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 0, 2048, 256, None, p, None, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 5000, None, p, None, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p + 4, p, None, 1, 32, 2048, 256, None, p, None, None, 0, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, "dmoe_router_logits", p, p, None, 1, 32, 2048, 256, None, p, None, p + 8, 64, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    st, msg = status(L, "dmoe_router_logits", p, p, None, 1, 32, 2000, 256, None, p, None, None, 0, None)
     assert st == lib.DMOE_ERR_UNSUPPORTED and "H % 128" in msg
 
 
@@ -113,34 +113,67 @@ def test_schedule_validation(L, buf):
 
 
 def _ffn(L, p, **over):
-    a = dict(x=p, wg=p, wu=p, wd=p, wsg=p, wsu=p, wsd=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512,
-             I_s=512, k=8, max_unique=8, sched=lib.dmoe_schedule(p, p, p, p, p), slot=p, shared=p, ws=p,
-             ws_bytes=1 << 30)
+    a = dict(x=p, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512, k=8,
+             max_unique=8, sched=lib.dmoe_schedule(p, p, p, p, p), slot=p, shared=p, ws=p, ws_bytes=1 << 30)
     a.update(over)
-    return status(L, "dmoe_expert_ffn", a["x"], a["wg"], a["wu"], a["wd"], a["wsg"], a["wsu"], a["wsd"],
-                  a["dt"], a["T"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_unique"], a["sched"],
-                  a["slot"], a["shared"], a["ws"], a["ws_bytes"], None)
+    return status(L, "dmoe_expert_ffn", a["x"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"], a["T"],
+                  a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_unique"], a["sched"], a["slot"],
+                  a["shared"], a["ws"], a["ws_bytes"], None)
 
 
 def test_ffn_validation(L, buf):
     _, p = buf
     INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
     assert _ffn(L, p, x=None)[0] == INV
+    assert _ffn(L, p, w13=None)[0] == INV
     assert _ffn(L, p, ws=None)[0] == INV
     assert _ffn(L, p, dt=5)[0] == INV
     assert _ffn(L, p, k=0)[0] == INV
     assert _ffn(L, p, max_unique=0)[0] == INV
     assert _ffn(L, p, max_unique=257)[0] == INV
-    assert _ffn(L, p, wsd=None)[0] == INV            # shared triple inconsistent
+    assert _ffn(L, p, ws2=None)[0] == INV            # shared pair inconsistent
     assert _ffn(L, p, shared=None)[0] == INV
     assert _ffn(L, p, I_s=0)[0] == INV               # shared pointers set without a shared expert
     st, msg = _ffn(L, p, ws_bytes=100)
     assert st == INV and "workspace" in msg
     assert _ffn(L, p, slot=p + 4)[0] == INV
+    assert _ffn(L, p, w2=p + 8)[0] == INV
     assert _ffn(L, p, sched=lib.dmoe_schedule(p, None, p, p, p))[0] == INV
+    assert _ffn(L, p, H=2004)[0] == INV              # not a whole number of 16-byte chunks
+    assert _ffn(L, p, dt=lib.DMOE_F32, H=98, ws_bytes=1 << 30)[0] == INV
     assert _ffn(L, p, H=2000)[0] == UNS
     assert _ffn(L, p, I=500)[0] == UNS
     assert _ffn(L, p, E=1024, max_unique=8)[0] == UNS
+    st, msg = _ffn(L, p, T=1 << 20, k=64, E=512, max_unique=64, I=1024, I_s=1024, H=128)
+    assert st == INV and "too large" in msg
+
+
+def test_pack_activations_validation(L, buf):
+    _, p = buf
+    f, INV = "dmoe_pack_activations", lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, None, lib.DMOE_BF16, 32, 2048, p + 4096, None)[0] == INV
+    assert status(L, f, p, lib.DMOE_BF16, 32, 2048, None, None)[0] == INV
+    assert status(L, f, p, lib.DMOE_BF16, 32, 2048, p, None)[0] == INV      # aliasing
+    assert status(L, f, p, lib.DMOE_BF16, 0, 2048, p + 4096, None)[0] == INV
+    assert status(L, f, p, lib.DMOE_BF16, 32, 2044, p + 4096, None)[0] == INV
+    assert status(L, f, p, lib.DMOE_F32, 32, 2046, p + 4096, None)[0] == INV
+    assert status(L, f, p, 3, 32, 2048, p + 4096, None)[0] == INV
+    assert status(L, f, p + 8, lib.DMOE_BF16, 32, 2048, p + 4096, None)[0] == INV
+
+
+def test_pack_expert_weights_validation(L, buf):
+    _, p = buf
+    f, INV, UNS = "dmoe_pack_expert_weights", lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    q, r = p + 4096, p + 8192
+    assert status(L, f, None, p + 16, p + 32, lib.DMOE_BF16, 8, 128, 128, q, r, None)[0] == INV
+    assert status(L, f, p, p + 16, p + 32, lib.DMOE_BF16, 8, 128, 128, None, r, None)[0] == INV
+    assert status(L, f, p, p + 16, p + 32, lib.DMOE_BF16, 8, 128, 128, p, r, None)[0] == INV  # aliasing
+    assert status(L, f, p, p + 16, p + 32, lib.DMOE_BF16, 8, 128, 128, q, q, None)[0] == INV
+    assert status(L, f, p, p + 16, p + 32, lib.DMOE_BF16, 0, 128, 128, q, r, None)[0] == INV
+    assert status(L, f, p, p + 16, p + 32, lib.DMOE_BF16, 8, 128, 128, q + 4, r, None)[0] == INV
+    assert status(L, f, p, p + 16, p + 32, 9, 8, 128, 128, q, r, None)[0] == INV
+    st, msg = status(L, f, p, p + 16, p + 32, lib.DMOE_BF16, 8, 128, 96, q, r, None)
+    assert st == UNS and "multiples of 128" in msg
 
 
 def test_combine_validation(L, buf):

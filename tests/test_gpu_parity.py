@@ -7,7 +7,7 @@ import torch
 import oracle as O
 from dmoe_synth import get_config, make_inputs
 from paper_2605_30876_amd import lib
-from paper_2605_30876_amd.layer import MoELayer
+from paper_2605_30876_amd.layer import MoELayer, pack_weights
 from parity import run_and_check
 
 pytestmark = pytest.mark.gpu
@@ -67,12 +67,14 @@ def test_workspace_reuse_across_inputs(gpu_lib, name):
     layer = _layer(cfg)
     dev = "cuda"
     inputs = [make_inputs(cfg, seed=s, device=dev) for s in (0, 7)]
+    packed = [pack_weights(d) for d in inputs]
     for routing in ("block", "token", "block"):
-        layer.forward(inputs[0]["x"], inputs[0], routing)
+        layer.forward(inputs[0]["x"], packed[0], routing)
         rep = run_and_check(cfg, inputs[1], routing, layer, sample_tokens=[0, 5, cfg.T - 1],
-                            check_determinism=False)
+                            check_determinism=False, packed=packed[1])
         _say("  ", routing, {k: v for k, v in rep.items() if k != "near_ties"})
         inputs.reverse()
+        packed.reverse()
 
 
 @pytest.mark.parametrize("name", ["small_bf16", "small_f32"])
@@ -80,14 +82,15 @@ def test_block_size_one_equals_token_routing(gpu_lib, name):
     base = get_config(name)
     cfg = base.with_(name=base.name + "_bs1", NB=base.T if base.T <= 64 else 37, bs=1)
     d = _to_gpu(make_inputs(cfg, seed=5))
+    w = pack_weights(d)
     layer = _layer(cfg)
-    yb = layer.forward(d["x"], d, "block").clone()
+    yb = layer.forward(d["x"], w, "block").clone()
     eb = layer.block_experts.clone()
-    yt = layer.forward(d["x"], d, "token").clone()
+    yt = layer.forward(d["x"], w, "token").clone()
     torch.cuda.synchronize()
     assert torch.equal(eb, layer.token_experts)
     assert torch.equal(yb, yt)
-    run_and_check(cfg, d, "block", layer)
+    run_and_check(cfg, d, "block", layer, packed=w)
 
 
 @pytest.mark.parametrize("routing", ["block", "token"])
@@ -150,11 +153,12 @@ def test_bf16_output_is_rounded_fp32_output(gpu_lib, name):
     """Storing the layer output as bf16 rounds the fp32 result once (RNE)."""
     cfg = get_config(name)
     d = make_inputs(cfg, seed=0, device="cuda")
+    w = pack_weights(d)
     l32 = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, out_dtype=torch.float32)
     l16 = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, out_dtype=torch.bfloat16)
     for routing in ("block", "token"):
-        y32 = l32.forward(d["x"], d, routing).clone()
-        y16 = l16.forward(d["x"], d, routing).clone()
+        y32 = l32.forward(d["x"], w, routing).clone()
+        y16 = l16.forward(d["x"], w, routing).clone()
         torch.cuda.synchronize()
         assert y16.dtype == torch.bfloat16
         assert torch.equal(y16, y32.to(torch.bfloat16))
