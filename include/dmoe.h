@@ -19,7 +19,8 @@
  *                              rows, plus the always-on shared expert
  *   dmoe_combine               y_t = sum_j w[t,j] * FFN_{e_tj}(x_t) + FFN_s(x_t)
  *
- * and two layout conversions for the expert FFN's operands:
+ * dmoe_route_block / dmoe_route_token run the first three (or the token
+ * variant) as one call with fewer kernel launches; and two layout conversions for the expert FFN's operands:
  *
  *   dmoe_pack_expert_weights   expert weights -> the FFN's packed layout
  *                              (once, when the model is loaded)
@@ -170,6 +171,33 @@ dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* to
  */
 dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int group_size,
                                        int k, int E, dmoe_schedule sched, void* stream);
+
+/*
+ * The whole routing stage of one forward in one call, block-level:
+ *   dmoe_router_logits(x, ..., logits, probs, x_chunked, workspace)
+ *   dmoe_block_aggregate_topk(probs, n_blocks, block_size, E, k, ...)
+ *   dmoe_build_expert_schedule(block_experts, n_blocks, block_size, k, E, sched)
+ * with T = n_blocks*block_size, arguments as documented there, and results
+ * bit-identical to that sequence.  A small forward (all T x E probabilities
+ * fit in on-chip memory) runs as two kernels instead of four.
+ * Limits: the union of the three calls' limits (E <= 512).
+ */
+dmoe_status dmoe_route_block(const void* x, const void* w_router, const float* bias, dmoe_dtype dt,
+                             int n_blocks, int block_size, int H, int E, int k, float* logits,
+                             float* probs, void* x_chunked, float* block_scores, int32_t* block_experts,
+                             float* combine_w, float* gap, dmoe_schedule sched, void* workspace,
+                             size_t ws_bytes, void* stream);
+
+/*
+ * The same for token-level routing (the baseline):
+ *   dmoe_router_logits, dmoe_token_topk(probs, T, E, k, token_experts, ...),
+ *   dmoe_build_expert_schedule(token_experts, T, 1, k, E, sched)
+ * bit-identical to that sequence.
+ */
+dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* bias, dmoe_dtype dt,
+                             int T, int H, int E, int k, float* logits, float* probs, void* x_chunked,
+                             int32_t* token_experts, float* combine_w, float* gap, dmoe_schedule sched,
+                             void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Hidden states x [T][H] (row-major, type dt) -> x_chunked [T*H] in the

@@ -1,10 +1,20 @@
 // Weighted combine of the routed expert outputs and the shared expert:
 //   y[t][h] = sum_j w[t][j] * slot_out[t][j][h] (+ shared_out[t][h])
-// summed in slot order in fp32.  One thread per four consecutive outputs.
+// summed in slot order in fp32.  One thread per four consecutive outputs; a
+// batch of slot rows is loaded at once (one memory round trip per batch).
 #include "dmoe_common.h"
 
 namespace dmoe {
 namespace {
+
+constexpr int kSlotBatch = 8;  // slot loads in flight together
+
+__device__ __forceinline__ void store4(float* dst, const f32x4& v) { *reinterpret_cast<f32x4*>(dst) = v; }
+__device__ __forceinline__ void store4(bf16_t* dst, const f32x4& v) {
+  const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+  const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+  *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+}
 
 template <typename OutT>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ slot_out,
@@ -19,14 +29,23 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   const float* wt = w + static_cast<size_t>(t) * k;
   const float* so = slot_out + static_cast<size_t>(t) * k * H + h;
-  for (int j = 0; j < k; ++j) {
-    const f32x4 v = *reinterpret_cast<const f32x4*>(so + static_cast<size_t>(j) * H);
-    acc += wt[j] * v;
-  }
-  if (shared_out) acc += *reinterpret_cast<const f32x4*>(shared_out + static_cast<size_t>(t) * H + h);
-  OutT* dst = y + static_cast<size_t>(t) * H + h;
+  const f32x4 sh = shared_out ? *reinterpret_cast<const f32x4*>(shared_out + static_cast<size_t>(t) * H + h)
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j0 = 0; j0 < k; j0 += kSlotBatch) {
+    f32x4 v[kSlotBatch];
+    float wj[kSlotBatch];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) store_from_f32<OutT>(dst + i, acc[i]);
+    for (int u = 0; u < kSlotBatch; ++u)
+      if (j0 + u < k) {
+        v[u] = *reinterpret_cast<const f32x4*>(so + static_cast<size_t>(j0 + u) * H);
+        wj[u] = wt[j0 + u];
+      }
+#pragma unroll
+    for (int u = 0; u < kSlotBatch; ++u)
+      if (j0 + u < k) acc += wj[u] * v[u];  // slot order
+  }
+  if (shared_out) acc += sh;
+  store4(y + static_cast<size_t>(t) * H + h, acc);
 }
 
 }  // namespace

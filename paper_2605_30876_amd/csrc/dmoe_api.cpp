@@ -149,6 +149,94 @@ dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int
                     __func__);
 }
 
+dmoe_status dmoe_route_block(const void* x, const void* w_router, const float* bias, dmoe_dtype dt,
+                             int n_blocks, int block_size, int H, int E, int k, float* logits,
+                             float* probs, void* x_chunked, float* block_scores, int32_t* block_experts,
+                             float* combine_w, float* gap, dmoe_schedule sched, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  REQUIRE(x && w_router && probs && block_experts && combine_w,
+          "x, w_router, probs, block_experts and combine_w must not be NULL");
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+          "every schedule array must be set");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
+  REQUIRE(block_size >= 1 && block_size <= 4096, "block_size=%d must be in [1, 4096]", block_size);
+  REQUIRE(H >= 1, "H=%d must be >= 1", H);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  const long T = static_cast<long>(n_blocks) * block_size;
+  REQUIRE(T * E <= kIntLimit && T * H <= kIntLimit && T * k < kIntLimit, "T*E, T*H and T*k must fit in int32");
+  ALIGNED(x);
+  ALIGNED(w_router);
+  ALIGNED(bias);
+  ALIGNED(logits);
+  ALIGNED(probs);
+  ALIGNED(x_chunked);
+  ALIGNED(block_scores);
+  ALIGNED(block_experts);
+  ALIGNED(combine_w);
+  ALIGNED(gap);
+  ALIGNED(workspace);
+  ALIGNED(sched.n_unique);
+  ALIGNED(sched.unique);
+  ALIGNED(sched.offsets);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
+  if (x_chunked) {
+    REQUIRE(H % dmoe::chunk_elems(dt) == 0, "x_chunked needs H %% %d == 0 (H=%d)", dmoe::chunk_elems(dt), H);
+  }
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
+  }
+  SUPPORT(E <= kMaxScheduleE, "the schedule supports E <= %d (E=%d)", kMaxScheduleE, E);
+  dmoe::RouteArgs a{x, w_router, bias, static_cast<int>(T), H, E, k, block_size, true, logits, probs,
+                    x_chunked, block_scores, block_experts, combine_w, gap, sched, workspace,
+                    workspace ? ws_bytes : 0};
+  return hip_status(dmoe::launch_route(a, dt, static_cast<hipStream_t>(stream)), __func__);
+}
+
+dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* bias, dmoe_dtype dt,
+                             int T, int H, int E, int k, float* logits, float* probs, void* x_chunked,
+                             int32_t* token_experts, float* combine_w, float* gap, dmoe_schedule sched,
+                             void* workspace, size_t ws_bytes, void* stream) {
+  REQUIRE(x && w_router && probs && token_experts && combine_w,
+          "x, w_router, probs, token_experts and combine_w must not be NULL");
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+          "every schedule array must be set");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(static_cast<long>(T) * E <= kIntLimit && static_cast<long>(T) * H <= kIntLimit &&
+              static_cast<long>(T) * k < kIntLimit,
+          "T*E, T*H and T*k must fit in int32");
+  ALIGNED(x);
+  ALIGNED(w_router);
+  ALIGNED(bias);
+  ALIGNED(logits);
+  ALIGNED(probs);
+  ALIGNED(x_chunked);
+  ALIGNED(token_experts);
+  ALIGNED(combine_w);
+  ALIGNED(gap);
+  ALIGNED(workspace);
+  ALIGNED(sched.n_unique);
+  ALIGNED(sched.unique);
+  ALIGNED(sched.offsets);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
+  if (x_chunked) {
+    REQUIRE(H % dmoe::chunk_elems(dt) == 0, "x_chunked needs H %% %d == 0 (H=%d)", dmoe::chunk_elems(dt), H);
+  }
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
+  }
+  SUPPORT(E <= kMaxScheduleE, "the schedule supports E <= %d (E=%d)", kMaxScheduleE, E);
+  dmoe::RouteArgs a{x, w_router, bias, T, H, E, k, 1, false, logits, probs, x_chunked, nullptr, token_experts,
+                    combine_w, gap, sched, workspace, workspace ? ws_bytes : 0};
+  return hip_status(dmoe::launch_route(a, dt, static_cast<hipStream_t>(stream)), __func__);
+}
+
 dmoe_status dmoe_pack_activations(const void* x, dmoe_dtype dt, int T, int H, void* x_chunked,
                                   void* stream) {
   REQUIRE(x && x_chunked, "x and x_chunked must not be NULL");

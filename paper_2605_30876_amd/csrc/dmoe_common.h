@@ -60,12 +60,42 @@ hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_d
                          int H, int E, float* logits, float* probs, void* x_chunked,
                          void* workspace, size_t ws_bytes, hipStream_t s);
 size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt);
+// Router logits only, as S partial planes [S][T][E] (summed in slice order by
+// the softmax) in *part: the workspace when it is large enough, else S = 1
+// and *part = probs.
+hipError_t launch_router_partials(const void* x, const void* w, dmoe_dtype dt, int T, int H, int E,
+                                  float* probs, void* x_chunked, void* workspace, size_t ws_bytes,
+                                  hipStream_t s, float** part, int* S);
 hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, float* scores,
                              int32_t* experts, float* w, float* gap, hipStream_t s);
 hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* experts, float* w,
                              float* gap, hipStream_t s);
 hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, int E,
                            dmoe_schedule sched, hipStream_t s);
+
+// The whole routing stage: router, selection (blocks of gs tokens when block,
+// else per token), combine weights and schedule.  Small forwards run the
+// selection and schedule in one workgroup after the router; others chain the
+// separate launchers.  Results are identical either way.
+struct RouteArgs {
+  const void* x;
+  const void* w;
+  const float* bias;
+  int T, H, E, k, gs;
+  bool block;
+  float* logits;
+  float* probs;
+  void* x_chunked;
+  float* block_scores;
+  int32_t* experts;
+  float* combine_w;
+  float* gap;
+  dmoe_schedule sched;
+  void* workspace;
+  size_t ws_bytes;
+};
+hipError_t launch_route(const RouteArgs& a, dmoe_dtype dt, hipStream_t s);
+bool route_fused_fits(int T, int E, int k, int gs, bool block);
 
 // 16-byte chunks: elements of one chunk of the chunk-major activation layout.
 inline int chunk_elems(dmoe_dtype dt) { return dt == DMOE_F32 ? 4 : 8; }

@@ -178,11 +178,14 @@ __device__ __forceinline__ void zero(f32x4 (&acc)[NT]) {
   for (int ct = 0; ct < NT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
+// Occupancy floors (waves per SIMD) for the two-tile variants, which serve
+// block-routed decode steps: 3 (gate/up) and 4 (down) keep every workgroup of
+// such a launch resident at once instead of leaving a second partial round.
 // grid (ldh / 8, groups): packed gate/up tile `it` = 8 intermediate units.
 // Wave w reduces over hidden chunks [w*H/32, (w+1)*H/32) (K-steps
 // [w*H/128, (w+1)*H/128)).
 template <int NT, int KMAX>
-__global__ __launch_bounds__(kThreads) void ffn_gateup_bf16_kernel(FfnParams p) {
+__global__ __launch_bounds__(kThreads, NT == 2 ? 3 : 1) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
     return;
@@ -231,7 +234,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_bf16_kernel(FfnParams p) 
 
 // grid (H / 16, groups): packed down tile `jt` = 16 output features.
 template <int NT, int KMAX>
-__global__ __launch_bounds__(kThreads) void ffn_down_bf16_kernel(FfnParams p) {
+__global__ __launch_bounds__(kThreads, NT == 2 ? 4 : 1) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
     return;

@@ -18,67 +18,15 @@
 // first expert tile already hold every 16-byte chunk of x in registers.
 #include <algorithm>
 
-#include "dmoe_common.h"
+#include "route_dev.h"
 
 namespace dmoe {
 namespace {
 
+using dev::kMaxSplits;
+
 constexpr int kRouterTile = 32;
 constexpr int kRouterSteps = 8;  // K steps of 32 per load burst
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-  return v;
-}
-
-constexpr int kMaxSplits = 4;
-
-// Softmax of one token row from S partial planes (slice order) + bias; z is
-// the wave's LDS row of E floats.  A lane handles 4 elements (e = lane + 64*u)
-// per pass and issues all their partial loads together.
-__device__ void softmax_row(const float* pr, size_t plane, int S, const float* bias, int E,
-                            float* z, float* out, float* lo) {
-  const int lane = threadIdx.x & 63;
-  float m = -INFINITY;
-  for (int e0 = 0; e0 < E; e0 += 4 * kWave) {
-    float p[4][kMaxSplits];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int e = e0 + u * kWave + lane;
-#pragma unroll
-      for (int s = 0; s < kMaxSplits; ++s)
-        if (s < S && e < E) p[u][s] = pr[s * plane + e];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int e = e0 + u * kWave + lane;
-      if (e >= E) continue;
-      float v = p[u][0];
-#pragma unroll
-      for (int s = 1; s < kMaxSplits; ++s)
-        if (s < S) v += p[u][s];
-      if (bias) v += bias[e];
-      z[e] = v;
-      m = fmaxf(m, v);
-    }
-  }
-  m = wave_max(m);
-  float sum = 0.f;
-  for (int e = lane; e < E; e += kWave) sum += expf(z[e] - m);
-  sum = wave_sum(sum);
-  for (int e = lane; e < E; e += kWave) {
-    const float v = z[e];
-    out[e] = expf(v - m) / sum;
-    if (lo) lo[e] = v;
-  }
-}
 
 __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, int T, int H, int E, int S,
@@ -187,8 +135,25 @@ __global__ __launch_bounds__(256) void router_logits_f32_kernel(
   part[static_cast<size_t>(t) * E + e] = acc;
 }
 
-// One wave per token row, four rows per workgroup; dynamic LDS: 4*E floats.
-// part may alias probs (S == 1): the row is read to LDS before it is written.
+// One wave per token row, four rows per workgroup.  Up to 512 experts the
+// row is reduced in registers (dev::softmax_loaded, the routine the fused
+// routing kernel uses); wider rows are staged in LDS (dynamic: 4*E floats).
+// part may alias probs (S == 1): a row is read whole before it is written.
+template <int NQ>
+__global__ __launch_bounds__(256) void softmax_rows_reg_kernel(const float* part, int S,
+                                                               const float* __restrict__ bias, int T, int E,
+                                                               float* probs, float* logits) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  dev::RowPartials<NQ> r[1];
+  dev::load_row<NQ>(part, static_cast<size_t>(T) * E, S, bias, E, t, r[0]);
+  const bool live[1] = {true};
+  float* const out[1] = {probs + static_cast<size_t>(t) * E};
+  float* const lds[1] = {nullptr};
+  float* const lo[1] = {logits ? logits + static_cast<size_t>(t) * E : nullptr};
+  dev::softmax_loaded<NQ, 1>(r, live, S, bias != nullptr, E, out, lds, lo);
+}
+
 __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* part, int S,
                                                            const float* __restrict__ bias, int T,
                                                            int E, float* probs, float* logits) {
@@ -196,9 +161,9 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* part, in
   const int wave = threadIdx.x >> 6;
   const int t = blockIdx.x * 4 + wave;
   if (t >= T) return;
-  softmax_row(part + static_cast<size_t>(t) * E, static_cast<size_t>(T) * E, S, bias, E,
-              zrow + static_cast<size_t>(wave) * E, probs + static_cast<size_t>(t) * E,
-              logits ? logits + static_cast<size_t>(t) * E : nullptr);
+  dev::softmax_row(part + static_cast<size_t>(t) * E, static_cast<size_t>(T) * E, S, bias, E,
+                   zrow + static_cast<size_t>(wave) * E, probs + static_cast<size_t>(t) * E,
+                   logits ? logits + static_cast<size_t>(t) * E : nullptr);
 }
 
 // Slices of the hidden dimension: enough router workgroups to spread the
@@ -217,12 +182,11 @@ size_t router_workspace_bytes(int T, int H, int E, dmoe_dtype dt) {
   return S > 1 ? static_cast<size_t>(S) * T * E * sizeof(float) : 0;
 }
 
-hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
-                         int H, int E, float* logits, float* probs, void* x_chunked,
-                         void* workspace, size_t ws_bytes, hipStream_t s) {
+hipError_t launch_router_partials(const void* x, const void* w, dmoe_dtype dt, int T, int H, int E,
+                                  float* probs, void* x_chunked, void* workspace, size_t ws_bytes,
+                                  hipStream_t s, float** part_out, int* S_out) {
   int S = 1;
-  float* part = probs;  // S == 1: the softmax reads the logits in place
-  const size_t lds = static_cast<size_t>(4) * E * sizeof(float);
+  float* part = probs;  // S == 1: the logits go to probs, read back in place by the softmax
   if (dt == DMOE_BF16) {
     const size_t need = router_workspace_bytes(T, H, E, dt);
     if (need > 0 && workspace && ws_bytes >= need) {
@@ -239,9 +203,28 @@ hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_d
                                                    static_cast<const float*>(w), T, H, E, part,
                                                    static_cast<float*>(x_chunked));
   }
-  hipError_t err = hipGetLastError();
+  *part_out = part;
+  *S_out = S;
+  return hipGetLastError();
+}
+
+hipError_t launch_router(const void* x, const void* w, const float* bias, dmoe_dtype dt, int T,
+                         int H, int E, float* logits, float* probs, void* x_chunked,
+                         void* workspace, size_t ws_bytes, hipStream_t s) {
+  float* part = nullptr;
+  int S = 1;
+  hipError_t err = launch_router_partials(x, w, dt, T, H, E, probs, x_chunked, workspace, ws_bytes, s,
+                                          &part, &S);
   if (err != hipSuccess) return err;
-  softmax_rows_kernel<<<(T + 3) / 4, 256, lds, s>>>(part, S, bias, T, E, probs, logits);
+  const unsigned blocks = (T + 3) / 4;
+  if (E <= 256) {
+    softmax_rows_reg_kernel<1><<<blocks, 256, 0, s>>>(part, S, bias, T, E, probs, logits);
+  } else if (E <= dev::kRegSoftmaxMaxE) {
+    softmax_rows_reg_kernel<2><<<blocks, 256, 0, s>>>(part, S, bias, T, E, probs, logits);
+  } else {
+    const size_t lds = static_cast<size_t>(4) * E * sizeof(float);
+    softmax_rows_kernel<<<blocks, 256, lds, s>>>(part, S, bias, T, E, probs, logits);
+  }
   return hipGetLastError();
 }
 

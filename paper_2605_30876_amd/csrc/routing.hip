@@ -9,67 +9,24 @@
 // probability row.
 //
 // Selection uses the total order (score desc, id asc), so an exact tie goes
-// to the lower id.  Block routing (one workgroup per block): for E <=
-// kRankMaxE each element's rank is counted directly (how many elements
-// precede it), one pass with no serial rounds; above that, and for token
-// routing (one wave per token), a top-k walks the order: round r picks the
-// best element strictly after round r-1's pick.
+// to the lower id.  Up to 1024 experts a wave selects by radix search over
+// order-preserving keys (dev::wave_topk_radix); above that a top-k walks the
+// order: round r picks the best element strictly after round r-1's pick.
 #include <algorithm>
 
-#include "dmoe_common.h"
+#include "route_dev.h"
 
 namespace dmoe {
 namespace {
 
-struct Cand {
-  float v;
-  int i;
-};
+using dev::Cand;
+using dev::kMaxK;
+using dev::kNone;
+using dev::ranks_before;
+using dev::wave_best;
 
-// (v, i) ranks before (w, j) in (score desc, id asc) order.
-__device__ __forceinline__ bool ranks_before(float v, int i, float w, int j) {
-  return v > w || (v == w && i < j);
-}
-
-__device__ __forceinline__ Cand wave_best(Cand c) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    float ov = __shfl_xor(c.v, m);
-    int oi = __shfl_xor(c.i, m);
-    if (ranks_before(ov, oi, c.v, c.i)) {
-      c.v = ov;
-      c.i = oi;
-    }
-  }
-  return c;
-}
-
-constexpr int kMaxK = 64;
-constexpr int kNone = 0x7fffffff;
-constexpr int kRankMaxE = 1024;
-
-__device__ __forceinline__ int precedes(float u, int e, float v, int i) {
-  return (u > v || (u == v && e < i)) ? 1 : 0;
-}
-
-// Rank of (v, i) among vals[0..E) (LDS, 16-byte aligned): the number of
-// elements that precede it.  Sixteen values per step, four 128-bit reads.
-__device__ __forceinline__ int rank_of(const float* vals, int E, float v, int i) {
-  int r = 0;
-  int e = 0;
-  const f32x4* v4 = reinterpret_cast<const f32x4*>(vals);
-  for (; e + 16 <= E; e += 16) {
-    f32x4 a[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) a[j] = v4[(e >> 2) + j];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int l = 0; l < 4; ++l) r += precedes(a[j][l], e + 4 * j + l, v, i);
-  }
-  for (; e < E; ++e) r += precedes(vals[e], e, v, i);
-  return r;
-}
+constexpr int kRadixMaxE = 64 * dev::kRadixMaxPerLane;
+constexpr int kSumBatch = 32;  // token loads of a block sum issued together
 
 constexpr int kWChunk = 64;  // tokens whose selected probabilities are staged at once
 
@@ -84,6 +41,8 @@ __global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict
   float* V = S + E;  // kWChunk * k floats
   __shared__ int sel[kMaxK + 1];
   __shared__ float selv[kMaxK + 1];
+  __shared__ float bufv[kMaxK + 1];
+  __shared__ int bufi[kMaxK + 1];
   __shared__ Cand wbest[4];
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -91,11 +50,19 @@ __global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict
   const int b = blockIdx.x;
   const float* pb = probs + static_cast<size_t>(b) * bs * E;
 
+  // Block mean in token order; a batch of token loads is in flight at once.
   const float n_tok = static_cast<float>(bs);
   for (int e = tid; e < E; e += blockDim.x) {
     float acc = 0.f;
-#pragma unroll 8
-    for (int t = 0; t < bs; ++t) acc += pb[static_cast<size_t>(t) * E + e];  // token order
+    for (int t0 = 0; t0 < bs; t0 += kSumBatch) {
+      float v[kSumBatch];
+#pragma unroll
+      for (int u = 0; u < kSumBatch; ++u)
+        if (t0 + u < bs) v[u] = pb[static_cast<size_t>(t0 + u) * E + e];
+#pragma unroll
+      for (int u = 0; u < kSumBatch; ++u)
+        if (t0 + u < bs) acc += v[u];
+    }
     const float v = acc / n_tok;
     S[e] = v;
     if (scores) scores[static_cast<size_t>(b) * E + e] = v;
@@ -103,15 +70,8 @@ __global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict
   __syncthreads();
 
   const int rounds = k < E ? k + 1 : k;
-  if (E <= kRankMaxE) {
-    for (int e = tid; e < E; e += blockDim.x) {
-      const float v = S[e];
-      const int r = rank_of(S, E, v, e);
-      if (r < rounds) {
-        sel[r] = e;
-        selv[r] = v;
-      }
-    }
+  if (E <= kRadixMaxE) {
+    if (wave == 0) dev::wave_topk_radix(S, E, rounds, sel, selv, bufv, bufi);
     __syncthreads();
   } else {
     float pv = INFINITY;
@@ -166,7 +126,7 @@ __global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict
 }
 
 // One wave per token, four tokens per workgroup; the token's row is staged in
-// LDS (dynamic: 4*E floats) so the k+1 rounds do not go back to memory.
+// LDS (dynamic: 4*E floats) so the selection does not go back to memory.
 __global__ __launch_bounds__(256) void token_topk_kernel(const float* __restrict__ probs, int T,
                                                          int E, int k,
                                                          int32_t* __restrict__ experts,
@@ -175,6 +135,8 @@ __global__ __launch_bounds__(256) void token_topk_kernel(const float* __restrict
   extern __shared__ float rows[];
   __shared__ int sel[4][kMaxK + 1];
   __shared__ float selv[4][kMaxK + 1];
+  __shared__ float bufv[4][kMaxK + 1];
+  __shared__ int bufi[4][kMaxK + 1];
   __shared__ float denom_s[4];
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -185,22 +147,12 @@ __global__ __launch_bounds__(256) void token_topk_kernel(const float* __restrict
   float* row = rows + static_cast<size_t>(wave) * E;
   for (int e = lane; e < E; e += kWave) row[e] = grow[e];
 
-  const int rounds = live ? (k < E ? k + 1 : k) : 0;
-  float pv = INFINITY;
-  int pi = -1;
-  for (int r = 0; r < rounds; ++r) {
-    Cand best{-INFINITY, kNone};
-    for (int e = lane; e < E; e += kWave) {
-      const float v = row[e];
-      if (ranks_before(pv, pi, v, e) && ranks_before(v, e, best.v, best.i)) best = Cand{v, e};
-    }
-    best = wave_best(best);
-    if (lane == 0) {
-      sel[wave][r] = best.i;
-      selv[wave][r] = best.v;
-    }
-    pv = best.v;
-    pi = best.i;
+  const int rounds = k < E ? k + 1 : k;
+  if (live) {
+    if (E <= kRadixMaxE)
+      dev::wave_topk_radix(row, E, rounds, sel[wave], selv[wave], bufv[wave], bufi[wave]);
+    else
+      dev::wave_topk(row, E, rounds, sel[wave], selv[wave]);
   }
   __syncthreads();
   if (live && lane == 0) {

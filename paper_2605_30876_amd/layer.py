@@ -5,7 +5,8 @@
     dmoe_router_logits -> dmoe_block_aggregate_topk | dmoe_token_topk
     -> dmoe_build_expert_schedule -> dmoe_expert_ffn -> dmoe_combine
 
-on the current stream.  It allocates only in its constructor, so a forward
+on the current stream (the routing steps as one dmoe_route_block /
+dmoe_route_token call by default).  It allocates only in its constructor, so a forward
 can be captured in a HIP graph.  Nothing is computed on the host.
 
 Expert weights are used in the library's packed layout: :func:`pack_weights`
@@ -76,20 +77,32 @@ class MoELayer:
         groups = self.NB if routing == "block" else self.T
         return min(self.E, groups * self.k)
 
-    def route(self, x, w_router, bias=None, routing: str = "block", stream=None):
+    def route(self, x, w_router, bias=None, routing: str = "block", stream=None, fused: bool = True):
+        """Routing stage: one dmoe_route_* call, or (fused=False) the chain of
+        the separate entry points; both give identical results."""
         T, H, E, k = self.T, self.H, self.E, self.k
+        if routing not in ("block", "token"):
+            raise ValueError(f"routing must be 'block' or 'token', not {routing!r}")
+        if fused and routing == "block":
+            lib.dmoe_route_block(x, w_router, bias, self.NB, self.bs, H, E, k, self.logits, self.probs,
+                                 self.x_chunked, self.block_scores, self.block_experts, self.combine_w,
+                                 self.block_gap, self.sched, self.router_ws, stream)
+            return
+        if fused:
+            lib.dmoe_route_token(x, w_router, bias, T, H, E, k, self.logits, self.probs, self.x_chunked,
+                                 self.token_experts, self.combine_w, self.token_gap, self.sched, self.router_ws,
+                                 stream)
+            return
         lib.dmoe_router_logits(x, w_router, bias, T, H, E, self.logits, self.probs, self.x_chunked,
                                self.router_ws, stream)
         if routing == "block":
             lib.dmoe_block_aggregate_topk(self.probs, self.NB, self.bs, E, k, self.block_scores,
                                           self.block_experts, self.combine_w, self.block_gap, stream)
             lib.dmoe_build_expert_schedule(self.block_experts, self.NB, self.bs, k, E, self.sched, stream)
-        elif routing == "token":
+        else:
             lib.dmoe_token_topk(self.probs, T, E, k, self.token_experts, self.combine_w, self.token_gap,
                                 stream)
             lib.dmoe_build_expert_schedule(self.token_experts, T, 1, k, E, self.sched, stream)
-        else:
-            raise ValueError(f"routing must be 'block' or 'token', not {routing!r}")
 
     def experts_ffn(self, w: dict, routing: str = "block", stream=None):
         """Expert FFN on the chunk-major copy of x that :meth:`route` stored."""
@@ -101,10 +114,10 @@ class MoELayer:
         lib.dmoe_combine(self.slot_out, self.combine_w, self.shared_out, self.T, self.H, self.k, self.y,
                          stream)
 
-    def forward(self, x, w: dict, routing: str = "block", stream=None) -> torch.Tensor:
+    def forward(self, x, w: dict, routing: str = "block", stream=None, fused_routing: bool = True) -> torch.Tensor:
         """Whole layer on hidden states x[T, H] with weights from
         :func:`pack_weights`; returns (a view of) y[T, H]."""
-        self.route(x, w["w_router"], w.get("bias"), routing, stream)
+        self.route(x, w["w_router"], w.get("bias"), routing, stream, fused=fused_routing)
         self.experts_ffn(w, routing, stream)
         self.combine(stream)
         return self.y

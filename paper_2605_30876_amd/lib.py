@@ -29,7 +29,7 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 
 # Every symbol include/dmoe.h declares.
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
-           "dmoe_build_expert_schedule", "dmoe_pack_activations", "dmoe_pack_expert_weights",
+           "dmoe_build_expert_schedule", "dmoe_route_block", "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights",
            "dmoe_ffn_workspace_size", "dmoe_expert_ffn", "dmoe_combine", "dmoe_last_error", "dmoe_version")
 
 
@@ -54,6 +54,9 @@ _SIGS = {
     "dmoe_block_aggregate_topk": ([_P, _I, _I, _I, _I, _P, _P, _P, _P, _P], _I),
     "dmoe_token_topk": ([_P, _I, _I, _I, _P, _P, _P, _P], _I),
     "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
+    "dmoe_route_block": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S,
+                          _P], _I),
+    "dmoe_route_token": ([_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S, _P], _I),
     "dmoe_pack_activations": ([_P, _I, _I, _I, _P, _P], _I),
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
@@ -162,6 +165,25 @@ class Schedule:
 def dmoe_build_expert_schedule(experts, n_groups, group_size, k, E, sched: Schedule, stream=None):
     _check(load().dmoe_build_expert_schedule(ptr(experts), n_groups, group_size, k, E, sched.as_c(),
                                              stream_handle(stream)))
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def dmoe_route_block(x, w_router, bias, n_blocks, block_size, H, E, k, logits, probs, x_chunked,
+                     block_scores, block_experts, combine_w, gap, sched: Schedule, workspace=None, stream=None):
+    _check(load().dmoe_route_block(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), n_blocks, block_size, H, E,
+                                   k, ptr(logits), ptr(probs), ptr(x_chunked), ptr(block_scores),
+                                   ptr(block_experts), ptr(combine_w), ptr(gap), sched.as_c(), ptr(workspace),
+                                   _nbytes(workspace), stream_handle(stream)))
+
+
+def dmoe_route_token(x, w_router, bias, T, H, E, k, logits, probs, x_chunked, token_experts, combine_w, gap,
+                     sched: Schedule, workspace=None, stream=None):
+    _check(load().dmoe_route_token(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), T, H, E, k, ptr(logits),
+                                   ptr(probs), ptr(x_chunked), ptr(token_experts), ptr(combine_w), ptr(gap),
+                                   sched.as_c(), ptr(workspace), _nbytes(workspace), stream_handle(stream)))
 
 
 def dmoe_pack_activations(x, T, H, x_chunked, stream=None):

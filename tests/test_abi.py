@@ -186,6 +186,45 @@ def test_combine_validation(L, buf):
     assert status(L, f, p, p, p + 4, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
 
 
+def _route(L, p, routing, **over):
+    a = dict(x=p, w=p, bias=None, dt=lib.DMOE_BF16, nb=1, bs=32, T=32, H=2048, E=256, k=8, logits=None, probs=p,
+             xc=None, scores=None, experts=p, cw=p, gap=None, sched=lib.dmoe_schedule(p, p, p, p, p), ws=None,
+             ws_bytes=0)
+    a.update(over)
+    if routing == "block":
+        return status(L, "dmoe_route_block", a["x"], a["w"], a["bias"], a["dt"], a["nb"], a["bs"], a["H"], a["E"],
+                      a["k"], a["logits"], a["probs"], a["xc"], a["scores"], a["experts"], a["cw"], a["gap"],
+                      a["sched"], a["ws"], a["ws_bytes"], None)
+    return status(L, "dmoe_route_token", a["x"], a["w"], a["bias"], a["dt"], a["T"], a["H"], a["E"], a["k"],
+                  a["logits"], a["probs"], a["xc"], a["experts"], a["cw"], a["gap"], a["sched"], a["ws"],
+                  a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("routing", ["block", "token"])
+def test_route_validation(L, buf, routing):
+    _, p = buf
+    INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    assert _route(L, p, routing, x=None)[0] == INV
+    assert _route(L, p, routing, experts=None)[0] == INV
+    assert _route(L, p, routing, cw=None)[0] == INV
+    assert _route(L, p, routing, sched=lib.dmoe_schedule(p, p, None, p, p))[0] == INV
+    assert _route(L, p, routing, dt=4)[0] == INV
+    assert _route(L, p, routing, k=0)[0] == INV
+    assert _route(L, p, routing, k=9, E=8)[0] == INV
+    assert _route(L, p, routing, E=5000)[0] == INV
+    assert _route(L, p, routing, probs=p + 4)[0] == INV
+    assert _route(L, p, routing, xc=p + 8)[0] == INV
+    assert _route(L, p, routing, H=2000)[0] == UNS
+    st, msg = _route(L, p, routing, E=1024)
+    assert st == UNS and "E <= 512" in msg
+    if routing == "block":
+        assert _route(L, p, routing, nb=0)[0] == INV
+        assert _route(L, p, routing, bs=5000)[0] == INV
+        assert _route(L, p, routing, nb=2**20, bs=2**11)[0] == INV
+    else:
+        assert _route(L, p, routing, T=0)[0] == INV
+
+
 def test_router_workspace_size():
     # decode step: the hidden dimension is split, one fp32 partial plane per slice
     n = lib.dmoe_router_workspace_size(32, 2048, 256, lib.DMOE_BF16)
