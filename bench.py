@@ -18,7 +18,6 @@ oracle timed on a bounded sample as ``cpu_baseline``.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import statistics
@@ -48,6 +47,8 @@ def parse():
     ap.add_argument("--ffn-only", action="store_true",
                     help="only replay the expert FFN (for hardware-counter runs)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-MiB buffer a few times (calibrates HBM byte counters)")
     return ap.parse_args()
 
 
@@ -56,11 +57,9 @@ def log(*a):
 
 
 def source_hash() -> str:
-    h = hashlib.sha256()
-    for f in ("ffn.hip", "pack.hip", "dmoe_common.h"):
-        with open(os.path.join(ROOT, "paper_2605_30876_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
+    from paper_2605_30876_amd.build import ffn_source_hash
+
+    return ffn_source_hash()
 
 
 def main():
@@ -72,6 +71,16 @@ def main():
         return 2
 
     import torch
+
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.full((n,), 3, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(8):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 8}))
+        return 0
 
     from dmoe_synth import get_config, make_inputs
     from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes

@@ -25,6 +25,18 @@ SOURCES = ["dmoe_api.cpp", "router.hip", "routing.hip", "schedule.hip", "route.h
 ARCH = os.environ.get("DMOE_OFFLOAD_ARCH", "gfx950")
 
 
+def ffn_source_hash() -> str:
+    """Hash of the sources of the expert-FFN kernels: hardware-counter figures
+    taken on other sources are stale."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in ("ffn.hip", "pack.hip", "dmoe_common.h"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):

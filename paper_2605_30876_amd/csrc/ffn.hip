@@ -90,49 +90,48 @@ constexpr int kFrag = 512;  // bf16 elements of one packed 16 x 32 weight tile (
 
 // Operands of one wave for up to KMAX K-steps (32 each) of its K-slice.
 // A: one 16-row weight tile, all steps issued at once; B: NT 16-column token
-// tiles, double-buffered in chunks of kBChunk steps.
-constexpr int kBChunk = 4;
-
-template <int NT, int KMAX>
+// tiles in chunks of BC steps, double-buffered when a burst has more than one
+// chunk.
+template <int NT, int KMAX, int BC>
 struct WaveOps {
+  static constexpr int kChunks = KMAX / BC;
   bf16x8 a[KMAX];
-  bf16x8 b[2][kBChunk][NT];
+  bf16x8 b[kChunks > 1 ? 2 : 1][BC][NT];
 };
 
 // A: packed tiles, step s at pa + s*kFrag (one contiguous burst per wave).
-template <int NT, int KMAX>
-__device__ __forceinline__ void issue_a(WaveOps<NT, KMAX>& w, const bf16_t* pa, int ns) {
+template <int NT, int KMAX, int BC>
+__device__ __forceinline__ void issue_a(WaveOps<NT, KMAX, BC>& w, const bf16_t* pa, int ns) {
 #pragma unroll
   for (int s = 0; s < KMAX; ++s)
     if (s < ns) w.a[s] = ld_bf16x8(pa + s * kFrag);
 }
 
 // B: chunk-major rows, step s at pb[ct] + s*bstep.
-template <int BUF, int NT, int KMAX>
-__device__ __forceinline__ void issue_b(WaveOps<NT, KMAX>& w, const bf16_t* const* pb, int bstep, int chunk,
+template <int BUF, int NT, int KMAX, int BC>
+__device__ __forceinline__ void issue_b(WaveOps<NT, KMAX, BC>& w, const bf16_t* const* pb, int bstep, int chunk,
                                         int ns) {
 #pragma unroll
-  for (int s = 0; s < kBChunk; ++s)
-    if (chunk * kBChunk + s < ns)
+  for (int s = 0; s < BC; ++s)
+    if (chunk * BC + s < ns)
 #pragma unroll
-      for (int ct = 0; ct < NT; ++ct) w.b[BUF][s][ct] = ld_bf16x8(pb[ct] + (chunk * kBChunk + s) * bstep);
+      for (int ct = 0; ct < NT; ++ct) w.b[BUF][s][ct] = ld_bf16x8(pb[ct] + (chunk * BC + s) * bstep);
 }
 
-template <int C, int NT, int KMAX>
-__device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX>& w, const bf16_t* const* pb, int bstep, int ns,
+template <int C, int NT, int KMAX, int BC>
+__device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC>& w, const bf16_t* const* pb, int bstep, int ns,
                                           f32x4 (&acc)[NT]) {
-  constexpr int NCH = KMAX / kBChunk;
+  constexpr int NCH = KMAX / BC;
   if constexpr (C < NCH) {
-    if (C * kBChunk < ns) {
+    if (C * BC < ns) {
       if constexpr (C + 1 < NCH) issue_b<(C + 1) & 1>(w, pb, bstep, C + 1, ns);
       __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads where they are
 #pragma unroll
-      for (int s = 0; s < kBChunk; ++s)
-        if (C * kBChunk + s < ns)
+      for (int s = 0; s < BC; ++s)
+        if (C * BC + s < ns)
 #pragma unroll
           for (int ct = 0; ct < NT; ++ct)
-            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.a[C * kBChunk + s], w.b[C & 1][s][ct],
-                                                              acc[ct], 0, 0, 0);
+            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.a[C * BC + s], w.b[C & 1][s][ct], acc[ct], 0, 0, 0);
       mma_chunk<C + 1>(w, pb, bstep, ns, acc);
     }
   }
@@ -140,10 +139,10 @@ __device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX>& w, const bf16_t* co
 
 // acc[ct] += A . B_ct^T over this wave's `steps` K-steps, in bursts of KMAX
 // steps: token chunk 0, the weight burst, then the remaining token chunks.
-template <int NT, int KMAX>
+template <int NT, int KMAX, int BC>
 __device__ __forceinline__ void wave_dot(const bf16_t* pa, const bf16_t* const* pb, int bstep, int steps,
                                          f32x4 (&acc)[NT]) {
-  WaveOps<NT, KMAX> w;
+  WaveOps<NT, KMAX, BC> w;
   for (int sc = 0; sc < steps; sc += KMAX) {
     const int ns = min(KMAX, steps - sc);
     const bf16_t* pbs[NT];
@@ -184,8 +183,8 @@ __device__ __forceinline__ void zero(f32x4 (&acc)[NT]) {
 // grid (ldh / 8, groups): packed gate/up tile `it` = 8 intermediate units.
 // Wave w reduces over hidden chunks [w*H/32, (w+1)*H/32) (K-steps
 // [w*H/128, (w+1)*H/128)).
-template <int NT, int KMAX>
-__global__ __launch_bounds__(kThreads, NT == 2 ? 3 : 1) void ffn_gateup_bf16_kernel(FfnParams p) {
+template <int NT, int KMAX, int BC, int MINW>
+__global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
     return;
@@ -212,7 +211,7 @@ __global__ __launch_bounds__(kThreads, NT == 2 ? 3 : 1) void ffn_gateup_bf16_ker
     }
     f32x4 acc[NT];
     zero(acc);
-    wave_dot<NT, KMAX>(pa, pb, bstep, steps, acc);
+    wave_dot<NT, KMAX, BC>(pa, pb, bstep, steps, acc);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -233,8 +232,8 @@ __global__ __launch_bounds__(kThreads, NT == 2 ? 3 : 1) void ffn_gateup_bf16_ker
 }
 
 // grid (H / 16, groups): packed down tile `jt` = 16 output features.
-template <int NT, int KMAX>
-__global__ __launch_bounds__(kThreads, NT == 2 ? 4 : 1) void ffn_down_bf16_kernel(FfnParams p) {
+template <int NT, int KMAX, int BC, int MINW>
+__global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
     return;
@@ -259,7 +258,7 @@ __global__ __launch_bounds__(kThreads, NT == 2 ? 4 : 1) void ffn_down_bf16_kerne
     }
     f32x4 acc[NT];
     zero(acc);
-    wave_dot<NT, KMAX>(pa, pb, bstep, steps, acc);
+    wave_dot<NT, KMAX, BC>(pa, pb, bstep, steps, acc);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -344,13 +343,32 @@ int pick_ntiles(int T, int k, int max_unique) {
   return rows <= 16 ? 1 : (rows <= 32 ? 2 : 4);
 }
 
+// Launch shapes per token-tile count NT: weight burst KMAX steps, token
+// chunks of BC steps, occupancy floor MINW (waves per SIMD).  The two-tile
+// variants serve block-routed decode steps, whose launches are small enough
+// that a higher floor keeps every workgroup resident at once.
+template <int NT>
+struct Shape;
+template <>
+struct Shape<1> {
+  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 1, kDnMax = 8, kDnChunk = 4, kDnWaves = 1;
+};
+template <>
+struct Shape<2> {
+  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 3, kDnMax = 8, kDnChunk = 4, kDnWaves = 4;
+};
+template <>
+struct Shape<4> {
+  static constexpr int kGuMax = 8, kGuChunk = 4, kGuWaves = 1, kDnMax = 8, kDnChunk = 4, kDnWaves = 1;
+};
+
 template <int NT>
 hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
-  constexpr int KMAX = NT <= 2 ? 16 : 8;
-  ffn_gateup_bf16_kernel<NT, KMAX><<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
+  using S = Shape<NT>;
+  ffn_gateup_bf16_kernel<NT, S::kGuMax, S::kGuChunk, S::kGuWaves><<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_down_bf16_kernel<NT, 8><<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
+  ffn_down_bf16_kernel<NT, S::kDnMax, S::kDnChunk, S::kDnWaves><<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -1,0 +1,159 @@
+"""Summaries of rocprofv3 output for profiles/.
+
+    python -m paper_2605_30876_amd.prof_summary trace RESULTS.db --title T --cmd C
+        per-kernel calls / avg / min / max / total (us) from a kernel trace
+        (``rocprofv3 --kernel-trace --stats``), as markdown.
+
+    python -m paper_2605_30876_amd.prof_summary traffic --config NAME \\
+            --fetch MODE=CSV ... --write MODE=CSV ... \\
+            --copy-fetch CSV --copy-write CSV --copy-bytes N [--json OUT] [--cmd C]
+        HBM traffic per expert-FFN launch (the gate/up + down kernels) from
+        ``rocprofv3 --pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE`` counter runs
+        (KiB per dispatch), each scaled by what the same counter reads for a
+        plain copy kernel of N bytes.  Writes markdown to stdout and, with
+        --json, the figures bench.py reports as ``roofline.traffic``.
+
+    python -m paper_2605_30876_amd.prof_summary mfma --csv CSV --kernel PATTERN ...
+        MFMA busy fraction and bf16 MFMA throughput per dispatch from a
+        ``--pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16
+        GRBM_GUI_ACTIVE`` run.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import json
+import re
+import sqlite3
+import statistics
+import sys
+
+FFN_KERNELS = ("ffn_gateup_bf16_kernel", "ffn_down_bf16_kernel", "ffn_gateup_f32_kernel", "ffn_down_f32_kernel")
+
+
+def short(name: str) -> str:
+    n = name.replace("(anonymous namespace)::", "").replace("void ", "")
+    n = re.sub(r"\(.*", "", n)
+    return n[:90]
+
+
+def cmd_trace(a):
+    c = sqlite3.connect(glob.glob(a.db)[0])
+    rows = list(c.execute("select name, count(*), sum(duration), avg(duration), min(duration), max(duration) "
+                          "from kernels group by name order by sum(duration) desc"))
+    total = sum(r[2] for r in rows)
+    print(f"# {a.title}\n\nCommand (from the repository root on the GPU box):\n\n```\n{a.cmd}\n```\n")
+    print("Durations in microseconds, from the kernel trace (`rocprofv3 --kernel-trace --stats`).\n")
+    print("| kernel | calls | avg | min | max | total | % GPU time |\n|---|---|---|---|---|---|---|")
+    for n, calls, tot, avg, mn, mx in rows:
+        if "at::native" in n or "rocclr" in n:
+            continue
+        print(f"| `{short(n)}` | {calls} | {avg / 1e3:.2f} | {mn / 1e3:.2f} | {mx / 1e3:.2f} | {tot / 1e3:.0f} "
+              f"| {100 * tot / total:.1f} |")
+    print("\n(torch's kernels are omitted: input generation and copies run outside the timed region.)")
+
+
+def read_counters(path: str, counter: str):
+    """[(dispatch_id, kernel_name, value)] of one counter from a counter_collection.csv."""
+    out = []
+    with open(glob.glob(path)[0], newline="") as fh:
+        for r in csv.DictReader(fh):
+            if r.get("Counter_Name") == counter:
+                out.append((int(r.get("Dispatch_Id", 0)), r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def mean_per_dispatch(rows, pattern: str):
+    vals = [v for _, n, v in rows if pattern in n]
+    return (statistics.mean(vals), len(vals)) if vals else (None, 0)
+
+
+def copy_kib(rows):
+    """Median KiB of the largest plain-copy dispatches (torch's elementwise copy kernel)."""
+    vals = [v for _, n, v in rows if "copy" in n.lower() and "dmoe" not in n]
+    big = max(vals)
+    return statistics.median([v for v in vals if v > 0.5 * big])
+
+
+def cmd_traffic(a):
+    from paper_2605_30876_amd.build import ffn_source_hash
+
+    fetch = dict(x.split("=", 1) for x in a.fetch)
+    write = dict(x.split("=", 1) for x in a.write)
+    copy_read = copy_kib(read_counters(a.copy_fetch, "FETCH_SIZE")) * 1024
+    copy_write = copy_kib(read_counters(a.copy_write, "WRITE_SIZE")) * 1024
+    f_scale = a.copy_bytes / copy_read
+    w_scale = a.copy_bytes / copy_write
+    print(f"# Expert-FFN HBM traffic, {a.config}\n")
+    if a.cmd:
+        print(f"Commands (from the repository root on the GPU box):\n\n```\n{a.cmd}\n```\n")
+    print(f"Calibration: a plain copy of {a.copy_bytes} bytes reads {copy_read:.0f} B by FETCH_SIZE "
+          f"(scale {f_scale:.4f}) and writes {copy_write:.0f} B by WRITE_SIZE (scale {w_scale:.4f}).\n")
+    print("| routing | kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled read MB | scaled write MB |")
+    print("|---|---|---|---|---|---|---|")
+    per_launch = {}
+    for mode in fetch:
+        fr, wr = read_counters(fetch[mode], "FETCH_SIZE"), read_counters(write[mode], "WRITE_SIZE")
+        total = 0.0
+        for k in FFN_KERNELS:
+            fk, nf = mean_per_dispatch(fr, k)
+            wk, nw = mean_per_dispatch(wr, k)
+            if fk is None:
+                continue
+            rb, wb = fk * 1024 * f_scale, (wk or 0) * 1024 * w_scale
+            total += rb + wb
+            print(f"| {mode} | `{k}` | {nf} | {fk:.0f} | {wk or 0:.0f} | {rb / 1e6:.2f} | {wb / 1e6:.2f} |")
+        per_launch[mode] = int(total)
+    print("\nPer expert-FFN launch (gate/up + down), read + write, scaled: " +
+          ", ".join(f"{m} {v / 1e6:.2f} MB" for m, v in per_launch.items()))
+    if a.json:
+        with open(a.json, "w") as fh:
+            json.dump({"config": a.config, "source_hash": ffn_source_hash(), "hbm_bytes_per_launch": per_launch,
+                       "fetch_scale": f_scale, "write_scale": w_scale, "command": a.cmd}, fh, indent=1)
+
+
+def cmd_mfma(a):
+    busy = read_counters(a.csv, "SQ_VALU_MFMA_BUSY_CYCLES")
+    mops = read_counters(a.csv, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+    gui = read_counters(a.csv, "GRBM_GUI_ACTIVE")
+    print("| kernel | dispatches | MFMA busy % of SIMD cycles | bf16 MFMA MOPs per dispatch |\n|---|---|---|---|")
+    for pat in a.kernel:
+        b, n = mean_per_dispatch(busy, pat)
+        m, _ = mean_per_dispatch(mops, pat)
+        g, _ = mean_per_dispatch(gui, pat)
+        if b is None:
+            continue
+        util = 100.0 * b / (g * a.simds) if g else float("nan")
+        print(f"| `{pat}` | {n} | {util:.1f} | {m:.0f} |")
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    sub = ap.add_subparsers(dest="what", required=True)
+    t = sub.add_parser("trace")
+    t.add_argument("db")
+    t.add_argument("--title", required=True)
+    t.add_argument("--cmd", required=True)
+    t.set_defaults(fn=cmd_trace)
+    r = sub.add_parser("traffic")
+    r.add_argument("--config", required=True)
+    r.add_argument("--fetch", nargs="+", required=True, help="MODE=counter_collection.csv of a FETCH_SIZE run")
+    r.add_argument("--write", nargs="+", required=True, help="MODE=counter_collection.csv of a WRITE_SIZE run")
+    r.add_argument("--copy-fetch", required=True)
+    r.add_argument("--copy-write", required=True)
+    r.add_argument("--copy-bytes", type=int, required=True)
+    r.add_argument("--json")
+    r.add_argument("--cmd", default="")
+    r.set_defaults(fn=cmd_traffic)
+    m = sub.add_parser("mfma")
+    m.add_argument("--csv", required=True)
+    m.add_argument("--kernel", nargs="+", required=True)
+    m.add_argument("--simds", type=int, default=1024, help="SIMDs on the chip (256 CUs x 4)")
+    m.set_defaults(fn=cmd_mfma)
+    a = ap.parse_args(argv)
+    a.fn(a)
+
+
+if __name__ == "__main__":
+    sys.exit(main())
