@@ -87,22 +87,40 @@ typedef enum dmoe_dtype {
 
 /*
  * Unique-expert schedule of one forward (device arrays, caller-allocated).
- * Written by dmoe_build_expert_schedule, read by dmoe_expert_ffn.
+ * Written by dmoe_build_expert_schedule (or dmoe_route_*), read by
+ * dmoe_expert_ffn.
  *   n_unique [1]        number of distinct experts selected in the forward
  *   unique   [E]        their ids, ascending, in unique[0 .. n_unique)
  *   offsets  [E + 1]    rows of unique[u] are rows offsets[u] .. offsets[u+1]
  *                       of row_token / row_slot; offsets[n_unique] = n_rows
  *   row_token[n_rows]   token of each row (n_rows = n_groups*group_size*k)
  *   row_slot [n_rows]   slot j in 0..k-1 of the token's expert list
+ *   n_work   [1]        number of work items
+ *   work     [4*max_work] work items {expert id, first row, row count, 0}:
+ *                       each unique expert's rows cut, in order, into pieces
+ *                       of at most DMOE_WORK_ROWS rows; items are ordered by
+ *                       expert id, then row.  max_work: dmoe_schedule_max_work.
  * Within one expert, rows are ordered by token.
  */
+#define DMOE_WORK_ROWS 64
+
 typedef struct dmoe_schedule {
   int32_t* n_unique;
   int32_t* unique;
   int32_t* offsets;
   int32_t* row_token;
   int32_t* row_slot;
+  int32_t* n_work;
+  int32_t* work;
 } dmoe_schedule;
+
+/*
+ * Upper bound of the schedule's work items for n_groups expert lists of k
+ * experts over groups of group_size tokens (E experts): the capacity of
+ * sched.work (in items of 4 int32) and the max_work argument of
+ * dmoe_expert_ffn.  0 on invalid sizes.
+ */
+int dmoe_schedule_max_work(int n_groups, int group_size, int k, int E);
 
 /*
  * Bytes of optional workspace that let dmoe_router_logits split the hidden
@@ -250,21 +268,22 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  * ws13, ws2: the shared expert packed the same way (n_experts = 1, I = I_s),
  * both NULL with I_s == 0 or both set with I_s > 0.  All of type dt.
  * sched: written by dmoe_build_expert_schedule for these T and k.
- * max_unique: an upper bound of sched.n_unique known on the host (the grid is
- * sized for it): min(E, n_groups*k).
+ * max_work: the bound dmoe_schedule_max_work gave for the schedule (the
+ * grid is sized for it).  The shared expert's T rows are cut into pieces of
+ * DMOE_WORK_ROWS the same way.
  * slot_out [T][k][H] float32 (every (t, j) is written); shared_out [T][H]
  * float32 (NULL iff no shared expert).
  * workspace: device scratch of at least dmoe_ffn_workspace_size(...) bytes,
  * ws_bytes its size.  Its contents on entry do not matter; calls that share
  * one workspace must not overlap in time (use one stream).
- * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 512; 1 <= max_unique <= E;
+ * Limits: T >= 1; 1 <= k <= min(E, 64); E <= 512; 1 <= max_work <= T*k;
  * H % c == 0; (T*k + T) * max(I, I_s) < 2^31.
  * DMOE_BF16: H % 128 == 0, I % 128 == 0, I_s % 128 == 0 (matrix-core tiles).
  * DMOE_F32: any I, I_s >= 1.
  */
 dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* w2, const void* ws13,
                             const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
-                            int max_unique, dmoe_schedule sched, float* slot_out, float* shared_out,
+                            int max_work, dmoe_schedule sched, float* slot_out, float* shared_out,
                             void* workspace, size_t ws_bytes, void* stream);
 
 /*

@@ -130,7 +130,8 @@ dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* to
 dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int group_size, int k,
                                        int E, dmoe_schedule sched, void* stream) {
   REQUIRE(experts, "experts must not be NULL");
-  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
           "every schedule array must be set");
   REQUIRE(n_groups >= 1 && group_size >= 1, "n_groups=%d and group_size=%d must be >= 1", n_groups,
           group_size);
@@ -144,6 +145,8 @@ dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int
   ALIGNED(sched.offsets);
   ALIGNED(sched.row_token);
   ALIGNED(sched.row_slot);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
   return hip_status(dmoe::launch_schedule(experts, n_groups, group_size, k, E, sched,
                                           static_cast<hipStream_t>(stream)),
                     __func__);
@@ -156,7 +159,8 @@ dmoe_status dmoe_route_block(const void* x, const void* w_router, const float* b
                              size_t ws_bytes, void* stream) {
   REQUIRE(x && w_router && probs && block_experts && combine_w,
           "x, w_router, probs, block_experts and combine_w must not be NULL");
-  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
           "every schedule array must be set");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
   REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
@@ -182,6 +186,8 @@ dmoe_status dmoe_route_block(const void* x, const void* w_router, const float* b
   ALIGNED(sched.offsets);
   ALIGNED(sched.row_token);
   ALIGNED(sched.row_slot);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
   if (x_chunked) {
     REQUIRE(H % dmoe::chunk_elems(dt) == 0, "x_chunked needs H %% %d == 0 (H=%d)", dmoe::chunk_elems(dt), H);
   }
@@ -201,7 +207,8 @@ dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* b
                              void* workspace, size_t ws_bytes, void* stream) {
   REQUIRE(x && w_router && probs && token_experts && combine_w,
           "x, w_router, probs, token_experts and combine_w must not be NULL");
-  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
           "every schedule array must be set");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
   REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
@@ -225,6 +232,8 @@ dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* b
   ALIGNED(sched.offsets);
   ALIGNED(sched.row_token);
   ALIGNED(sched.row_slot);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
   if (x_chunked) {
     REQUIRE(H % dmoe::chunk_elems(dt) == 0, "x_chunked needs H %% %d == 0 (H=%d)", dmoe::chunk_elems(dt), H);
   }
@@ -274,6 +283,12 @@ dmoe_status dmoe_pack_expert_weights(const void* w_gate, const void* w_up, const
                     __func__);
 }
 
+int dmoe_schedule_max_work(int n_groups, int group_size, int k, int E) {
+  if (n_groups < 1 || group_size < 1 || k < 1 || E < 1 || k > E) return 0;
+  const long n = dmoe::schedule_max_work(n_groups, group_size, k, E);
+  return n <= kIntLimit ? static_cast<int>(n) : 0;
+}
+
 size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
   if (T < 1 || I < 1 || I_s < 0 || k < 1 || !valid_dtype(dt)) return 0;
   return dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
@@ -281,18 +296,20 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
 
 dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* w2, const void* ws13,
                             const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
-                            int max_unique, dmoe_schedule sched, float* slot_out, float* shared_out,
+                            int max_work, dmoe_schedule sched, float* slot_out, float* shared_out,
                             void* workspace, size_t ws_bytes, void* stream) {
   REQUIRE(x_chunked && w13 && w2 && slot_out && workspace,
           "x_chunked, w13, w2, slot_out and workspace must not be NULL");
-  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot,
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
           "every schedule array must be set");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
   REQUIRE(T >= 1 && H >= 1 && I >= 1 && I_s >= 0, "T=%d, H=%d, I=%d must be >= 1 and I_s=%d >= 0",
           T, H, I, I_s);
   REQUIRE(E >= 1, "E=%d must be >= 1", E);
   REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
-  REQUIRE(max_unique >= 1 && max_unique <= E, "max_unique=%d must be in [1, E]", max_unique);
+  REQUIRE(max_work >= 1 && static_cast<long>(max_work) <= static_cast<long>(T) * k,
+          "max_work=%d must be in [1, T*k]", max_work);
   REQUIRE(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
   const bool shared = I_s > 0;
   REQUIRE(shared == (ws13 != nullptr) && shared == (ws2 != nullptr) && shared == (shared_out != nullptr),
@@ -306,6 +323,10 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
   ALIGNED(x_chunked);
   ALIGNED(w13);
   ALIGNED(w2);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
   ALIGNED(ws13);
   ALIGNED(ws2);
   ALIGNED(slot_out);
@@ -316,7 +337,7 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
     SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
             "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
   }
-  dmoe::FfnArgs a{x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_unique,
+  dmoe::FfnArgs a{x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
                   sched, slot_out, shared_out, workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }

@@ -111,7 +111,7 @@ struct FfnArgs {
   const void* w2;    // packed routed down weights
   const void* ws13;  // packed shared-expert gate/up (or nullptr)
   const void* ws2;   // packed shared-expert down (or nullptr)
-  int T, H, E, I, I_s, k, max_unique;
+  int T, H, E, I, I_s, k, max_work;
   dmoe_schedule sched;
   float* slot_out;
   float* shared_out;
@@ -119,6 +119,7 @@ struct FfnArgs {
 };
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
+long schedule_max_work(long n_groups, long group_size, long k, long E);
 
 hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
                           dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);

@@ -4,12 +4,12 @@
 //   h    = silu(Wg x) * (Wu x)        gate/up kernel -> h rows (workspace)
 //   out  = Wd h                       down kernel    -> slot_out[t][j] / shared_out[t]
 //
-// Groups: g < n_unique is the g-th unique routed expert of the schedule; the
-// shared expert is one more group.  A workgroup owns one 16-row weight tile
-// of one group, streams it from HBM once and applies it to every row (token)
-// of the group, so each selected expert's weights are read once per forward.
-// The grid covers the largest possible group count; workgroups of groups past
-// the device-side count exit at once.
+// Work items: grid row y < max_work is the schedule's y-th work item (up to
+// DMOE_WORK_ROWS rows of one routed expert; rows past n_work exit at once);
+// the rows after those cut the shared expert's T tokens into pieces of
+// DMOE_WORK_ROWS.  A workgroup owns one 16-row weight tile of one item,
+// streams it from HBM and applies it to the item's rows (tokens): each
+// selected expert's weights are read once per forward per piece of its rows.
 //
 // bf16 path (matrix cores, v_mfma_f32_16x16x32_bf16, fp32 accumulation):
 //  * A operand = weight rows, B operand = token rows, C = [weight row][token].
@@ -43,25 +43,32 @@ namespace {
 constexpr int kThreads = 256;
 
 struct Group {
-  int r0;          // first row of the group in the row space (h buffer row)
-  int n;           // rows (tokens) in the group
+  int r0;          // first row of the item in the row space (h buffer row)
+  int n;           // rows (tokens) in the item
   int expert;      // routed expert id, or -1 for the shared expert
-  const int* tok;  // token of each row (routed) or nullptr (row c is token c)
+  const int* tok;  // token of each row (routed), or nullptr: row c is token t0 + c
+  int t0;
 };
 
-__device__ __forceinline__ bool decode_group(int gidx, int max_unique, const int* n_unique,
-                                             const int* unique, const int* offsets,
-                                             const int* row_token, int T, int Tk, Group& g) {
-  if (gidx < max_unique) {
-    if (gidx >= *n_unique) return false;
-    g.expert = unique[gidx];
-    g.r0 = offsets[gidx];
-    g.n = offsets[gidx + 1] - g.r0;
-    g.tok = row_token + g.r0;
+// One memory round trip: the item count and the item are loaded together
+// (y < max_work keeps the index inside the work array; an item past n_work
+// is loaded but not used).
+__device__ __forceinline__ bool decode_item(int y, int max_work, const int* n_work, const int* work,
+                                            const int* row_token, int T, int Tk, Group& g) {
+  if (y < max_work) {
+    const int nw = *n_work;
+    const int4 it = reinterpret_cast<const int4*>(work)[y];
+    g.expert = it.x;
+    g.r0 = it.y;
+    g.n = y < nw ? it.z : 0;
+    g.tok = row_token + it.y;
+    g.t0 = 0;
   } else {
+    const int c = y - max_work;
     g.expert = -1;
-    g.r0 = Tk;
-    g.n = T;
+    g.t0 = c * DMOE_WORK_ROWS;
+    g.r0 = Tk + g.t0;
+    g.n = min(DMOE_WORK_ROWS, T - g.t0);
     g.tok = nullptr;
   }
   return g.n > 0;
@@ -75,12 +82,11 @@ struct FfnParams {
   const bf16_t* w2;    // routed down, fragment-packed
   const bf16_t* ws13;  // shared gate/up, fragment-packed
   const bf16_t* ws2;   // shared down, fragment-packed
-  const int* n_unique;
-  const int* unique;
-  const int* offsets;
+  const int* n_work;
+  const int* work;
   const int* row_token;
   const int* row_slot;
-  int T, H, I, I_s, k, Tk, R, max_unique;  // R: rows of the h buffer
+  int T, H, I, I_s, k, Tk, R, max_work;  // R: rows of the h buffer
   bf16_t* hk;                              // SwiGLU activations, chunk-major [ldh/8][R][8]
   float* slot_out;
   float* shared_out;
@@ -186,7 +192,7 @@ __device__ __forceinline__ void zero(f32x4 (&acc)[NT]) {
 template <int NT, int KMAX, int BC, int MINW>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
-  if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
+  if (!decode_item(blockIdx.y, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g))
     return;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int it = blockIdx.x;
@@ -206,7 +212,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
       const int col = min(p0 + ct * 16 + c, g.n - 1);
-      const int tok = g.tok ? g.tok[col] : col;
+      const int tok = g.tok ? g.tok[col] : g.t0 + col;
       pb[ct] = p.xk + (static_cast<size_t>(chunk0) * p.T + tok) * 8;
     }
     f32x4 acc[NT];
@@ -235,7 +241,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
 template <int NT, int KMAX, int BC, int MINW>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
-  if (!decode_group(blockIdx.y, p.max_unique, p.n_unique, p.unique, p.offsets, p.row_token, p.T, p.Tk, g))
+  if (!decode_item(blockIdx.y, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g))
     return;
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
             const int r = g.r0 + col;
             dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H + j;
           } else {
-            dst = p.shared_out + static_cast<size_t>(col) * H + j;
+            dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H + j;
           }
           *reinterpret_cast<f32x4*>(dst) = acc[ct];
         }
@@ -285,11 +291,10 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 
 __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
     const float* __restrict__ xk, const float* __restrict__ w13, const float* __restrict__ ws13,
-    const int* __restrict__ n_unique, const int* __restrict__ unique, const int* __restrict__ offsets,
-    const int* __restrict__ row_token, int T, int H, int I, int I_s, int Tk, int max_unique, int ldh,
-    float* __restrict__ hbuf) {
+    const int* __restrict__ n_work, const int* __restrict__ work, const int* __restrict__ row_token, int T, int H,
+    int I, int I_s, int Tk, int max_work, int ldh, float* __restrict__ hbuf) {
   Group g;
-  if (!decode_group(blockIdx.y, max_unique, n_unique, unique, offsets, row_token, T, Tk, g)) return;
+  if (!decode_item(blockIdx.y, max_work, n_work, work, row_token, T, Tk, g)) return;
   const int Iw = g.expert >= 0 ? I : I_s;
   const int i = blockIdx.x * kThreads + threadIdx.x;
   if (i >= Iw) return;
@@ -298,7 +303,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
   const float* wgr = W + static_cast<size_t>(i) * H;
   const float* wur = W + (static_cast<size_t>(Iw) + i) * H;
   for (int col = 0; col < g.n; ++col) {
-    const int tok = g.tok ? g.tok[col] : col;
+    const int tok = g.tok ? g.tok[col] : g.t0 + col;
     float a = 0.f, b = 0.f;
     for (int h = 0; h < H; ++h) {
       const float xv = xk[(static_cast<size_t>(h >> 2) * T + tok) * 4 + (h & 3)];
@@ -310,13 +315,12 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
 }
 
 __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
-    const float* __restrict__ w2, const float* __restrict__ ws2, const int* __restrict__ n_unique,
-    const int* __restrict__ unique, const int* __restrict__ offsets,
-    const int* __restrict__ row_token, const int* __restrict__ row_slot, int T, int H, int I,
-    int I_s, int k, int Tk, int max_unique, int ldh, const float* __restrict__ hbuf,
+    const float* __restrict__ w2, const float* __restrict__ ws2, const int* __restrict__ n_work,
+    const int* __restrict__ work, const int* __restrict__ row_token, const int* __restrict__ row_slot, int T,
+    int H, int I, int I_s, int k, int Tk, int max_work, int ldh, const float* __restrict__ hbuf,
     float* __restrict__ slot_out, float* __restrict__ shared_out) {
   Group g;
-  if (!decode_group(blockIdx.y, max_unique, n_unique, unique, offsets, row_token, T, Tk, g)) return;
+  if (!decode_item(blockIdx.y, max_work, n_work, work, row_token, T, Tk, g)) return;
   const int Kd = g.expert >= 0 ? I : I_s;
   const int j = blockIdx.x * kThreads + threadIdx.x;
   if (j >= H) return;
@@ -329,7 +333,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
       const int r = g.r0 + col;
       slot_out[(static_cast<size_t>(row_token[r]) * k + row_slot[r]) * H + j] = acc;
     } else {
-      shared_out[static_cast<size_t>(col) * H + j] = acc;
+      shared_out[static_cast<size_t>(g.t0 + col) * H + j] = acc;
     }
   }
 }
@@ -337,9 +341,10 @@ __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
 // ---- launch ---------------------------------------------------------------
 
 // Token columns per pass: enough 16-wide tiles for the expected rows of a
-// routed expert (T*k spread over max_unique experts), at most 4.
-int pick_ntiles(int T, int k, int max_unique) {
-  const long rows = (static_cast<long>(T) * k + max_unique - 1) / max_unique;
+// work item (the rows of the forward spread over max_work items, at most
+// DMOE_WORK_ROWS), at most 4.
+int pick_ntiles(int T, int k, int max_work) {
+  const long rows = std::min<long>(DMOE_WORK_ROWS, (static_cast<long>(T) * k + max_work - 1) / max_work);
   return rows <= 16 ? 1 : (rows <= 32 ? 2 : 4);
 }
 
@@ -384,31 +389,31 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
   const int Tk = a.T * a.k;
   const int R = Tk + (a.I_s > 0 ? a.T : 0);
   const int ldh = std::max(a.I, a.I_s);
-  const int groups = a.max_unique + (a.I_s > 0 ? 1 : 0);
+  const int shared_items = a.I_s > 0 ? (a.T + DMOE_WORK_ROWS - 1) / DMOE_WORK_ROWS : 0;
+  const int items = a.max_work + shared_items;
   if (dt == DMOE_BF16) {
     FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w13),
                 static_cast<const bf16_t*>(a.w2), static_cast<const bf16_t*>(a.ws13),
-                static_cast<const bf16_t*>(a.ws2), a.sched.n_unique, a.sched.unique,
-                a.sched.offsets, a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k,
-                Tk, R, a.max_unique, static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
-    switch (pick_ntiles(a.T, a.k, a.max_unique)) {
-      case 1: return launch_bf16<1>(p, ldh, groups, s);
-      case 2: return launch_bf16<2>(p, ldh, groups, s);
-      default: return launch_bf16<4>(p, ldh, groups, s);
+                static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
+                a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work,
+                static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
+    switch (pick_ntiles(a.T, a.k, a.max_work)) {
+      case 1: return launch_bf16<1>(p, ldh, items, s);
+      case 2: return launch_bf16<2>(p, ldh, items, s);
+      default: return launch_bf16<4>(p, ldh, items, s);
     }
   }
   float* hbuf = static_cast<float*>(a.workspace);
-  dim3 g_gu((ldh + kThreads - 1) / kThreads, groups), g_dn((a.H + kThreads - 1) / kThreads, groups);
+  dim3 g_gu((ldh + kThreads - 1) / kThreads, items), g_dn((a.H + kThreads - 1) / kThreads, items);
   ffn_gateup_f32_kernel<<<g_gu, kThreads, 0, s>>>(
       static_cast<const float*>(a.x), static_cast<const float*>(a.w13), static_cast<const float*>(a.ws13),
-      a.sched.n_unique, a.sched.unique, a.sched.offsets, a.sched.row_token, a.T, a.H, a.I, a.I_s, Tk,
-      a.max_unique, ldh, hbuf);
+      a.sched.n_work, a.sched.work, a.sched.row_token, a.T, a.H, a.I, a.I_s, Tk, a.max_work, ldh, hbuf);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_down_f32_kernel<<<g_dn, kThreads, 0, s>>>(
-      static_cast<const float*>(a.w2), static_cast<const float*>(a.ws2), a.sched.n_unique,
-      a.sched.unique, a.sched.offsets, a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s,
-      a.k, Tk, a.max_unique, ldh, hbuf, a.slot_out, a.shared_out);
+      static_cast<const float*>(a.w2), static_cast<const float*>(a.ws2), a.sched.n_work, a.sched.work,
+      a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, a.max_work, ldh, hbuf, a.slot_out,
+      a.shared_out);
   return hipGetLastError();
 }
 

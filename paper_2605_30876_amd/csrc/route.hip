@@ -153,11 +153,9 @@ __global__ __launch_bounds__(kThreads) void route_small_kernel(
 
   // 4. unique-expert schedule of the G expert lists (one block: closed form)
   if (G == 1 && k <= kWave)
-    dev::schedule_one_group(expc, gs, k, slds, sched.n_unique, sched.unique, sched.offsets, sched.row_token,
-                            sched.row_slot);
+    dev::schedule_one_group(expc, gs, k, slds, sched);
   else
-    dev::schedule_wg(expc, G, gs, k, E, slds, sched.n_unique, sched.unique, sched.offsets, sched.row_token,
-                     sched.row_slot);
+    dev::schedule_wg(expc, G, gs, k, E, slds, sched);
 }
 
 }  // namespace

@@ -458,8 +458,12 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 //      in token order and the schedule is identical on every run; then all
 //      threads write the round's rows.
 __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs, int k, int E, int* lds,
-                                   int32_t* n_unique, int32_t* unique, int32_t* offsets,
-                                   int32_t* row_token, int32_t* row_slot) {
+                                   const dmoe_schedule& sched) {
+  int32_t* const n_unique = sched.n_unique;
+  int32_t* const unique = sched.unique;
+  int32_t* const offsets = sched.offsets;
+  int32_t* const row_token = sched.row_token;
+  int32_t* const row_slot = sched.row_slot;
   const int Ep = pad4(E);
   int* cnt = lds;                                          // [E] selections
   int* base = cnt + Ep;                                    // [E] first row
@@ -468,6 +472,7 @@ __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs,
   int* pos = reinterpret_cast<int*>(mask + static_cast<size_t>(Ep) * kMaskWords);  // [kSchedThreads]
   __shared__ int wrows[kSchedThreads / kWave];
   __shared__ int wuniq[kSchedThreads / kWave];
+  __shared__ int wchunk[kSchedThreads / kWave];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -492,30 +497,39 @@ __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs,
   const int c = tid < E ? cnt[tid] : 0;
   const int rows = c * gs;
   const int pres = c > 0 ? 1 : 0;
+  const int chunks = (rows + DMOE_WORK_ROWS - 1) / DMOE_WORK_ROWS;  // work items of this expert
   const int r_incl = wave_incl_scan(rows);
   const int u_incl = wave_incl_scan(pres);
+  const int c_incl = wave_incl_scan(chunks);
   if (lane == kWave - 1) {
     wrows[wave] = r_incl;
     wuniq[wave] = u_incl;
+    wchunk[wave] = c_incl;
   }
   __syncthreads();
-  int r_off = 0, u_off = 0;
+  int r_off = 0, u_off = 0, c_off = 0;
   for (int w = 0; w < wave; ++w) {
     r_off += wrows[w];
     u_off += wuniq[w];
+    c_off += wchunk[w];
   }
   const int r_excl = r_off + r_incl - rows;
   const int u_excl = u_off + u_incl - pres;
+  const int c_excl = c_off + c_incl - chunks;
   if (tid < E) {
     base[tid] = r_excl;
     if (pres) {
       unique[u_excl] = tid;
       offsets[u_excl] = r_excl;
     }
+    int4* work = reinterpret_cast<int4*>(sched.work) + c_excl;
+    for (int c = 0; c < chunks; ++c)
+      work[c] = make_int4(tid, r_excl + c * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, rows - c * DMOE_WORK_ROWS), 0);
   }
   if (tid == kSchedThreads - 1) {
     offsets[u_excl + pres] = r_excl + rows;
     *n_unique = u_excl + pres;
+    *sched.n_work = c_excl + chunks;
   }
   __syncthreads();
 
@@ -575,33 +589,37 @@ __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs,
 
 // The schedule of a single group (one block): its k distinct experts in
 // ascending id order, each with all gs rows of the group, slot = the expert's
-// position in the group's list.  The same schedule schedule_wg builds for
-// n_groups == 1.  Called by all threads of the workgroup (k <= kWave); lds
-// holds 2*kWave ints.
-__device__ inline void schedule_one_group(const int32_t* experts, int gs, int k, int* lds, int32_t* n_unique,
-                                          int32_t* unique, int32_t* offsets, int32_t* row_token,
-                                          int32_t* row_slot) {
-  int* slot_of = lds;           // [k] slot of the rank-u expert
+// position in the group's list, and their work items.  The same schedule
+// schedule_wg builds for n_groups == 1.  Called by all threads of the
+// workgroup (k <= kWave); lds holds kWave ints.
+__device__ inline void schedule_one_group(const int32_t* experts, int gs, int k, int* lds,
+                                          const dmoe_schedule& sched) {
+  int* slot_of = lds;  // [k] slot of the rank-u expert
   const int tid = threadIdx.x;
+  const int chunks = (gs + DMOE_WORK_ROWS - 1) / DMOE_WORK_ROWS;  // work items per expert
   if (tid < kWave) {
     const int e = tid < k ? experts[tid] : 0x7fffffff;
     int r = 0;
     for (int m = 0; m < k; ++m) r += __builtin_amdgcn_readlane(e, m) < e ? 1 : 0;
     if (tid < k) {
       slot_of[r] = tid;
-      unique[r] = e;
-      offsets[r] = r * gs;
+      sched.unique[r] = e;
+      sched.offsets[r] = r * gs;
+      int4* work = reinterpret_cast<int4*>(sched.work) + r * chunks;
+      for (int c = 0; c < chunks; ++c)
+        work[c] = make_int4(e, r * gs + c * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, gs - c * DMOE_WORK_ROWS), 0);
     }
     if (tid == 0) {
-      offsets[k] = k * gs;
-      *n_unique = k;
+      sched.offsets[k] = k * gs;
+      *sched.n_unique = k;
+      *sched.n_work = k * chunks;
     }
   }
   __syncthreads();
   for (int i = tid; i < k * gs; i += blockDim.x) {
     const int u = i / gs;
-    row_token[i] = i - u * gs;
-    row_slot[i] = slot_of[u];
+    sched.row_token[i] = i - u * gs;
+    sched.row_slot[i] = slot_of[u];
   }
 }
 

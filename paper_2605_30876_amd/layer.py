@@ -62,7 +62,10 @@ class MoELayer:
         self.token_experts = torch.empty((T, k), **i32)
         self.token_gap = torch.empty((T,), **f32)
         self.combine_w = torch.empty((T, k), **f32)
-        self.sched = lib.Schedule.empty(E, T * k, device)
+        # work-item capacity: the larger of the two routings' bounds
+        self._max_work = {"block": lib.dmoe_schedule_max_work(n_blocks, block_size, k, E),
+                          "token": lib.dmoe_schedule_max_work(T, 1, k, E)}
+        self.sched = lib.Schedule.empty(E, T * k, device, max(self._max_work.values()))
         self.slot_out = torch.empty((T, k, H), **f32)
         self.shared_out = torch.empty((T, H), **f32) if I_s > 0 else None
         dt = lib.DMOE_F32 if dtype == torch.float32 else lib.DMOE_BF16
@@ -73,9 +76,9 @@ class MoELayer:
         # The layer output is accumulated in fp32; it is stored as out_dtype.
         self.y = torch.empty((T, H), dtype=out_dtype, device=device)
 
-    def max_unique(self, routing: str) -> int:
-        groups = self.NB if routing == "block" else self.T
-        return min(self.E, groups * self.k)
+    def max_work(self, routing: str) -> int:
+        """Work items the expert FFN's grid is sized for (dmoe_schedule_max_work)."""
+        return self._max_work[routing]
 
     def route(self, x, w_router, bias=None, routing: str = "block", stream=None, fused: bool = True):
         """Routing stage: one dmoe_route_* call, or (fused=False) the chain of
@@ -107,7 +110,7 @@ class MoELayer:
     def experts_ffn(self, w: dict, routing: str = "block", stream=None):
         """Expert FFN on the chunk-major copy of x that :meth:`route` stored."""
         lib.dmoe_expert_ffn(self.x_chunked, w["w13"], w["w2"], w.get("ws13"), w.get("ws2"), self.T, self.H,
-                            self.E, self.I, self.I_s, self.k, self.max_unique(routing), self.sched,
+                            self.E, self.I, self.I_s, self.k, self.max_work(routing), self.sched,
                             self.slot_out, self.shared_out, self.workspace, stream)
 
     def combine(self, stream=None):

@@ -29,7 +29,7 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 
 # Every symbol include/dmoe.h declares.
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
-           "dmoe_build_expert_schedule", "dmoe_route_block", "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights",
+           "dmoe_build_expert_schedule", "dmoe_schedule_max_work", "dmoe_route_block", "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights",
            "dmoe_ffn_workspace_size", "dmoe_expert_ffn", "dmoe_combine", "dmoe_last_error", "dmoe_version")
 
 
@@ -39,10 +39,13 @@ class DmoeError(RuntimeError):
         self.status = status
 
 
+WORK_ROWS = 64  # DMOE_WORK_ROWS: rows of one expert per work item at most
+
+
 class dmoe_schedule(ctypes.Structure):
     _fields_ = [("n_unique", ctypes.c_void_p), ("unique", ctypes.c_void_p),
                 ("offsets", ctypes.c_void_p), ("row_token", ctypes.c_void_p),
-                ("row_slot", ctypes.c_void_p)]
+                ("row_slot", ctypes.c_void_p), ("n_work", ctypes.c_void_p), ("work", ctypes.c_void_p)]
 
 
 _P = ctypes.c_void_p
@@ -54,6 +57,7 @@ _SIGS = {
     "dmoe_block_aggregate_topk": ([_P, _I, _I, _I, _I, _P, _P, _P, _P, _P], _I),
     "dmoe_token_topk": ([_P, _I, _I, _I, _P, _P, _P, _P], _I),
     "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
+    "dmoe_schedule_max_work": ([_I, _I, _I, _I], _I),
     "dmoe_route_block": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S,
                           _P], _I),
     "dmoe_route_token": ([_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S, _P], _I),
@@ -151,15 +155,23 @@ class Schedule:
     offsets: torch.Tensor
     row_token: torch.Tensor
     row_slot: torch.Tensor
+    n_work: torch.Tensor
+    work: torch.Tensor  # [max_work, 4]: expert id, first row, row count, 0
 
     @staticmethod
-    def empty(E: int, n_rows: int, device) -> "Schedule":
+    def empty(E: int, n_rows: int, device, max_work: int | None = None) -> "Schedule":
         z = lambda n: torch.zeros(max(n, 4), dtype=torch.int32, device=device)  # noqa: E731
-        return Schedule(z(1), z(E), z(E + 1), z(n_rows), z(n_rows))
+        mw = max(max_work if max_work is not None else n_rows, 1)
+        return Schedule(z(1), z(E), z(E + 1), z(n_rows), z(n_rows), z(1),
+                        torch.zeros((mw, 4), dtype=torch.int32, device=device))
 
     def as_c(self) -> dmoe_schedule:
         return dmoe_schedule(ptr(self.n_unique), ptr(self.unique), ptr(self.offsets),
-                             ptr(self.row_token), ptr(self.row_slot))
+                             ptr(self.row_token), ptr(self.row_slot), ptr(self.n_work), ptr(self.work))
+
+
+def dmoe_schedule_max_work(n_groups, group_size, k, E) -> int:
+    return int(load().dmoe_schedule_max_work(n_groups, group_size, k, E))
 
 
 def dmoe_build_expert_schedule(experts, n_groups, group_size, k, E, sched: Schedule, stream=None):
@@ -199,10 +211,10 @@ def dmoe_ffn_workspace_size(T, I, I_s, k, dt) -> int:
     return int(load().dmoe_ffn_workspace_size(T, I, I_s, k, dt))
 
 
-def dmoe_expert_ffn(x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_unique, sched: Schedule,
+def dmoe_expert_ffn(x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work, sched: Schedule,
                     slot_out, shared_out, workspace, stream=None):
     _check(load().dmoe_expert_ffn(ptr(x_chunked), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
-                                  dtype_code(x_chunked), T, H, E, I, I_s, k, max_unique, sched.as_c(),
+                                  dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
                                   ptr(slot_out), ptr(shared_out), ptr(workspace),
                                   workspace.numel() * workspace.element_size(), stream_handle(stream)))
 

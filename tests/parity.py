@@ -51,6 +51,27 @@ def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: lis
     return out
 
 
+def expected_work(uniq, rows: dict, work_rows: int = 64):
+    """Work items {expert, first row, rows} from the oracle's per-expert rows:
+    each unique expert's rows, in ascending id order, cut into pieces of at
+    most work_rows (the schedule's documented layout)."""
+    items, r0 = [], 0
+    for e in uniq.tolist():
+        n = len(rows[e])
+        for c in range(0, n, work_rows):
+            items.append([e, r0 + c, min(work_rows, n - c), 0])
+        r0 += n
+    return items
+
+
+def check_work(sched, uniq, rows: dict):
+    items = expected_work(uniq, rows)
+    n_work = int(cpu(sched.n_work)[0])
+    assert n_work == len(items), f"n_work {n_work} != {len(items)}"
+    got = cpu(sched.work)[:n_work].numpy().tolist()
+    assert got == items, "work items differ"
+
+
 def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, check_determinism=True,
                   packed=None):
     """Run the GPU forward on d_gpu, compare with the oracle, return a report.
@@ -125,6 +146,8 @@ def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, che
         got = list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist()))
         assert got == rows[e], f"rows of expert {e} differ"
     assert offs[n_u] == cfg.T * k
+    check_work(layer.sched, uniq, rows)
+    assert int(cpu(layer.sched.n_work)[0]) <= layer.max_work(routing)
     report["n_unique"] = n_u
 
     # ---- layer output ---------------------------------------------------

@@ -92,7 +92,7 @@ def test_topk_validation(L, buf):
 
 
 def _sched(p, bad=None):
-    s = lib.dmoe_schedule(p, p, p, p, p)
+    s = lib.dmoe_schedule(p, p, p, p, p, p, p)
     if bad:
         setattr(s, bad, None)
     return s
@@ -101,7 +101,7 @@ def _sched(p, bad=None):
 def test_schedule_validation(L, buf):
     _, p = buf
     f = "dmoe_build_expert_schedule"
-    for field in ("n_unique", "unique", "offsets", "row_token", "row_slot"):
+    for field in ("n_unique", "unique", "offsets", "row_token", "row_slot", "n_work", "work"):
         assert status(L, f, p, 1, 32, 8, 256, _sched(p, field), None)[0] == lib.DMOE_ERR_INVALID_ARG
     assert status(L, f, None, 1, 32, 8, 256, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
     assert status(L, f, p, 0, 32, 8, 256, _sched(p), None)[0] == lib.DMOE_ERR_INVALID_ARG
@@ -114,10 +114,10 @@ def test_schedule_validation(L, buf):
 
 def _ffn(L, p, **over):
     a = dict(x=p, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512, k=8,
-             max_unique=8, sched=lib.dmoe_schedule(p, p, p, p, p), slot=p, shared=p, ws=p, ws_bytes=1 << 30)
+             max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, shared=p, ws=p, ws_bytes=1 << 30)
     a.update(over)
     return status(L, "dmoe_expert_ffn", a["x"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"], a["T"],
-                  a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_unique"], a["sched"], a["slot"],
+                  a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"],
                   a["shared"], a["ws"], a["ws_bytes"], None)
 
 
@@ -129,8 +129,10 @@ def test_ffn_validation(L, buf):
     assert _ffn(L, p, ws=None)[0] == INV
     assert _ffn(L, p, dt=5)[0] == INV
     assert _ffn(L, p, k=0)[0] == INV
-    assert _ffn(L, p, max_unique=0)[0] == INV
-    assert _ffn(L, p, max_unique=257)[0] == INV
+    assert _ffn(L, p, max_work=0)[0] == INV
+    assert _ffn(L, p, max_work=257)[0] == INV  # more than T*k
+    assert _ffn(L, p, sched=lib.dmoe_schedule(p, p, p, p, p, p, None))[0] == INV
+    assert _ffn(L, p, sched=lib.dmoe_schedule(p, p, p, p, p, p, p + 4))[0] == INV
     assert _ffn(L, p, ws2=None)[0] == INV            # shared pair inconsistent
     assert _ffn(L, p, shared=None)[0] == INV
     assert _ffn(L, p, I_s=0)[0] == INV               # shared pointers set without a shared expert
@@ -138,13 +140,13 @@ def test_ffn_validation(L, buf):
     assert st == INV and "workspace" in msg
     assert _ffn(L, p, slot=p + 4)[0] == INV
     assert _ffn(L, p, w2=p + 8)[0] == INV
-    assert _ffn(L, p, sched=lib.dmoe_schedule(p, None, p, p, p))[0] == INV
+    assert _ffn(L, p, sched=lib.dmoe_schedule(p, None, p, p, p, p, p))[0] == INV
     assert _ffn(L, p, H=2004)[0] == INV              # not a whole number of 16-byte chunks
     assert _ffn(L, p, dt=lib.DMOE_F32, H=98, ws_bytes=1 << 30)[0] == INV
     assert _ffn(L, p, H=2000)[0] == UNS
     assert _ffn(L, p, I=500)[0] == UNS
-    assert _ffn(L, p, E=1024, max_unique=8)[0] == UNS
-    st, msg = _ffn(L, p, T=1 << 20, k=64, E=512, max_unique=64, I=1024, I_s=1024, H=128)
+    assert _ffn(L, p, E=1024, max_work=8)[0] == UNS
+    st, msg = _ffn(L, p, T=1 << 20, k=64, E=512, max_work=64, I=1024, I_s=1024, H=128)
     assert st == INV and "too large" in msg
 
 
@@ -188,7 +190,7 @@ def test_combine_validation(L, buf):
 
 def _route(L, p, routing, **over):
     a = dict(x=p, w=p, bias=None, dt=lib.DMOE_BF16, nb=1, bs=32, T=32, H=2048, E=256, k=8, logits=None, probs=p,
-             xc=None, scores=None, experts=p, cw=p, gap=None, sched=lib.dmoe_schedule(p, p, p, p, p), ws=None,
+             xc=None, scores=None, experts=p, cw=p, gap=None, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), ws=None,
              ws_bytes=0)
     a.update(over)
     if routing == "block":
@@ -207,7 +209,7 @@ def test_route_validation(L, buf, routing):
     assert _route(L, p, routing, x=None)[0] == INV
     assert _route(L, p, routing, experts=None)[0] == INV
     assert _route(L, p, routing, cw=None)[0] == INV
-    assert _route(L, p, routing, sched=lib.dmoe_schedule(p, p, None, p, p))[0] == INV
+    assert _route(L, p, routing, sched=lib.dmoe_schedule(p, p, None, p, p, p, p))[0] == INV
     assert _route(L, p, routing, dt=4)[0] == INV
     assert _route(L, p, routing, k=0)[0] == INV
     assert _route(L, p, routing, k=9, E=8)[0] == INV
@@ -223,6 +225,24 @@ def test_route_validation(L, buf, routing):
         assert _route(L, p, routing, nb=2**20, bs=2**11)[0] == INV
     else:
         assert _route(L, p, routing, T=0)[0] == INV
+
+
+@pytest.mark.parametrize("n_groups,gs,k,E,expect", [
+    (1, 32, 8, 256, 8),        # one decode block: one item per expert
+    (32, 1, 8, 256, 256),      # its token routing: one row per item at worst
+    (16, 32, 8, 256, 128),     # 4096 rows, items of >= 32 rows
+    (64, 64, 8, 256, 512),     # 32768 rows, full items only
+    (3, 5, 3, 7, 8),           # 45 rows over <= 7 experts: one partial item each
+    (1, 1, 1, 1, 1),
+    (8, 100, 8, 256, 164),     # 6400 rows: 100 full items + one partial per expert (<= 64)
+])
+def test_schedule_max_work(n_groups, gs, k, E, expect):
+    assert lib.dmoe_schedule_max_work(n_groups, gs, k, E) == expect
+
+
+def test_schedule_max_work_invalid():
+    assert lib.dmoe_schedule_max_work(0, 32, 8, 256) == 0
+    assert lib.dmoe_schedule_max_work(1, 32, 9, 8) == 0
 
 
 def test_router_workspace_size():

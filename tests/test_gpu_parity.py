@@ -8,7 +8,7 @@ import oracle as O
 from dmoe_synth import get_config, make_inputs
 from paper_2605_30876_amd import lib
 from paper_2605_30876_amd.layer import MoELayer, pack_weights
-from parity import run_and_check
+from parity import check_work, run_and_check
 
 pytestmark = pytest.mark.gpu
 
@@ -133,7 +133,7 @@ def test_schedule_against_oracle(gpu_lib, n_groups, gs, k, E):
     pop = rng.zipf(1.3, size=E).astype(np.float64)
     pop /= pop.sum()
     ex = np.stack([rng.choice(E, size=k, replace=False, p=pop) for _ in range(n_groups)]).astype(np.int32)
-    sched = lib.Schedule.empty(E, n_groups * gs * k, "cuda")
+    sched = lib.Schedule.empty(E, n_groups * gs * k, "cuda", lib.dmoe_schedule_max_work(n_groups, gs, k, E))
     lib.dmoe_build_expert_schedule(torch.from_numpy(ex).cuda(), n_groups, gs, k, E, sched)
     torch.cuda.synchronize()
     uniq = O.unique_experts(ex)
@@ -146,6 +146,8 @@ def test_schedule_against_oracle(gpu_lib, n_groups, gs, k, E):
     for u, e in enumerate(uniq.tolist()):
         assert list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist())) == rows[e]
     assert offs[n] == n_groups * gs * k
+    check_work(sched, uniq, rows)
+    assert int(sched.n_work[0]) <= lib.dmoe_schedule_max_work(n_groups, gs, k, E)
 
 
 @pytest.mark.parametrize("name", ["small_bf16", "decode_b1"])
