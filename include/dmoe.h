@@ -102,7 +102,7 @@ typedef enum dmoe_dtype {
  *                       expert id, then row.  max_work: dmoe_schedule_max_work.
  * Within one expert, rows are ordered by token.
  */
-#define DMOE_WORK_ROWS 64
+#define DMOE_WORK_ROWS 128
 
 typedef struct dmoe_schedule {
   int32_t* n_unique;

@@ -287,6 +287,137 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   }
 }
 
+// ---- tile kernels: many tokens per work item --------------------------------
+//
+// A workgroup covers 64 weight rows (wave w: packed 16-row tile 4*bx + w,
+// over the whole reduction) x up to 128 tokens of one work item (8 token
+// tiles).  The reduction runs in stages of kStageSteps K-steps: the
+// stage's token fragments are loaded from global memory once per workgroup
+// into a double-buffered LDS stage and read by all four waves, while each
+// wave streams its own weight tile into registers one stage ahead.
+// Accumulation order (K ascending) and the epilogues match the decode
+// kernels.
+constexpr int kTileTok = 8;       // token tiles per workgroup (128 tokens)
+constexpr int kStageSteps = 4;    // K-steps per LDS stage
+static_assert(kTileTok * 16 == DMOE_WORK_ROWS, "a tile workgroup covers one work item's rows");
+
+template <bool kGateUp>
+__global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p) {
+  Group g;
+  if (!decode_item(blockIdx.y, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g)) return;
+  const int H = p.H;
+  const int Iw = g.expert >= 0 ? p.I : p.I_s;
+  const int Kd = kGateUp ? H : Iw;                    // reduction length
+  const int tiles = kGateUp ? Iw / 8 : H / 16;        // packed 16-row tiles of the matrix
+  if (blockIdx.x * 4 >= tiles) return;                // uniform: the whole workgroup is past the matrix
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tile = blockIdx.x * 4 + wave;             // tiles % 4 == 0 (H, I, I_s multiples of 128)
+  const int ksteps = Kd >> 5;                         // multiple of kStageSteps
+  const bf16_t* W;
+  if (kGateUp)
+    W = g.expert >= 0 ? p.w13 + static_cast<size_t>(g.expert) * 2 * p.I * H : p.ws13;
+  else
+    W = g.expert >= 0 ? p.w2 + static_cast<size_t>(g.expert) * H * p.I : p.ws2;
+  const bf16_t* pa = W + static_cast<size_t>(tile) * ksteps * kFrag + lane * 8;
+  const int nt = (g.n + 15) >> 4;  // live token tiles
+
+  // Token-fragment producer: thread t loads pieces (tile t/64, lane t%64) and
+  // (tile t/64 + 4, same lane) of every K-step of a stage.
+  const int tid = threadIdx.x;
+  const int pl = tid & 63, pq = pl >> 4, pc = pl & 15, pct = tid >> 6;
+  const int rows_b = kGateUp ? p.T : p.R;  // rows of the chunk-major source
+  const bf16_t* src = kGateUp ? p.xk : p.hk;
+  const int bstep = 32 * rows_b;
+  const bf16_t* pb[2];
+  bool pl_live[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int ct = pct + 4 * h;
+    const int col = min(ct * 16 + pc, g.n - 1);
+    int row;
+    if (kGateUp)
+      row = g.tok ? g.tok[col] : g.t0 + col;
+    else
+      row = g.r0 + col;
+    pb[h] = src + (static_cast<size_t>(pq) * rows_b + row) * 8;
+    pl_live[h] = ct < nt;
+  }
+
+  __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 64 KiB
+  f32x4 acc[kTileTok];
+#pragma unroll
+  for (int ct = 0; ct < kTileTok; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 a_cur[kStageSteps], a_nxt[kStageSteps], b_nxt[kStageSteps][2];
+
+  auto load_stage = [&](int st) {
+#pragma unroll
+    for (int s = 0; s < kStageSteps; ++s) {
+      const int ks = st * kStageSteps + s;
+      a_nxt[s] = ld_bf16x8(pa + ks * kFrag);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (pl_live[h]) b_nxt[s][h] = ld_bf16x8(pb[h] + ks * bstep);
+    }
+  };
+  auto store_stage = [&](int buf) {
+#pragma unroll
+    for (int s = 0; s < kStageSteps; ++s)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (pl_live[h]) stage[buf][s][pct + 4 * h][pl] = b_nxt[s][h];
+  };
+
+  const int nstages = ksteps / kStageSteps;
+  load_stage(0);
+  store_stage(0);
+#pragma unroll
+  for (int s = 0; s < kStageSteps; ++s) a_cur[s] = a_nxt[s];
+  __syncthreads();
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st & 1;
+    const bool more = st + 1 < nstages;
+    if (more) load_stage(st + 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < kStageSteps; ++s)
+#pragma unroll
+      for (int ct = 0; ct < kTileTok; ++ct)
+        if (ct < nt)
+          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur[s], stage[buf][s][ct][lane], acc[ct], 0, 0, 0);
+    if (more) {
+      store_stage(buf ^ 1);
+#pragma unroll
+      for (int s = 0; s < kStageSteps; ++s) a_cur[s] = a_nxt[s];
+    }
+    __syncthreads();
+  }
+
+  const int q = lane >> 4, c = lane & 15;
+#pragma unroll
+  for (int ct = 0; ct < kTileTok; ++ct) {
+    const int col = ct * 16 + c;
+    if (ct >= nt || col >= g.n) continue;
+    const f32x4 v = acc[ct];
+    if (kGateUp) {
+      // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*tile + 2q
+      const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
+      const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3]);
+      bf16_t* dst = p.hk + (static_cast<size_t>(tile) * p.R + g.r0 + col) * 8 + 2 * q;
+      *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
+    } else {
+      const int j = tile * 16 + 4 * q;
+      float* dst;
+      if (g.tok) {
+        const int r = g.r0 + col;
+        dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H + j;
+      } else {
+        dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H + j;
+      }
+      *reinterpret_cast<f32x4*>(dst) = v;
+    }
+  }
+}
+
 // ---- f32 path -------------------------------------------------------------
 
 __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
@@ -377,6 +508,11 @@ hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool use_tile_kernels(int T, int k, int max_work, int ldh) {
+  const long rows = (static_cast<long>(T) * k + max_work - 1) / max_work;
+  return rows >= 32 && static_cast<long>(ldh / 32) * max_work >= 512;
+}
+
 }  // namespace
 
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt) {
@@ -397,6 +533,13 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
                 a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
+    if (use_tile_kernels(a.T, a.k, a.max_work, ldh)) {
+      ffn_tile_bf16_kernel<true><<<dim3(ldh / 32, items), kThreads, 0, s>>>(p);
+      hipError_t err = hipGetLastError();
+      if (err != hipSuccess) return err;
+      ffn_tile_bf16_kernel<false><<<dim3(a.H / 64, items), kThreads, 0, s>>>(p);
+      return hipGetLastError();
+    }
     switch (pick_ntiles(a.T, a.k, a.max_work)) {
       case 1: return launch_bf16<1>(p, ldh, items, s);
       case 2: return launch_bf16<2>(p, ldh, items, s);

@@ -39,7 +39,7 @@ class DmoeError(RuntimeError):
         self.status = status
 
 
-WORK_ROWS = 64  # DMOE_WORK_ROWS: rows of one expert per work item at most
+WORK_ROWS = 128  # DMOE_WORK_ROWS: rows of one expert per work item at most
 
 
 class dmoe_schedule(ctypes.Structure):

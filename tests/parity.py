@@ -14,6 +14,7 @@ import numpy as np
 import torch
 
 import oracle as O
+from paper_2605_30876_amd import lib
 from paper_2605_30876_amd.layer import pack_weights
 
 BF16_TOL = 2e-2   # max|y - y_ref| <= 2e-2 * RMS(y_ref) for bf16 weights
@@ -51,7 +52,7 @@ def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: lis
     return out
 
 
-def expected_work(uniq, rows: dict, work_rows: int = 64):
+def expected_work(uniq, rows: dict, work_rows: int = 128):
     """Work items {expert, first row, rows} from the oracle's per-expert rows:
     each unique expert's rows, in ascending id order, cut into pieces of at
     most work_rows (the schedule's documented layout)."""
@@ -65,7 +66,7 @@ def expected_work(uniq, rows: dict, work_rows: int = 64):
 
 
 def check_work(sched, uniq, rows: dict):
-    items = expected_work(uniq, rows)
+    items = expected_work(uniq, rows, lib.WORK_ROWS)
     n_work = int(cpu(sched.n_work)[0])
     assert n_work == len(items), f"n_work {n_work} != {len(items)}"
     got = cpu(sched.work)[:n_work].numpy().tolist()

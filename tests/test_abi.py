@@ -231,10 +231,10 @@ def test_route_validation(L, buf, routing):
     (1, 32, 8, 256, 8),        # one decode block: one item per expert
     (32, 1, 8, 256, 256),      # its token routing: one row per item at worst
     (16, 32, 8, 256, 128),     # 4096 rows, items of >= 32 rows
-    (64, 64, 8, 256, 512),     # 32768 rows, full items only
+    (64, 64, 8, 256, 512),     # 32768 rows, items of >= 64 rows
     (3, 5, 3, 7, 8),           # 45 rows over <= 7 experts: one partial item each
     (1, 1, 1, 1, 1),
-    (8, 100, 8, 256, 164),     # 6400 rows: 100 full items + one partial per expert (<= 64)
+    (8, 100, 8, 256, 114),     # 6400 rows: 50 full items + one partial per expert (<= 64)
 ])
 def test_schedule_max_work(n_groups, gs, k, E, expect):
     assert lib.dmoe_schedule_max_work(n_groups, gs, k, E) == expect

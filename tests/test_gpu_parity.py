@@ -40,6 +40,23 @@ def test_small_layer_parity(gpu_lib, name, routing, seed):
     _say("  ", rep)
 
 
+# Shapes whose expert FFN takes the tile kernels (work items of >= 32 rows on
+# average, >= 512 tile workgroups) while the oracle still checks every token:
+# 8 blocks of 32 tokens over 32 experts, and 4 blocks of 64 with top-8.
+TILE = {"tile_b8x32": dict(H=512, E=32, I=512, I_s=512, k=4, NB=8, bs=32),
+        "tile_b4x64": dict(H=256, E=16, I=1024, I_s=512, k=8, NB=4, bs=64)}
+
+
+@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("name", list(TILE))
+def test_tile_kernel_parity(gpu_lib, name, routing):
+    cfg = get_config("small_bf16").with_(name=name, **TILE[name])
+    _say("case", name, routing)
+    d = _to_gpu(make_inputs(cfg, seed=3))
+    rep = run_and_check(cfg, d, routing, _layer(cfg))
+    _say("  ", {k: v for k, v in rep.items() if k != "near_ties"})
+
+
 # Full-size layers: routing and schedule are checked on every token, the
 # output on a sample of tokens the oracle computes one by one.
 FULL = {"decode_b1": None, "decode_b16": [0, 1, 31, 32, 250, 511], "large_zipf_b8": [0, 77, 255],
