@@ -239,6 +239,17 @@ def top_p(scores: np.ndarray, p: float, min_size: int = 1) -> np.ndarray:
     return order[:max(n, min_size)].astype(np.int32)
 
 
+def normalize(S: np.ndarray) -> np.ndarray:
+    """Normalize of Alg. 1: S / sum(S), the sum taken in expert-id order in
+    float32 (the paper fixes no order; a fixed one makes the Top-P cut a
+    reproducible float32 decision)."""
+    S = np.asarray(S, dtype=np.float32)
+    total = np.float32(0.0)
+    for v in S:
+        total = np.float32(total + v)
+    return (S / total).astype(np.float32)
+
+
 def alg1_route(token_scores: np.ndarray, k: int, p: float, min_coreset: int | None = None):
     """Alg. 1 on one block: returns (S_block, coreset C, routed experts R[bs, k]).
 
@@ -252,8 +263,7 @@ def alg1_route(token_scores: np.ndarray, k: int, p: float, min_coreset: int | No
     S = np.zeros(E, dtype=np.float32)
     for i in range(n_tok):
         S = (S + topk_mask(s[i], k)).astype(np.float32)
-    total = np.float32(S.sum(dtype=np.float32))
-    S_norm = (S / total).astype(np.float32)
+    S_norm = normalize(S)
     C = top_p(S_norm, p, min_size=k if min_coreset is None else min_coreset)
     R = np.zeros((n_tok, k), dtype=np.int32)
     inside = np.zeros(E, dtype=bool)
