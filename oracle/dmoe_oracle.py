@@ -274,6 +274,27 @@ def alg1_route(token_scores: np.ndarray, k: int, p: float, min_coreset: int | No
     return S, C, R
 
 
+def alg1_valid_coresets(S_norm: np.ndarray, p: float, min_size: int, tol: float = NEAR_TIE):
+    """The coresets Top-P may return when values within ``tol`` are treated as
+    tied: the cut may move by one where the cumulative mass is within tol of
+    p, and at each admissible size any near-tied ranking at the cut is valid
+    (used only to accept a GPU decision at a near-tie)."""
+    s = np.asarray(S_norm, dtype=np.float32)
+    E = s.shape[0]
+    n_ref = top_p(s, p, min_size).size
+    order = ranked(s)
+    acc = np.cumsum(s[order].astype(np.float64))
+    sizes = {n_ref}
+    if n_ref - 1 >= max(min_size, 1) and acc[n_ref - 2] >= p - tol:
+        sizes.add(n_ref - 1)
+    if n_ref + 1 <= E and acc[n_ref - 1] < p + tol:
+        sizes.add(n_ref + 1)
+    out = set()
+    for n in sizes:
+        out.update(valid_topk_sets(s, n, tol))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # Expert FFN and combine (float64)
 # ---------------------------------------------------------------------------

@@ -431,3 +431,81 @@ def test_planted_mistake_is_caught(monkeypatch, attr, bad, pin):
             fn("block")
         else:
             fn()
+
+
+# ---- Alg. 1 (TopKMask-sum, Normalize, Top-P coreset, top-k inside it) ------
+
+def _probs(rng, T, E):
+    z = rng.standard_normal((T, E)).astype(np.float32)
+    return O.softmax_rows(z)
+
+
+@pytest.mark.parametrize("E,k,p", [(16, 2, 0.6), (64, 8, 0.4), (32, 4, 0.9)])
+def test_alg1_block_of_one_token_is_token_routing(E, k, p):
+    """With one token, the coreset holds that token's top-k (the only non-zero
+    scores, ranked first, and padded to k), so Alg. 1 routes it like top-k."""
+    rng = np.random.default_rng(E + k)
+    probs = _probs(rng, 5, E)
+    for t in range(5):
+        _, C, R = O.alg1_route(probs[t:t + 1], k, p)
+        idx, _ = O.topk(probs[t], k)
+        assert set(C.tolist()) == set(idx.tolist())
+        assert R[0].tolist() == idx.tolist()
+
+
+@pytest.mark.parametrize("min_coreset", [None, "E"])
+def test_alg1_full_coreset_is_token_routing(min_coreset):
+    """p = 1 (or a coreset forced to all experts) keeps every token's own top-k
+    inside the coreset, so every token is routed like top-k."""
+    rng = np.random.default_rng(11)
+    E, k, bs = 24, 3, 6
+    probs = _probs(rng, bs, E)
+    p = 1.0 if min_coreset is None else 0.3
+    _, C, R = O.alg1_route(probs, k, p, None if min_coreset is None else E)
+    for t in range(bs):
+        idx, _ = O.topk(probs[t], k)
+        assert set(idx.tolist()) <= set(C.tolist())
+        assert R[t].tolist() == idx.tolist()
+
+
+def test_alg1_coreset_is_shortest_prefix_reaching_p():
+    """The coreset's normalised mass reaches p and drops below p without its
+    last expert (when larger than the minimum); the size never falls as p
+    grows; every routed expert lies in the coreset."""
+    rng = np.random.default_rng(5)
+    E, k, bs = 40, 4, 8
+    probs = _probs(rng, bs, E)
+    sizes = []
+    for p in np.linspace(0.05, 1.0, 20):
+        S, C, R = O.alg1_route(probs, k, float(p))
+        Sn = S / S.sum(dtype=np.float64)
+        mass = Sn[C].sum()
+        assert mass >= p - 1e-6
+        if C.size > k:
+            assert mass - Sn[C[-1]] < p + 1e-6
+        assert set(R.reshape(-1).tolist()) <= set(C.tolist())
+        sizes.append(C.size)
+    assert sizes == sorted(sizes)
+
+
+def test_alg1_scores_are_topk_masked_sums():
+    """S counts only each token's own top-k probabilities: summing the masks
+    over tokens in float64 agrees, and S's total is the retained mass."""
+    rng = np.random.default_rng(9)
+    E, k, bs = 20, 3, 7
+    probs = _probs(rng, bs, E)
+    S, _, _ = O.alg1_route(probs, k, 0.5)
+    ref = np.zeros(E)
+    for t in range(bs):
+        idx, _ = O.topk(probs[t], k)
+        ref[idx] += probs[t][idx]
+    np.testing.assert_allclose(S, ref, rtol=1e-6)
+    assert np.count_nonzero(S) <= bs * k
+
+
+def test_alg1_valid_coresets_contains_reference():
+    rng = np.random.default_rng(3)
+    probs = _probs(rng, 8, 32)
+    S, C, _ = O.alg1_route(probs, 4, 0.6)
+    Sn = O.normalize(S)
+    assert frozenset(C.tolist()) in O.alg1_valid_coresets(Sn, 0.6, 4)
