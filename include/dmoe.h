@@ -12,6 +12,9 @@
  *                              (Sec. 4.2 aggregation; Alg. 1 with |C| = k)
  *   dmoe_token_topk            token-level top-k (the "Original" routing of
  *                              Sec. 5.1, the baseline)
+ *   dmoe_block_topp_route      Alg. 1 with its Top-P coreset: block scores from
+ *                              each token's top-k, a shared coreset per block,
+ *                              each token's top-k inside it
  *   dmoe_build_expert_schedule unique experts of the forward and the rows
  *                              (token, slot) that use each one (the unique
  *                              expert count of Sec. 3 is its n_unique)
@@ -175,6 +178,31 @@ dmoe_status dmoe_block_aggregate_topk(const float* probs, int n_blocks, int bloc
  */
 dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* token_experts,
                             float* combine_w, float* gap, void* stream);
+
+/*
+ * Alg. 1 of Sec. 4.2 with the Top-P coreset, on each block b of block_size
+ * consecutive tokens:
+ *   S[e]  = sum over the block's tokens, in token order, of TopKMask(probs[t], k)[e]
+ *           (the token's own top-k probabilities, zeros elsewhere)
+ *   Sn[e] = S[e] / sum_e' S[e']          (Normalize; the sum in expert-id order)
+ *   C_b   = the shortest prefix of the experts ranked by Sn (desc, id asc) whose
+ *           cumulative Sn, summed in that order in float32, reaches p; at least
+ *           min_coreset experts                                  -> coreset[b]
+ *   R_t   = top-k of probs[t] restricted to C_b                  -> token_experts[t]
+ *   w[t][j] = probs[t][R_t[j]] / sum_j' probs[t][R_t[j']]
+ * Every token of a block picks its own k experts inside the block's shared
+ * coreset, so the unique experts of the block are at most |C_b|.
+ * probs [n_blocks*block_size][E]; block_scores [n_blocks][E] (Sn) or NULL;
+ * coreset [n_blocks][E] int32 (ids in rank order; the first coreset_size[b]
+ * are C_b); coreset_size [n_blocks] int32; token_experts [T][k] int32;
+ * combine_w [T][k]; gap [T] or NULL (k-th minus (k+1)-th probability inside
+ * C_b; +inf if |C_b| == k).  Schedule token_experts with group_size = 1.
+ * Limits: 1 <= k <= min(E, 64); k <= min_coreset <= E; 0 < p <= 1;
+ * 1 <= block_size <= 4096; E <= 1024 and block_size*k <= 8192 (kernel limits).
+ */
+dmoe_status dmoe_block_topp_route(const float* probs, int n_blocks, int block_size, int E, int k, float p,
+                                  int min_coreset, float* block_scores, int32_t* coreset, int32_t* coreset_size,
+                                  int32_t* token_experts, float* combine_w, float* gap, void* stream);
 
 /*
  * Unique-expert schedule.  experts [n_groups][k] int32 holds one expert list

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdmoe.so")
-SOURCES = ["dmoe_api.cpp", "router.hip", "routing.hip", "schedule.hip", "route.hip", "pack.hip",
+SOURCES = ["dmoe_api.cpp", "router.hip", "routing.hip", "topp.hip", "schedule.hip", "route.hip", "pack.hip",
            "ffn.hip", "combine.hip"]
 ARCH = os.environ.get("DMOE_OFFLOAD_ARCH", "gfx950")
 

@@ -127,6 +127,33 @@ dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* to
                     __func__);
 }
 
+dmoe_status dmoe_block_topp_route(const float* probs, int n_blocks, int block_size, int E, int k, float p,
+                                  int min_coreset, float* block_scores, int32_t* coreset, int32_t* coreset_size,
+                                  int32_t* token_experts, float* combine_w, float* gap, void* stream) {
+  REQUIRE(probs && coreset && coreset_size && token_experts && combine_w,
+          "probs, coreset, coreset_size, token_experts and combine_w must not be NULL");
+  REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
+  REQUIRE(block_size >= 1 && block_size <= 4096, "block_size=%d must be in [1, 4096]", block_size);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(min_coreset >= k && min_coreset <= E, "min_coreset=%d must be in [k, E]", min_coreset);
+  REQUIRE(p > 0.f && p <= 1.f, "p=%g must be in (0, 1]", static_cast<double>(p));
+  REQUIRE(static_cast<long>(n_blocks) * block_size * E <= kIntLimit, "T*E must fit in int32");
+  ALIGNED(probs);
+  ALIGNED(block_scores);
+  ALIGNED(coreset);
+  ALIGNED(coreset_size);
+  ALIGNED(token_experts);
+  ALIGNED(combine_w);
+  ALIGNED(gap);
+  SUPPORT(E <= 1024, "the Top-P coreset supports E <= 1024 (E=%d)", E);
+  SUPPORT(static_cast<long>(block_size) * k <= 8192, "the Top-P coreset supports block_size*k <= 8192");
+  return hip_status(dmoe::launch_block_topp(probs, n_blocks, block_size, E, k, p, min_coreset, block_scores,
+                                            coreset, coreset_size, token_experts, combine_w, gap,
+                                            static_cast<hipStream_t>(stream)),
+                    __func__);
+}
+
 dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int group_size, int k,
                                        int E, dmoe_schedule sched, void* stream) {
   REQUIRE(experts, "experts must not be NULL");

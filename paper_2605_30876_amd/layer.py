@@ -45,7 +45,11 @@ def pack_weights(w: dict, keep_unpacked: bool = False) -> dict:
 class MoELayer:
     def __init__(self, H: int, E: int, I: int, I_s: int, k: int, n_blocks: int, block_size: int,
                  dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False,
-                 out_dtype: torch.dtype = torch.float32):
+                 out_dtype: torch.dtype = torch.float32, top_p: float = 0.6, min_coreset: int | None = None):
+        """Routing modes: "block" (block top-k), "token" (token top-k, the
+        baseline) and "topp" (Alg. 1: a Top-P coreset per block with mass
+        ``top_p`` and at least ``min_coreset`` (default k) experts, each token's
+        top-k inside it)."""
         self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
         self.NB, self.bs = n_blocks, block_size
         self.T = T = n_blocks * block_size
@@ -61,10 +65,15 @@ class MoELayer:
         self.block_gap = torch.empty((n_blocks,), **f32)
         self.token_experts = torch.empty((T, k), **i32)
         self.token_gap = torch.empty((T,), **f32)
+        self.top_p = top_p
+        self.min_coreset = k if min_coreset is None else min_coreset
+        self.coreset = torch.empty((n_blocks, E), **i32)
+        self.coreset_size = torch.empty((n_blocks,), **i32)
         self.combine_w = torch.empty((T, k), **f32)
         # work-item capacity: the larger of the two routings' bounds
         self._max_work = {"block": lib.dmoe_schedule_max_work(n_blocks, block_size, k, E),
                           "token": lib.dmoe_schedule_max_work(T, 1, k, E)}
+        self._max_work["topp"] = self._max_work["token"]
         self.sched = lib.Schedule.empty(E, T * k, device, max(self._max_work.values()))
         self.slot_out = torch.empty((T, k, H), **f32)
         self.shared_out = torch.empty((T, H), **f32) if I_s > 0 else None
@@ -82,16 +91,17 @@ class MoELayer:
 
     def route(self, x, w_router, bias=None, routing: str = "block", stream=None, fused: bool = True):
         """Routing stage: one dmoe_route_* call, or (fused=False) the chain of
-        the separate entry points; both give identical results."""
+        the separate entry points; both give identical results.  "topp" runs
+        the router, dmoe_block_topp_route and a token-level schedule."""
         T, H, E, k = self.T, self.H, self.E, self.k
-        if routing not in ("block", "token"):
-            raise ValueError(f"routing must be 'block' or 'token', not {routing!r}")
+        if routing not in ("block", "token", "topp"):
+            raise ValueError(f"routing must be 'block', 'token' or 'topp', not {routing!r}")
         if fused and routing == "block":
             lib.dmoe_route_block(x, w_router, bias, self.NB, self.bs, H, E, k, self.logits, self.probs,
                                  self.x_chunked, self.block_scores, self.block_experts, self.combine_w,
                                  self.block_gap, self.sched, self.router_ws, stream)
             return
-        if fused:
+        if fused and routing == "token":
             lib.dmoe_route_token(x, w_router, bias, T, H, E, k, self.logits, self.probs, self.x_chunked,
                                  self.token_experts, self.combine_w, self.token_gap, self.sched, self.router_ws,
                                  stream)
@@ -102,10 +112,15 @@ class MoELayer:
             lib.dmoe_block_aggregate_topk(self.probs, self.NB, self.bs, E, k, self.block_scores,
                                           self.block_experts, self.combine_w, self.block_gap, stream)
             lib.dmoe_build_expert_schedule(self.block_experts, self.NB, self.bs, k, E, self.sched, stream)
+            return
+        if routing == "topp":
+            lib.dmoe_block_topp_route(self.probs, self.NB, self.bs, E, k, self.top_p, self.min_coreset,
+                                      self.block_scores, self.coreset, self.coreset_size, self.token_experts,
+                                      self.combine_w, self.token_gap, stream)
         else:
             lib.dmoe_token_topk(self.probs, T, E, k, self.token_experts, self.combine_w, self.token_gap,
                                 stream)
-            lib.dmoe_build_expert_schedule(self.token_experts, T, 1, k, E, self.sched, stream)
+        lib.dmoe_build_expert_schedule(self.token_experts, T, 1, k, E, self.sched, stream)
 
     def experts_ffn(self, w: dict, routing: str = "block", stream=None):
         """Expert FFN on the chunk-major copy of x that :meth:`route` stored."""
@@ -130,3 +145,9 @@ class MoELayer:
 
     def gaps(self, routing: str) -> torch.Tensor:
         return self.block_gap if routing == "block" else self.token_gap
+
+    def coresets(self) -> list:
+        """Alg. 1 coresets of the last "topp" routing (host lists of ids, rank order)."""
+        sizes = self.coreset_size.cpu().tolist()
+        rows = self.coreset.cpu()
+        return [rows[b, :n].tolist() for b, n in enumerate(sizes)]

@@ -29,7 +29,7 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 
 # Every symbol include/dmoe.h declares.
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
-           "dmoe_build_expert_schedule", "dmoe_schedule_max_work", "dmoe_route_block", "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights",
+           "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work", "dmoe_route_block", "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights",
            "dmoe_ffn_workspace_size", "dmoe_expert_ffn", "dmoe_combine", "dmoe_last_error", "dmoe_version")
 
 
@@ -56,6 +56,7 @@ _SIGS = {
     "dmoe_router_logits": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P], _I),
     "dmoe_block_aggregate_topk": ([_P, _I, _I, _I, _I, _P, _P, _P, _P, _P], _I),
     "dmoe_token_topk": ([_P, _I, _I, _I, _P, _P, _P, _P], _I),
+    "dmoe_block_topp_route": ([_P, _I, _I, _I, _I, ctypes.c_float, _I, _P, _P, _P, _P, _P, _P, _P], _I),
     "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
     "dmoe_schedule_max_work": ([_I, _I, _I, _I], _I),
     "dmoe_route_block": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S,
@@ -145,6 +146,13 @@ def dmoe_block_aggregate_topk(probs, n_blocks, block_size, E, k, block_scores, b
 def dmoe_token_topk(probs, T, E, k, token_experts, combine_w, gap, stream=None):
     _check(load().dmoe_token_topk(ptr(probs), T, E, k, ptr(token_experts), ptr(combine_w), ptr(gap),
                                   stream_handle(stream)))
+
+
+def dmoe_block_topp_route(probs, n_blocks, block_size, E, k, p, min_coreset, block_scores, coreset, coreset_size,
+                          token_experts, combine_w, gap, stream=None):
+    _check(load().dmoe_block_topp_route(ptr(probs), n_blocks, block_size, E, k, float(p), min_coreset,
+                                        ptr(block_scores), ptr(coreset), ptr(coreset_size), ptr(token_experts),
+                                        ptr(combine_w), ptr(gap), stream_handle(stream)))
 
 
 @dataclass

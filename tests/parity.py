@@ -168,3 +168,85 @@ def run_and_check(cfg, d_gpu: dict, routing: str, layer, sample_tokens=None, che
         torch.cuda.synchronize()
         assert torch.equal(y, y2), "two runs differ bitwise"
     return report
+
+
+def run_and_check_topp(cfg, d_gpu: dict, layer, sample_tokens=None, check_determinism=True, packed=None):
+    """Alg. 1 with the Top-P coreset: GPU forward vs the oracle's alg1_route.
+
+    Coresets must equal the oracle's, or (near-tie: the cumulative mass or the
+    ranking at the cut within NEAR_TIE) be one the oracle enumerates as valid;
+    each token's experts inside the accepted coreset must be the oracle's
+    top-k there (near-ties as in run_and_check)."""
+    x = d_gpu["x"]
+    wp = packed if packed is not None else pack_weights(d_gpu)
+    y = layer.forward(x, wp, "topp").clone()
+    torch.cuda.synchronize()
+    report = {"near_ties": []}
+    k, bs, p_thr, min_c = cfg.k, cfg.bs, layer.top_p, layer.min_coreset
+
+    z = O.router_logits(x, d_gpu["w_router"], d_gpu.get("bias"))
+    p = O.softmax_rows(z)
+    perr = float(np.max(np.abs(cpu(layer.probs).numpy() - p)))
+    assert perr <= PROB_TOL, f"router probabilities differ by {perr:.3g}"
+
+    sn_gpu = cpu(layer.block_scores).numpy()
+    cores = layer.coresets()
+    sel_gpu = cpu(layer.token_experts).numpy()
+    w_gpu = cpu(layer.combine_w).numpy()
+    ept = np.zeros((cfg.T, k), dtype=np.int32)
+    for b in range(cfg.NB):
+        blk = p[b * bs:(b + 1) * bs]
+        S, C, _ = O.alg1_route(blk, k, p_thr, min_c)
+        sn = O.normalize(S)
+        serr = float(np.max(np.abs(sn_gpu[b] - sn)))
+        assert serr <= PROB_TOL, f"block {b}: normalised scores differ by {serr:.3g}"
+        if cores[b] == C.tolist():
+            coreset = C
+        else:
+            assert frozenset(cores[b]) in O.alg1_valid_coresets(sn, p_thr, min_c), (
+                f"block {b}: coreset {sorted(cores[b])} is not a valid Top-P coreset (oracle {sorted(C.tolist())})")
+            coreset = np.asarray(cores[b], dtype=np.int32)
+            report["near_ties"].append({"what": "coreset", "block": b})
+        inside = np.zeros(cfg.E, dtype=bool)
+        inside[coreset] = True
+        masked = np.where(inside[None, :], blk, np.float32(-np.inf)).astype(np.float32)
+        ept[b * bs:(b + 1) * bs] = accepted_selection(masked, sel_gpu[b * bs:(b + 1) * bs], k,
+                                                      report["near_ties"], f"topp block {b}")
+        # every GPU expert lies in the GPU's coreset
+        assert set(sel_gpu[b * bs:(b + 1) * bs].reshape(-1).tolist()) <= set(cores[b])
+
+    werr = 0.0
+    for t in range(cfg.T):
+        ref = dict(zip(ept[t].tolist(), O.renormalised_weights(p[t], ept[t]).tolist()))
+        got = dict(zip(sel_gpu[t].tolist(), w_gpu[t].tolist()))
+        assert ref.keys() == got.keys()
+        werr = max(werr, max(abs(ref[e] - got[e]) for e in ref))
+    assert werr <= PROB_TOL, f"combine weights differ by {werr:.3g}"
+
+    uniq = O.unique_experts(ept)
+    n_u = int(cpu(layer.sched.n_unique)[0])
+    assert n_u == uniq.size
+    rows = O.expert_rows(ept, 1)
+    offs = cpu(layer.sched.offsets).numpy()
+    rt, rs = cpu(layer.sched.row_token).numpy(), cpu(layer.sched.row_slot).numpy()
+    for u, e in enumerate(uniq.tolist()):
+        assert list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist())) == rows[e]
+    check_work(layer.sched, uniq, rows)
+    report["n_unique"] = n_u
+    report["coreset_sizes"] = [len(c) for c in cores]
+
+    w_acc = np.stack([O.renormalised_weights(p[t], ept[t]) for t in range(cfg.T)])
+    toks = None if sample_tokens is None else np.asarray(sample_tokens)
+    y_ref = O.combine(x, ept, w_acc, d_gpu["w_gate"], d_gpu["w_up"], d_gpu["w_down"],
+                      d_gpu.get("ws_gate"), d_gpu.get("ws_up"), d_gpu.get("ws_down"), tokens=toks)
+    y_got = cpu(y).float().numpy().astype(np.float64)
+    if toks is not None:
+        y_got = y_got[toks]
+    err = O.max_rel_err(y_got, y_ref)
+    report["y_err_rms"] = err
+    assert err <= tol_for(cfg), f"max|y - y_ref| = {err:.3g} * RMS(y_ref) > {tol_for(cfg)}"
+    if check_determinism:
+        y2 = layer.forward(x, wp, "topp").clone()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2), "two runs differ bitwise"
+    return report

@@ -245,6 +245,30 @@ def test_schedule_max_work_invalid():
     assert lib.dmoe_schedule_max_work(1, 32, 9, 8) == 0
 
 
+def test_topp_validation(L, buf):
+    _, p = buf
+    f, INV, UNS = "dmoe_block_topp_route", lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    P = ctypes.c_float
+
+    def call(**o):
+        a = dict(probs=p, nb=1, bs=32, E=256, k=8, pp=0.6, mc=8, sn=None, core=p, size=p, ex=p, w=p, gap=None)
+        a.update(o)
+        return status(L, f, a["probs"], a["nb"], a["bs"], a["E"], a["k"], P(a["pp"]), a["mc"], a["sn"], a["core"],
+                      a["size"], a["ex"], a["w"], a["gap"], None)[0]
+    assert call(probs=None) == INV
+    assert call(core=None) == INV
+    assert call(size=None) == INV
+    assert call(pp=0.0) == INV
+    assert call(pp=1.5) == INV
+    assert call(mc=7) == INV           # below k
+    assert call(mc=257) == INV         # above E
+    assert call(k=0) == INV
+    assert call(bs=0) == INV
+    assert call(ex=p + 4) == INV
+    assert call(E=2048, mc=8) == UNS
+    assert call(bs=4096, k=8) == UNS
+
+
 def test_router_workspace_size():
     # decode step: the hidden dimension is split, one fp32 partial plane per slice
     n = lib.dmoe_router_workspace_size(32, 2048, 256, lib.DMOE_BF16)

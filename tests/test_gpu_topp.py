@@ -1,0 +1,73 @@
+"""Alg. 1 with the Top-P coreset (dmoe_block_topp_route) on the GPU against the
+oracle's alg1_route, through the whole layer forward.  Marked ``gpu``."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from dmoe_synth import get_config, make_inputs
+from paper_2605_30876_amd import lib
+from paper_2605_30876_amd.layer import MoELayer
+from parity import run_and_check_topp
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer(cfg, p, min_c=None):
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    return MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt, device="cuda",
+                    top_p=p, min_coreset=min_c)
+
+
+@pytest.mark.parametrize("p", [0.4, 0.6, 0.8])
+@pytest.mark.parametrize("name", ["tiny_f32", "small_f32", "small_bf16", "small_bf16_zipf", "small_bf16_corr"])
+def test_topp_parity_small(gpu_lib, name, p):
+    cfg = get_config(name)
+    print("case", name, p, flush=True)
+    d = {k: (None if v is None else v.cuda()) for k, v in make_inputs(cfg, seed=1).items()}
+    rep = run_and_check_topp(cfg, d, _layer(cfg, p))
+    print("  ", rep, flush=True)
+
+
+@pytest.mark.parametrize("name,sample", [("decode_b1", None), ("decode_b16", [0, 31, 32, 300, 511])])
+def test_topp_parity_full(gpu_lib, name, sample):
+    cfg = get_config(name)
+    print("case", name, flush=True)
+    d = make_inputs(cfg, seed=0, device="cuda")
+    rep = run_and_check_topp(cfg, d, _layer(cfg, 0.6), sample_tokens=sample, check_determinism=(name == "decode_b1"))
+    print("  ", {k: v for k, v in rep.items() if k != "near_ties"}, flush=True)
+
+
+@pytest.mark.parametrize("min_c", ["k", "E"])
+def test_topp_edges(gpu_lib, min_c):
+    """p = 1 or a coreset of all experts route every token like token top-k."""
+    cfg = get_config("small_bf16")
+    d = {k: (None if v is None else v.cuda()) for k, v in make_inputs(cfg, seed=2).items()}
+    layer = _layer(cfg, 1.0 if min_c == "k" else 0.3, cfg.k if min_c == "k" else cfg.E)
+    run_and_check_topp(cfg, d, layer)
+    tok = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device="cuda")
+    tok.route(d["x"], d["w_router"], d.get("bias"), "token")
+    torch.cuda.synchronize()
+    assert torch.equal(tok.token_experts, layer.token_experts)
+
+
+def test_topp_direct_ties(gpu_lib):
+    """Block scores with exact ties: coresets and in-coreset selections follow
+    (score desc, id asc), on probabilities given directly."""
+    rng = np.random.default_rng(4)
+    E, k, bs, nb = 64, 4, 8, 3
+    pr = (rng.integers(1, 5, size=(nb * bs, E)).astype(np.float32) / 64)
+    probs = torch.from_numpy(pr).cuda()
+    T = nb * bs
+    out = dict(sn=torch.empty((nb, E), device="cuda"), core=torch.empty((nb, E), dtype=torch.int32, device="cuda"),
+               size=torch.empty((nb,), dtype=torch.int32, device="cuda"),
+               ex=torch.empty((T, k), dtype=torch.int32, device="cuda"), w=torch.empty((T, k), device="cuda"))
+    lib.dmoe_block_topp_route(probs, nb, bs, E, k, 0.5, k, out["sn"], out["core"], out["size"], out["ex"], out["w"],
+                              None)
+    torch.cuda.synchronize()
+    for b in range(nb):
+        S, C, R = O.alg1_route(pr[b * bs:(b + 1) * bs], k, 0.5)
+        assert np.array_equal(out["sn"][b].cpu().numpy(), O.normalize(S))
+        n = int(out["size"][b])
+        assert out["core"][b, :n].cpu().tolist() == C.tolist()
+        assert out["ex"][b * bs:(b + 1) * bs].cpu().numpy().tolist() == R.tolist()
