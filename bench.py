@@ -14,6 +14,14 @@ bandwidth and the expert-FFN roofline are reported beside it, with the CPU
 oracle timed on a bounded sample as ``cpu_baseline``.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config decode_b1]
+    python bench.py --sweep      # paper-shaped sweeps on the decode layer shape
+
+``--sweep`` replaces the headline run by three sweeps on the decode layer
+(hidden 2048, 256 experts of intermediate 512 + shared 512): block size 8, 16,
+24 and 32 for one sequence (Table 4's block sizes) under block, token and
+Top-P routing; top-4 instead of top-8 routing; and expert-FFN time against a
+forced number of unique experts (Fig. 2c's linear law), with the fitted
+per-expert slope.  It prints one JSON line of its own.
 """
 from __future__ import annotations
 
@@ -40,7 +48,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--config", default="decode_b1")
     ap.add_argument("--layers", type=int, default=0, help="distinct layers to rotate through (0: auto)")
-    ap.add_argument("--routing", choices=["both", "block", "token"], default="both")
+    ap.add_argument("--routing", choices=["all", "block", "token", "topp"], default="all",
+                    help="all: block, token and Alg. 1 Top-P routing (p = --top-p)")
+    ap.add_argument("--top-p", type=float, default=0.6)
+    ap.add_argument("--sweep", action="store_true", help="run the paper-shaped sweeps instead")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle timing per mode")
@@ -82,6 +93,9 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "copies": 8}))
         return 0
 
+    if args.sweep:
+        return sweep(args, torch)
+
     from dmoe_synth import get_config, make_inputs
     from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes
     from paper_2605_30876_amd import lib
@@ -116,12 +130,12 @@ def main():
             d0_host = {k: (None if v is None else v.to("cpu")) for k, v in d.items()}
         w = pack_weights(d)  # the layer keeps only the packed expert weights
         layers.append((d["x"], w, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
-                                           device=dev, out_dtype=dt)))
+                                           device=dev, out_dtype=dt, top_p=args.top_p)))
         del d
     torch.cuda.synchronize()
     log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
 
-    modes = ["block", "token"] if args.routing == "both" else [args.routing]
+    modes = ["block", "token", "topp"] if args.routing == "all" else [args.routing]
     results = {}
     for routing in modes:
         def step(l, routing=routing):
@@ -242,10 +256,133 @@ def main():
         "cpu_baseline": cpu,
         "block_routing": results.get("block"),
         "token_routing": results.get("token"),
+        "topp_routing": results.get("topp"),
     }
     if "block" in results and "token" in results:
         out["token_over_block_time"] = round(results["token"]["us_per_step"] / results["block"]["us_per_step"], 3)
     print(json.dumps(out))
+    return 0
+
+
+def graph_timer(torch, NL: int):
+    """Returns time(fn, steps): captures fn(0..NL-1) in one HIP graph, replays
+    it steps/NL times between two events and returns microseconds per fn call
+    (the events are on the stream the graph replays on)."""
+
+    def time_fn(fn, steps):
+        reps = max(1, -(-steps // NL))
+        stream = torch.cuda.Stream()
+        stream.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(stream):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                for l in range(NL):
+                    fn(l)
+        torch.cuda.current_stream().wait_stream(stream)
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(reps):
+            g.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        del g
+        return ev0.elapsed_time(ev1) * 1e3 / (reps * NL)
+
+    return time_fn
+
+
+def sweep(args, torch):
+    """Block size, top-k and unique-expert sweeps on the decode layer shape.
+
+    Weights of NL layers are generated and packed once and shared by every
+    point; each point has its own hidden states and MoELayer objects.  Every
+    timing replays a HIP graph over the NL layers, so the experts a launch
+    streams were last touched a rotation (>= 1.5 GiB of weights) earlier."""
+    import numpy as np
+
+    from dmoe_synth import get_config, make_inputs
+    from dmoe_synth.generate import expert_bytes, make_hidden_states, shared_bytes
+    from paper_2605_30876_amd import lib
+    from paper_2605_30876_amd.layer import MoELayer, pack_weights
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lib.load()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    base = get_config("decode_b1")
+    B_e, B_s = expert_bytes(base), shared_bytes(base)
+    NL = args.layers if args.layers > 0 else -(-int(1.5 * 2**30) // (base.k * B_e + B_s))
+    steps = max(NL, args.steps // 4)
+    log(f"[sweep] {NL} layers of the decode layer shape, {steps} steps per point")
+    weights = []
+    for l in range(NL):
+        d = make_inputs(base, seed=args.seed, layer=l, device=dev, hidden=False)
+        weights.append(pack_weights(d))
+        del d
+    torch.cuda.synchronize()
+    time_fn = graph_timer(torch, NL)
+    out = {"workload": "decode layer: hidden 2048, 256 routed experts of SwiGLU intermediate 512 + shared 512",
+           "layers_rotated": NL, "steps_per_point": steps}
+
+    def layer_point(cfg, routings):
+        """Whole-layer and expert-FFN time of each routing mode at one shape."""
+        xs = [make_hidden_states(cfg, seed=args.seed, layer=l, device=dev) for l in range(NL)]
+        ms = [MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device=dev, out_dtype=torch.bfloat16,
+                       top_p=args.top_p) for _ in range(NL)]
+        res = {}
+        for routing in routings:
+            for l in range(NL):
+                ms[l].forward(xs[l], weights[l], routing)
+            torch.cuda.synchronize()
+            U = statistics.mean(int(m.sched.n_unique[0]) for m in ms)
+            us = time_fn(lambda l: ms[l].forward(xs[l], weights[l], routing), steps)
+            ffn = time_fn(lambda l: ms[l].experts_ffn(weights[l], routing), steps)
+            res[routing] = {"us_per_step": round(us, 2), "us_per_token": round(us / cfg.T, 3),
+                            "unique_experts": round(U, 2), "expert_ffn_us": round(ffn, 2),
+                            "expert_ffn_gbps": round((U * B_e + B_s) / (ffn * 1e-6) / 1e9, 1)}
+            log(f"[sweep] bs={cfg.bs} k={cfg.k} {routing}: {us:.2f} us/step, U={U:.1f}, FFN {ffn:.2f} us")
+        return res
+
+    out["block_size"] = {str(bs): layer_point(base.with_(bs=bs), ("block", "token", "topp"))
+                         for bs in (8, 16, 24, 32)}
+    out["top4"] = layer_point(base.with_(k=4), ("block", "token", "topp"))
+
+    # Expert FFN against a forced unique-expert count U: 32 tokens x 8 slots,
+    # slot j of token t goes to expert (8 t + j) mod U (k distinct experts
+    # per token, all U experts used), then the token-level schedule.
+    cfg = base
+    xs = [make_hidden_states(cfg, seed=args.seed, layer=l, device=dev) for l in range(NL)]
+    ms = [MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device=dev, out_dtype=torch.bfloat16)
+          for _ in range(NL)]
+    for l in range(NL):  # the router writes the FFN's chunk-major activations
+        ms[l].route(xs[l], weights[l]["w_router"], None, "token")
+    pts = []
+    for U in (8, 16, 24, 32, 48, 64, 96, 128, 160, 192, 224, 256):
+        ids = (torch.arange(cfg.T * cfg.k, device=dev, dtype=torch.int32) % U).reshape(cfg.T, cfg.k)
+        for m in ms:
+            m.token_experts.copy_(ids)
+            lib.dmoe_build_expert_schedule(m.token_experts, cfg.T, 1, cfg.k, cfg.E, m.sched)
+        torch.cuda.synchronize()
+        assert all(int(m.sched.n_unique[0]) == U for m in ms)
+        ffn = time_fn(lambda l: ms[l].experts_ffn(weights[l], "token"), steps)
+        pts.append((U, ffn))
+        log(f"[sweep] U={U}: expert FFN {ffn:.2f} us = {(U * B_e + B_s) / (ffn * 1e-6) / 1e9:.0f} GB/s")
+    u = np.array([p[0] for p in pts], dtype=np.float64)
+    t = np.array([p[1] for p in pts], dtype=np.float64)
+    slope, icpt = np.polyfit(u, t, 1)
+    r2 = 1.0 - float(np.sum((t - (slope * u + icpt)) ** 2) / np.sum((t - t.mean()) ** 2))
+    out["ffn_vs_unique"] = {
+        "points": [{"unique": int(a), "expert_ffn_us": round(b, 2),
+                    "gbps": round((a * B_e + B_s) / (b * 1e-6) / 1e9, 1)} for a, b in pts],
+        "fit_us": {"intercept": round(float(icpt), 3), "per_expert": round(float(slope), 4), "r2": round(r2, 5)},
+        "marginal_gbps": round(B_e / (slope * 1e-6) / 1e9, 1),
+    }
+    log(f"[sweep] FFN = {icpt:.2f} us + {slope:.4f} us x U (r2 {r2:.4f}); marginal "
+        f"{B_e / (slope * 1e-6) / 1e9:.0f} GB/s")
+    print(json.dumps({"sweep": out}))
     return 0
 
 

@@ -17,6 +17,9 @@
         MFMA busy fraction and bf16 MFMA throughput per dispatch from a
         ``--pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16
         GRBM_GUI_ACTIVE`` run.
+
+    python -m paper_2605_30876_amd.prof_summary sweep --json OUT.json --cmd C
+        The JSON line of ``bench.py --sweep`` as markdown tables.
 """
 from __future__ import annotations
 
@@ -29,7 +32,8 @@ import sqlite3
 import statistics
 import sys
 
-FFN_KERNELS = ("ffn_gateup_bf16_kernel", "ffn_down_bf16_kernel", "ffn_gateup_f32_kernel", "ffn_down_f32_kernel")
+FFN_KERNELS = ("ffn_gateup_bf16_kernel", "ffn_down_bf16_kernel", "ffn_tile_bf16_kernel", "ffn_gateup_f32_kernel",
+               "ffn_down_f32_kernel")
 
 
 def short(name: str) -> str:
@@ -128,6 +132,35 @@ def cmd_mfma(a):
         print(f"| `{pat}` | {n} | {util:.1f} | {m:.0f} |")
 
 
+def cmd_sweep(a):
+    with open(a.json) as fh:
+        sw = json.loads(fh.read().strip().splitlines()[-1])["sweep"]
+    print(f"# Sweeps on the {sw['workload']}\n\nCommand (from the repository root on the GPU box):\n\n"
+          f"```\n{a.cmd}\n```\n")
+    print(f"Every time is a HIP-graph replay over {sw['layers_rotated']} layers with distinct weights "
+          f"(cache-cold expert streams), {sw['steps_per_point']} steps per point, bf16.\n")
+    modes = ("block", "token", "topp")
+    print("## Block size (one sequence, T = block size, top-8; Top-P routing with p = 0.6)\n")
+    print("| block size | " + " | ".join(f"{m} us/step | {m} U" for m in modes) + " | block FFN GB/s |")
+    print("|---" * (2 + 2 * len(modes)) + "|")
+    for bs, r in sw["block_size"].items():
+        cells = " | ".join(f"{r[m]['us_per_step']} | {r[m]['unique_experts']}" for m in modes)
+        print(f"| {bs} | {cells} | {r['block']['expert_ffn_gbps']} |")
+    print("\n## Top-4 routing (one block of 32 tokens)\n")
+    print("| routing | us/step | unique experts | expert FFN us | expert FFN GB/s |\n|---|---|---|---|---|")
+    for m in modes:
+        r = sw["top4"][m]
+        print(f"| {m} | {r['us_per_step']} | {r['unique_experts']} | {r['expert_ffn_us']} | {r['expert_ffn_gbps']} |")
+    f = sw["ffn_vs_unique"]
+    print("\n## Expert FFN time against the unique-expert count (32 tokens x 8 slots, forced experts)\n")
+    print("| unique experts | expert FFN us | GB/s |\n|---|---|---|")
+    for p in f["points"]:
+        print(f"| {p['unique']} | {p['expert_ffn_us']} | {p['gbps']} |")
+    fit = f["fit_us"]
+    print(f"\nLeast-squares line: t = {fit['intercept']} us + {fit['per_expert']} us x U (r^2 = {fit['r2']}); "
+          f"the slope streams one expert's 6 MiB at {f['marginal_gbps']} GB/s.")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="what", required=True)
@@ -151,6 +184,10 @@ def main(argv=None):
     m.add_argument("--kernel", nargs="+", required=True)
     m.add_argument("--simds", type=int, default=1024, help="SIMDs on the chip (256 CUs x 4)")
     m.set_defaults(fn=cmd_mfma)
+    w = sub.add_parser("sweep")
+    w.add_argument("--json", required=True)
+    w.add_argument("--cmd", required=True)
+    w.set_defaults(fn=cmd_sweep)
     a = ap.parse_args(argv)
     a.fn(a)
 
