@@ -299,6 +299,25 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// The float a key came from (-0 comes back as +0, which compares equal).
+__device__ __forceinline__ float key_value(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+__device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
+// Minimum over the 64 lanes (same DPP pattern as wave_max).
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  int x = static_cast<int>(v);
+  x = static_cast<int>(umin32(x, dpp<kDppXor1>(x, x)));
+  x = static_cast<int>(umin32(x, dpp<kDppXor2>(x, x)));
+  x = static_cast<int>(umin32(x, dpp<kDppHalfMirror>(x, x)));
+  x = static_cast<int>(umin32(x, dpp<kDppMirror>(x, x)));
+  x = static_cast<int>(umin32(x, dpp<kDppBcast15, 0xA>(x, x)));
+  x = static_cast<int>(umin32(x, dpp<kDppBcast31, 0xC>(x, x)));
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(x, 63));
+}
+
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
@@ -306,37 +325,75 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 
 // NJ values per lane (E <= 64*NJ): lane l holds e = 64*j + l.  RB rows are
 // searched together (their bit loops are independent chains); rows with
-// live[u] false are skipped.  See wave_topk_radix for the method.
-template <int NJ, int RB>
+// live[u] false are skipped (every row pointer must still be readable over
+// [0, E): all loads are issued unconditionally, then masked, so they are in
+// flight together).  With kMasked, only elements with inside[e] != 0 (LDS
+// flags) take part, and each row must hold at least `rounds` of them.  live
+// must be uniform over the wave.  See wave_topk_radix for the method.
+template <int NJ, int RB, bool kMasked = false>
 __device__ inline void wave_topk_radix_rows(const float* const (&row)[RB], const bool (&live)[RB], int E,
                                             int rounds, int* const (&sel)[RB], float* const (&selv)[RB],
-                                            float* buf_v, int* buf_i) {
+                                            float* buf_v, int* buf_i, const int* inside = nullptr) {
   const int lane = threadIdx.x & 63;
+  bool lv[RB];  // live, as a wave-uniform (scalar) value
+#pragma unroll
+  for (int u = 0; u < RB; ++u) lv[u] = __builtin_amdgcn_readfirstlane(live[u] ? 1 : 0) != 0;
+  float val[RB][NJ];
+  int flag[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int e = min(j * kWave + lane, E - 1);
+    flag[j] = kMasked ? inside[e] : 1;
+#pragma unroll
+    for (int u = 0; u < RB; ++u) val[u][j] = row[u][e];
+  }
   uint32_t key[RB][NJ];
 #pragma unroll
   for (int u = 0; u < RB; ++u)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const int e = j * kWave + lane;
-      key[u][j] = (live[u] && e < E) ? order_key(row[u][e]) : 0u;  // 0: below every real key
+      const bool in = lv[u] && j * kWave + lane < E && flag[j] != 0;
+      key[u][j] = in ? order_key(val[u][j]) : 0u;  // 0: below every real key
     }
+  // MSB-first search for the rounds-th largest key.  A row stops as soon as
+  // exactly `rounds` keys are >= its prefix: the answer is then the smallest
+  // of them (rows whose rounds-th and next keys are equal run all 32 bits).
   uint32_t prefix[RB];
+  bool exact[RB];
 #pragma unroll
-  for (int u = 0; u < RB; ++u) prefix[u] = 0;
+  for (int u = 0; u < RB; ++u) {
+    prefix[u] = 0;
+    exact[u] = !lv[u];
+  }
   for (int bit = 31; bit >= 0; --bit) {
+    bool all = true;
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
-      const uint32_t cand = prefix[u] | (1u << bit);
-      int cnt = 0;
+      if (!exact[u]) {
+        const uint32_t cand = prefix[u] | (1u << bit);
+        int cnt = 0;
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) cnt += __popcll(__ballot(key[u][j] >= cand));
-      prefix[u] = cnt >= rounds ? cand : prefix[u];
+        for (int j = 0; j < NJ; ++j) cnt += __popcll(__ballot(key[u][j] >= cand));
+        prefix[u] = cnt >= rounds ? cand : prefix[u];
+        exact[u] = cnt == rounds;
+      }
+      all = all && exact[u];
     }
+    if (all) break;
+  }
+#pragma unroll
+  for (int u = 0; u < RB; ++u) {
+    if (!lv[u] || !exact[u]) continue;
+    uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (key[u][j] >= prefix[u]) m = umin32(m, key[u][j]);
+    prefix[u] = wave_min_u32(m);
   }
   // prefix[u] is now row u's rounds-th largest key; gather and rank row by row
 #pragma unroll
   for (int u = 0; u < RB; ++u) {
-    if (!live[u]) continue;
+    if (!lv[u]) continue;
     int n_gt = 0;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) n_gt += __popcll(__ballot(key[u][j] > prefix[u]));
@@ -352,7 +409,7 @@ __device__ inline void wave_topk_radix_rows(const float* const (&row)[RB], const
       if (take) {
         const int pos = placed + lanes_below(t_mask);
         const int e = j * kWave + lane;
-        buf_v[pos] = row[u][e];
+        buf_v[pos] = key_value(key[u][j]);
         buf_i[pos] = e;
       }
       placed += __popcll(t_mask);

@@ -71,3 +71,44 @@ def test_topp_direct_ties(gpu_lib):
         n = int(out["size"][b])
         assert out["core"][b, :n].cpu().tolist() == C.tolist()
         assert out["ex"][b * bs:(b + 1) * bs].cpu().numpy().tolist() == R.tolist()
+
+
+@pytest.mark.parametrize("E,k,bs,nb,p", [(1024, 8, 64, 2, 0.6), (1000, 5, 33, 3, 0.8), (256, 8, 894, 1, 0.5)])
+def test_topp_direct_shapes(gpu_lib, E, k, bs, nb, p):
+    """Shapes whose masked sums take several LDS chunks (E = 1024, 1000) and
+    the largest block the kernel holds at E = 256, k = 8; router-like rows
+    (softmax of N(0, 2^2) logits) given directly."""
+    from parity import accepted_selection
+
+    print("case", E, k, bs, nb, p, flush=True)
+    rng = np.random.default_rng(5)
+    z = rng.standard_normal((nb * bs, E)).astype(np.float32) * 2
+    pr = O.softmax_rows(z)
+    T = nb * bs
+    dev = "cuda"
+    sn_g = torch.empty((nb, E), device=dev)
+    core = torch.empty((nb, E), dtype=torch.int32, device=dev)
+    size = torch.empty((nb,), dtype=torch.int32, device=dev)
+    ex = torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = torch.empty((T, k), device=dev)
+    lib.dmoe_block_topp_route(torch.from_numpy(pr).to(dev), nb, bs, E, k, p, k, sn_g, core, size, ex, w, None)
+    torch.cuda.synchronize()
+    ex_h, w_h = ex.cpu().numpy(), w.cpu().numpy()
+    log = []
+    for b in range(nb):
+        blk = pr[b * bs:(b + 1) * bs]
+        S, C, _ = O.alg1_route(blk, k, p)
+        sn = O.normalize(S)
+        assert float(np.max(np.abs(sn_g[b].cpu().numpy() - sn))) <= 1e-6
+        got = core[b, :int(size[b])].cpu().tolist()
+        if got != C.tolist():
+            assert frozenset(got) in O.alg1_valid_coresets(sn, p, k)
+        inside = np.zeros(E, dtype=bool)
+        inside[got] = True
+        masked = np.where(inside[None, :], blk, np.float32(-np.inf)).astype(np.float32)
+        acc = accepted_selection(masked, ex_h[b * bs:(b + 1) * bs], k, log, f"block {b}")
+        for t in range(bs):
+            ref = O.renormalised_weights(blk[t], acc[t])
+            gw = dict(zip(ex_h[b * bs + t].tolist(), w_h[b * bs + t].tolist()))
+            assert max(abs(gw[e] - r) for e, r in zip(acc[t].tolist(), ref.tolist())) <= 1e-6
+    print("   near-ties", len(log), "coreset sizes", size.cpu().tolist(), flush=True)
