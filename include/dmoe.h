@@ -198,10 +198,7 @@ dmoe_status dmoe_token_topk(const float* probs, int T, int E, int k, int32_t* to
  * combine_w [T][k]; gap [T] or NULL (k-th minus (k+1)-th probability inside
  * C_b; +inf if |C_b| == k).  Schedule token_experts with group_size = 1.
  * Limits: 1 <= k <= min(E, 64); k <= min_coreset <= E; 0 < p <= 1;
- * 1 <= block_size <= 4096.  Kernel limits (else DMOE_ERR_UNSUPPORTED): E <= 1024
- * and 5*E' + 4*ceil(block_size*k/2) + 80*(k+1) <= 16316 with E' = E rounded up to a
- * multiple of 4 (one workgroup's 64 KiB of LDS; E = 256, k = 8 allows
- * block_size <= 894).
+ * 1 <= block_size <= 4096.  Kernel limit (else DMOE_ERR_UNSUPPORTED): E <= 1024.
  */
 dmoe_status dmoe_block_topp_route(const float* probs, int n_blocks, int block_size, int E, int k, float p,
                                   int min_coreset, float* block_scores, int32_t* coreset, int32_t* coreset_size,

@@ -147,8 +147,8 @@ dmoe_status dmoe_block_topp_route(const float* probs, int n_blocks, int block_si
   ALIGNED(combine_w);
   ALIGNED(gap);
   SUPPORT(E <= 1024, "the Top-P coreset supports E <= 1024 (E=%d)", E);
-  SUPPORT(dmoe::topp_lds_bytes(block_size, E, k) != 0,
-          "the Top-P kernel's LDS does not hold block_size=%d, E=%d, k=%d", block_size, E, k);
+  SUPPORT(dmoe::topp_supported(block_size, E, k), "the Top-P kernels do not support block_size=%d, E=%d, k=%d",
+          block_size, E, k);
   return hip_status(dmoe::launch_block_topp(probs, n_blocks, block_size, E, k, p, min_coreset, block_scores,
                                             coreset, coreset_size, token_experts, combine_w, gap,
                                             static_cast<hipStream_t>(stream)),

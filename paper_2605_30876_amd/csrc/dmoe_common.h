@@ -75,7 +75,7 @@ hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, 
 hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, float p, int min_c,
                              float* block_scores, int32_t* coreset, int32_t* coreset_size, int32_t* experts,
                              float* w, float* gap, hipStream_t s);
-size_t topp_lds_bytes(int bs, int E, int k);
+bool topp_supported(int bs, int E, int k);
 
 // The whole routing stage: router, selection (blocks of gs tokens when block,
 // else per token), combine weights and schedule.  Small forwards run the

@@ -266,8 +266,6 @@ def test_topp_validation(L, buf):
     assert call(bs=0) == INV
     assert call(ex=p + 4) == INV
     assert call(E=2048, mc=8) == UNS
-    assert call(bs=4096, k=8) == UNS
-    assert call(bs=895, k=8) == UNS    # 5*256 + 4*3580 + 80*9 = 16320 words of LDS > 16316
 
 
 def test_router_workspace_size():

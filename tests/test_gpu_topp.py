@@ -75,9 +75,9 @@ def test_topp_direct_ties(gpu_lib):
 
 @pytest.mark.parametrize("E,k,bs,nb,p", [(1024, 8, 64, 2, 0.6), (1000, 5, 33, 3, 0.8), (256, 8, 894, 1, 0.5)])
 def test_topp_direct_shapes(gpu_lib, E, k, bs, nb, p):
-    """Shapes whose masked sums take several LDS chunks (E = 1024, 1000) and
-    the largest block the kernel holds at E = 256, k = 8; router-like rows
-    (softmax of N(0, 2^2) logits) given directly."""
+    """Shapes whose masked sums take several LDS chunks (E = 1024 and 1000,
+    and a block of 894 tokens at E = 256); router-like rows (softmax of
+    N(0, 2^2) logits) given directly."""
     from parity import accepted_selection
 
     print("case", E, k, bs, nb, p, flush=True)
