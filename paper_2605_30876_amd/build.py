@@ -31,7 +31,7 @@ def ffn_source_hash() -> str:
     import hashlib
 
     h = hashlib.sha256()
-    for f in ("ffn.hip", "pack.hip", "dmoe_common.h"):
+    for f in ("ffn.hip", "pack.hip"):
         with open(os.path.join(CSRC, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
