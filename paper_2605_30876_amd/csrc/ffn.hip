@@ -4,10 +4,13 @@
 //   h    = silu(Wg x) * (Wu x)        gate/up kernel -> h rows (workspace)
 //   out  = Wd h                       down kernel    -> slot_out[t][j] / shared_out[t]
 //
-// Work items: grid row y < max_work is the schedule's y-th work item (up to
-// DMOE_WORK_ROWS rows of one routed expert; rows past n_work exit at once);
-// the rows after those cut the shared expert's T tokens into pieces of
-// DMOE_WORK_ROWS.  A workgroup owns one 16-row weight tile of one item,
+// Work items: max_work grid rows for the schedule's work items (up to
+// DMOE_WORK_ROWS rows of one routed expert; rows past n_work exit at once)
+// and rows for the shared expert's T tokens cut into pieces of
+// DMOE_WORK_ROWS.  One-tile launches (schedules of many small items, whose
+// max_work bound is loose) put the shared pieces first so that the rows that
+// exit at once are dispatched last; the others put them last (measured
+// faster for block-routed decode steps).  A workgroup owns one 16-row weight tile of one item,
 // streams it from HBM and applies it to the item's rows (tokens): each
 // selected expert's weights are read once per forward per piece of its rows.
 //
@@ -50,21 +53,24 @@ struct Group {
   int t0;
 };
 
-// One memory round trip: the item count and the item are loaded together
-// (y < max_work keeps the index inside the work array; an item past n_work
-// is loaded but not used).
-__device__ __forceinline__ bool decode_item(int y, int max_work, const int* n_work, const int* work,
-                                            const int* row_token, int T, int Tk, Group& g) {
-  if (y < max_work) {
+// Grid row y: the schedule's max_work items, then the shared expert's pieces
+// (kSharedFirst: the pieces first).  One memory round trip: the item count
+// and the item are loaded together (the index stays inside the work array;
+// an item past n_work is loaded but not used).
+template <bool kSharedFirst = false>
+__device__ __forceinline__ bool decode_item(int y, int shared_items, int max_work, const int* n_work,
+                                            const int* work, const int* row_token, int T, int Tk, Group& g) {
+  const int w = kSharedFirst ? y - shared_items : y;
+  if (kSharedFirst ? w >= 0 : w < max_work) {
     const int nw = *n_work;
-    const int4 it = reinterpret_cast<const int4*>(work)[y];
+    const int4 it = reinterpret_cast<const int4*>(work)[w];
     g.expert = it.x;
     g.r0 = it.y;
-    g.n = y < nw ? it.z : 0;
+    g.n = w < nw ? it.z : 0;
     g.tok = row_token + it.y;
     g.t0 = 0;
   } else {
-    const int c = y - max_work;
+    const int c = kSharedFirst ? y : y - max_work;
     g.expert = -1;
     g.t0 = c * DMOE_WORK_ROWS;
     g.r0 = Tk + g.t0;
@@ -87,6 +93,7 @@ struct FfnParams {
   const int* row_token;
   const int* row_slot;
   int T, H, I, I_s, k, Tk, R, max_work;  // R: rows of the h buffer
+  int shared_items;                        // grid rows of the shared expert's pieces (0: none)
   bf16_t* hk;                              // SwiGLU activations, chunk-major [ldh/8][R][8]
   float* slot_out;
   float* shared_out;
@@ -184,15 +191,17 @@ __device__ __forceinline__ void zero(f32x4 (&acc)[NT]) {
 }
 
 // Occupancy floors (waves per SIMD) for the two-tile variants, which serve
-// block-routed decode steps: 3 (gate/up) and 4 (down) keep every workgroup of
-// such a launch resident at once instead of leaving a second partial round.
+// block-routed decode steps: 3 (gate/up) and 5 (down, with 4-step weight
+// bursts) keep every workgroup of such a launch resident at once instead of
+// leaving a second partial round.
 // grid (ldh / 8, groups): packed gate/up tile `it` = 8 intermediate units.
 // Wave w reduces over hidden chunks [w*H/32, (w+1)*H/32) (K-steps
 // [w*H/128, (w+1)*H/128)).
-template <int NT, int KMAX, int BC, int MINW>
+template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
-  if (!decode_item(blockIdx.y, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g))
+  if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
+                                 p.Tk, g))
     return;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int it = blockIdx.x;
@@ -238,10 +247,11 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
 }
 
 // grid (H / 16, groups): packed down tile `jt` = 16 output features.
-template <int NT, int KMAX, int BC, int MINW>
+template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
-  if (!decode_item(blockIdx.y, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g))
+  if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
+                                 p.Tk, g))
     return;
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
@@ -304,7 +314,7 @@ static_assert(kTileTok * 16 == DMOE_WORK_ROWS, "a tile workgroup covers one work
 template <bool kGateUp>
 __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p) {
   Group g;
-  if (!decode_item(blockIdx.y, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g)) return;
+  if (!decode_item(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g)) return;
   const int H = p.H;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int Kd = kGateUp ? H : Iw;                    // reduction length
@@ -425,7 +435,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
     const int* __restrict__ n_work, const int* __restrict__ work, const int* __restrict__ row_token, int T, int H,
     int I, int I_s, int Tk, int max_work, int ldh, float* __restrict__ hbuf) {
   Group g;
-  if (!decode_item(blockIdx.y, max_work, n_work, work, row_token, T, Tk, g)) return;
+  if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, g)) return;
   const int Iw = g.expert >= 0 ? I : I_s;
   const int i = blockIdx.x * kThreads + threadIdx.x;
   if (i >= Iw) return;
@@ -451,7 +461,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
     int H, int I, int I_s, int k, int Tk, int max_work, int ldh, const float* __restrict__ hbuf,
     float* __restrict__ slot_out, float* __restrict__ shared_out) {
   Group g;
-  if (!decode_item(blockIdx.y, max_work, n_work, work, row_token, T, Tk, g)) return;
+  if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, g)) return;
   const int Kd = g.expert >= 0 ? I : I_s;
   const int j = blockIdx.x * kThreads + threadIdx.x;
   if (j >= H) return;
@@ -480,7 +490,8 @@ int pick_ntiles(int T, int k, int max_work) {
 }
 
 // Launch shapes per token-tile count NT: weight burst KMAX steps, token
-// chunks of BC steps, occupancy floor MINW (waves per SIMD).  The two-tile
+// chunks of BC steps, occupancy floor MINW (waves per SIMD), and the order of
+// the grid rows (kSharedFirst, see the top of the file).  The two-tile
 // variants serve block-routed decode steps, whose launches are small enough
 // that a higher floor keeps every workgroup resident at once.
 template <int NT>
@@ -488,23 +499,28 @@ struct Shape;
 template <>
 struct Shape<1> {
   static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 1, kDnMax = 8, kDnChunk = 4, kDnWaves = 1;
+  static constexpr bool kSharedFirst = true;
 };
 template <>
 struct Shape<2> {
-  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 3, kDnMax = 8, kDnChunk = 4, kDnWaves = 4;
+  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 3, kDnMax = 4, kDnChunk = 4, kDnWaves = 5;
+  static constexpr bool kSharedFirst = false;
 };
 template <>
 struct Shape<4> {
   static constexpr int kGuMax = 8, kGuChunk = 4, kGuWaves = 1, kDnMax = 8, kDnChunk = 4, kDnWaves = 1;
+  static constexpr bool kSharedFirst = false;
 };
 
 template <int NT>
 hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   using S = Shape<NT>;
-  ffn_gateup_bf16_kernel<NT, S::kGuMax, S::kGuChunk, S::kGuWaves><<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
+  ffn_gateup_bf16_kernel<NT, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst>
+      <<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_down_bf16_kernel<NT, S::kDnMax, S::kDnChunk, S::kDnWaves><<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
+  ffn_down_bf16_kernel<NT, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst>
+      <<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -531,7 +547,7 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
     FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w13),
                 static_cast<const bf16_t*>(a.w2), static_cast<const bf16_t*>(a.ws13),
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
-                a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work,
+                a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
     if (use_tile_kernels(a.T, a.k, a.max_work, ldh)) {
       ffn_tile_bf16_kernel<true><<<dim3(ldh / 32, items), kThreads, 0, s>>>(p);
