@@ -20,6 +20,8 @@
  *                              expert count of Sec. 3 is its n_unique)
  *   dmoe_expert_ffn            SwiGLU FFN of every unique expert over its
  *                              rows, plus the always-on shared expert
+ *   dmoe_shared_expert_ffn     the shared expert alone (to overlap it with
+ *                              the routing of the same forward)
  *   dmoe_combine               y_t = sum_j w[t,j] * FFN_{e_tj}(x_t) + FFN_s(x_t)
  *
  * dmoe_route_block / dmoe_route_token run the first three (or the token
@@ -313,6 +315,27 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
                             const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
                             int max_work, dmoe_schedule sched, float* slot_out, float* shared_out,
                             void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn): for every
+ * token t,
+ *   shared_out[t][:] = Ws_down (silu(Ws_gate x_t) * (Ws_up x_t))
+ * It needs no routing, so a caller can run it on a second stream while the
+ * routing of the same forward runs, then call dmoe_expert_ffn with the
+ * shared expert left out (ws13 = ws2 = shared_out = NULL, I_s = 0); the
+ * results are those of one dmoe_expert_ffn call with the shared expert.
+ * x_chunked [T][H] chunk-major (see above); ws13, ws2: the shared expert
+ * packed by dmoe_pack_expert_weights (n_experts = 1, I = I_s); shared_out
+ * [T][H] float32.  workspace: device scratch of at least
+ * dmoe_shared_ffn_workspace_size(T, I_s, dt) bytes (contents on entry do
+ * not matter), not shared with a concurrent call.
+ * Limits: T, H, I_s >= 1; H % c == 0; DMOE_BF16: H % 128 == 0 and
+ * I_s % 128 == 0.
+ */
+size_t dmoe_shared_ffn_workspace_size(int T, int I_s, dmoe_dtype dt);
+dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, const void* ws2, dmoe_dtype dt, int T,
+                                   int H, int I_s, float* shared_out, void* workspace, size_t ws_bytes,
+                                   void* stream);
 
 /*
  * Weighted combine:

@@ -370,6 +370,38 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }
 
+size_t dmoe_shared_ffn_workspace_size(int T, int I_s, dmoe_dtype dt) {
+  if (T < 1 || I_s < 1 || !valid_dtype(dt)) return 0;
+  return dmoe::ffn_workspace_bytes(T, 0, I_s, 0, dt);
+}
+
+dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, const void* ws2, dmoe_dtype dt, int T,
+                                   int H, int I_s, float* shared_out, void* workspace, size_t ws_bytes,
+                                   void* stream) {
+  REQUIRE(x_chunked && ws13 && ws2 && shared_out && workspace,
+          "x_chunked, ws13, ws2, shared_out and workspace must not be NULL");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1 && I_s >= 1, "T=%d, H=%d and I_s=%d must be >= 1", T, H, I_s);
+  REQUIRE(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
+  REQUIRE(static_cast<long>(T) * I_s <= kIntLimit && static_cast<long>(T) * H <= kIntLimit,
+          "T*H or the SwiGLU buffer is too large");
+  const size_t need = dmoe::ffn_workspace_bytes(T, 0, I_s, 0, dt);
+  REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
+  ALIGNED(x_chunked);
+  ALIGNED(ws13);
+  ALIGNED(ws2);
+  ALIGNED(shared_out);
+  ALIGNED(workspace);
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0 && I_s % 128 == 0,
+            "bf16 experts need H and I_s to be multiples of 128 (H=%d, I_s=%d)", H, I_s);
+  }
+  const dmoe_schedule none{};
+  dmoe::FfnArgs a{x_chunked, nullptr, nullptr, ws13, ws2, T, H, 1, 0, I_s, 0, 0, none, nullptr, shared_out,
+                  workspace};
+  return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
+}
+
 dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const float* shared_out,
                          dmoe_dtype dt, int T, int H, int k, void* y, void* stream) {
   REQUIRE(slot_out && combine_w && y, "slot_out, combine_w and y must not be NULL");

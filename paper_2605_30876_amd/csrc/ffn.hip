@@ -484,8 +484,15 @@ __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
 // Token columns per pass: enough 16-wide tiles for the expected rows of a
 // work item (the rows of the forward spread over max_work items, at most
 // DMOE_WORK_ROWS), at most 4.
+// rows per item of the launch: the routed rows spread over max_work items, or
+// (max_work == 0, the shared expert alone) its pieces of up to DMOE_WORK_ROWS.
+long rows_per_item(int T, int k, int max_work) {
+  if (max_work == 0) return std::min<long>(DMOE_WORK_ROWS, T);
+  return std::min<long>(DMOE_WORK_ROWS, (static_cast<long>(T) * k + max_work - 1) / max_work);
+}
+
 int pick_ntiles(int T, int k, int max_work) {
-  const long rows = std::min<long>(DMOE_WORK_ROWS, (static_cast<long>(T) * k + max_work - 1) / max_work);
+  const long rows = rows_per_item(T, k, max_work);
   return rows <= 16 ? 1 : (rows <= 32 ? 2 : 4);
 }
 
@@ -524,9 +531,8 @@ hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   return hipGetLastError();
 }
 
-bool use_tile_kernels(int T, int k, int max_work, int ldh) {
-  const long rows = (static_cast<long>(T) * k + max_work - 1) / max_work;
-  return rows >= 32 && static_cast<long>(ldh / 32) * max_work >= 512;
+bool use_tile_kernels(int T, int k, int max_work, int items, int ldh) {
+  return rows_per_item(T, k, max_work) >= 32 && static_cast<long>(ldh / 32) * items >= 512;
 }
 
 }  // namespace
@@ -549,7 +555,7 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
                 a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
-    if (use_tile_kernels(a.T, a.k, a.max_work, ldh)) {
+    if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
       ffn_tile_bf16_kernel<true><<<dim3(ldh / 32, items), kThreads, 0, s>>>(p);
       hipError_t err = hipGetLastError();
       if (err != hipSuccess) return err;

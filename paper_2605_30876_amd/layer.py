@@ -45,11 +45,18 @@ def pack_weights(w: dict, keep_unpacked: bool = False) -> dict:
 class MoELayer:
     def __init__(self, H: int, E: int, I: int, I_s: int, k: int, n_blocks: int, block_size: int,
                  dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False,
-                 out_dtype: torch.dtype = torch.float32, top_p: float = 0.6, min_coreset: int | None = None):
+                 out_dtype: torch.dtype = torch.float32, top_p: float = 0.6, min_coreset: int | None = None,
+                 overlap_shared: bool = False):
         """Routing modes: "block" (block top-k), "token" (token top-k, the
         baseline) and "topp" (Alg. 1: a Top-P coreset per block with mass
         ``top_p`` and at least ``min_coreset`` (default k) experts, each token's
-        top-k inside it)."""
+        top-k inside it).
+
+        overlap_shared: run the shared expert (dmoe_shared_expert_ffn) on a
+        second stream, concurrently with the routing and the routed experts;
+        the results are bitwise those of the single dmoe_expert_ffn call.  Off
+        by default: replayed from a HIP graph, the two-stream forward of a
+        32-token decode step is slower (53 vs 40 us) than the one-stream one."""
         self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
         self.NB, self.bs = n_blocks, block_size
         self.T = T = n_blocks * block_size
@@ -80,8 +87,14 @@ class MoELayer:
         dt = lib.DMOE_F32 if dtype == torch.float32 else lib.DMOE_BF16
         rbytes = lib.dmoe_router_workspace_size(T, H, E, dt)
         self.router_ws = torch.empty((rbytes,), dtype=torch.uint8, device=device) if rbytes else None
-        nbytes = lib.dmoe_ffn_workspace_size(T, I, I_s, k, dt)
+        self.overlap_shared = overlap_shared and I_s > 0
+        nbytes = lib.dmoe_ffn_workspace_size(T, I, 0 if self.overlap_shared else I_s, k, dt)
         self.workspace = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=device)
+        if self.overlap_shared:
+            self.x_chunked_s = torch.empty((T * H,), dtype=dtype, device=device)
+            sbytes = lib.dmoe_shared_ffn_workspace_size(T, I_s, dt)
+            self.workspace_s = torch.empty((sbytes,), dtype=torch.uint8, device=device)
+            self._side = torch.cuda.Stream(device=device)
         # The layer output is accumulated in fp32; it is stored as out_dtype.
         self.y = torch.empty((T, H), dtype=out_dtype, device=device)
 
@@ -122,11 +135,29 @@ class MoELayer:
                                 stream)
         lib.dmoe_build_expert_schedule(self.token_experts, T, 1, k, E, self.sched, stream)
 
+    def _routed_ffn(self, w: dict, routing: str, stream):
+        shared = not self.overlap_shared and self.I_s > 0
+        lib.dmoe_expert_ffn(self.x_chunked, w["w13"], w["w2"], w.get("ws13") if shared else None,
+                            w.get("ws2") if shared else None, self.T, self.H, self.E, self.I,
+                            self.I_s if shared else 0, self.k, self.max_work(routing), self.sched, self.slot_out,
+                            self.shared_out if shared else None, self.workspace, stream)
+
+    def _shared_ffn(self, xk, w: dict):
+        """The shared expert on the side stream (queued after what the side
+        stream already holds)."""
+        lib.dmoe_shared_expert_ffn(xk, w["ws13"], w["ws2"], self.T, self.H, self.I_s, self.shared_out,
+                                   self.workspace_s, self._side)
+
     def experts_ffn(self, w: dict, routing: str = "block", stream=None):
-        """Expert FFN on the chunk-major copy of x that :meth:`route` stored."""
-        lib.dmoe_expert_ffn(self.x_chunked, w["w13"], w["w2"], w.get("ws13"), w.get("ws2"), self.T, self.H,
-                            self.E, self.I, self.I_s, self.k, self.max_work(routing), self.sched,
-                            self.slot_out, self.shared_out, self.workspace, stream)
+        """Expert FFN (routed experts and the shared expert) on the chunk-major
+        copy of x that :meth:`route` stored."""
+        main = stream if stream is not None else torch.cuda.current_stream()
+        if self.overlap_shared:
+            self._side.wait_stream(main)  # x_chunked and the previous call's readers
+            self._shared_ffn(self.x_chunked, w)
+        self._routed_ffn(w, routing, main)
+        if self.overlap_shared:
+            main.wait_stream(self._side)
 
     def combine(self, stream=None):
         lib.dmoe_combine(self.slot_out, self.combine_w, self.shared_out, self.T, self.H, self.k, self.y,
@@ -135,9 +166,18 @@ class MoELayer:
     def forward(self, x, w: dict, routing: str = "block", stream=None, fused_routing: bool = True) -> torch.Tensor:
         """Whole layer on hidden states x[T, H] with weights from
         :func:`pack_weights`; returns (a view of) y[T, H]."""
-        self.route(x, w["w_router"], w.get("bias"), routing, stream, fused=fused_routing)
-        self.experts_ffn(w, routing, stream)
-        self.combine(stream)
+        main = stream if stream is not None else torch.cuda.current_stream()
+        if self.overlap_shared:
+            # the shared expert needs no routing: pack x for it and run it
+            # on the side stream while the routing runs
+            self._side.wait_stream(main)
+            lib.dmoe_pack_activations(x, self.T, self.H, self.x_chunked_s, self._side)
+            self._shared_ffn(self.x_chunked_s, w)
+        self.route(x, w["w_router"], w.get("bias"), routing, main, fused=fused_routing)
+        self._routed_ffn(w, routing, main)
+        if self.overlap_shared:
+            main.wait_stream(self._side)
+        self.combine(main)
         return self.y
 
     def experts(self, routing: str) -> torch.Tensor:

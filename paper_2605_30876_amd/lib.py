@@ -29,8 +29,10 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 
 # Every symbol include/dmoe.h declares.
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
-           "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work", "dmoe_route_block", "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights",
-           "dmoe_ffn_workspace_size", "dmoe_expert_ffn", "dmoe_combine", "dmoe_last_error", "dmoe_version")
+           "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work", "dmoe_route_block",
+           "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
+           "dmoe_expert_ffn", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
+           "dmoe_last_error", "dmoe_version")
 
 
 class DmoeError(RuntimeError):
@@ -66,6 +68,8 @@ _SIGS = {
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
     "dmoe_expert_ffn": ([_P] * 5 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
+    "dmoe_shared_ffn_workspace_size": ([_I, _I, _I], _S),
+    "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
     "dmoe_last_error": ([], ctypes.c_char_p),
     "dmoe_version": ([], ctypes.c_char_p),
@@ -217,6 +221,16 @@ def dmoe_pack_expert_weights(w_gate, w_up, w_down, n_experts, H, I, w13, w2, str
 
 def dmoe_ffn_workspace_size(T, I, I_s, k, dt) -> int:
     return int(load().dmoe_ffn_workspace_size(T, I, I_s, k, dt))
+
+
+def dmoe_shared_ffn_workspace_size(T, I_s, dt) -> int:
+    return int(load().dmoe_shared_ffn_workspace_size(T, I_s, dt))
+
+
+def dmoe_shared_expert_ffn(x_chunked, ws13, ws2, T, H, I_s, shared_out, workspace, stream=None):
+    _check(load().dmoe_shared_expert_ffn(ptr(x_chunked), ptr(ws13), ptr(ws2), dtype_code(x_chunked), T, H, I_s,
+                                         ptr(shared_out), ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), stream_handle(stream)))
 
 
 def dmoe_expert_ffn(x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work, sched: Schedule,

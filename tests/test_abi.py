@@ -268,6 +268,32 @@ def test_topp_validation(L, buf):
     assert call(E=2048, mc=8) == UNS
 
 
+def test_shared_ffn_validation(L, buf):
+    _, p = buf
+    f, INV, UNS = "dmoe_shared_expert_ffn", lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    big = 1 << 30
+
+    def call(**o):
+        a = dict(x=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, I_s=512, out=p, ws=p, nbytes=big)
+        a.update(o)
+        return status(L, f, a["x"], a["ws13"], a["ws2"], a["dt"], a["T"], a["H"], a["I_s"], a["out"], a["ws"],
+                      ctypes.c_size_t(a["nbytes"]), None)[0]
+    assert call(x=None) == INV
+    assert call(ws13=None) == INV
+    assert call(out=None) == INV
+    assert call(ws=None) == INV
+    assert call(T=0) == INV
+    assert call(I_s=0) == INV
+    assert call(dt=7) == INV
+    assert call(H=2044) == INV            # not a multiple of the 8-element chunk
+    assert call(H=2056) == UNS            # bf16 tiles need H % 128 == 0
+    assert call(nbytes=32 * 512 * 2 - 1) == INV
+    assert call(I_s=320) == UNS
+    assert lib.dmoe_shared_ffn_workspace_size(32, 512, lib.DMOE_BF16) == 32 * 512 * 2
+    assert lib.dmoe_shared_ffn_workspace_size(8, 24, lib.DMOE_F32) == 8 * 24 * 4
+    assert lib.dmoe_shared_ffn_workspace_size(0, 24, lib.DMOE_F32) == 0
+
+
 def test_router_workspace_size():
     # decode step: the hidden dimension is split, one fp32 partial plane per slice
     n = lib.dmoe_router_workspace_size(32, 2048, 256, lib.DMOE_BF16)
