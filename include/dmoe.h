@@ -270,7 +270,8 @@ dmoe_status dmoe_pack_activations(const void* x, dmoe_dtype dt, int T, int H, vo
  *     being w_down row 16*jt + r, columns 32*ks .. 32*ks+31.  A tile is stored
  *     as 64 pieces of 8 elements; piece p = 16*g + r holds row r, columns
  *     8g .. 8g+7 of the tile.
- *   DMOE_F32: w13[e] = w_gate[e] followed by w_up[e]; w2 = w_down.
+ *   DMOE_F32: reduction-major.  w13[e][h][u] (u < 2*I) is w_gate[e][u][h]
+ *     for u < I and w_up[e][u-I][h] otherwise; w2[e][i][j] = w_down[e][j][i].
  * The shared expert is packed by a second call with n_experts = 1, I = I_s.
  * Limits: n_experts, H, I >= 1; DMOE_BF16: H % 128 == 0 and I % 128 == 0.
  */

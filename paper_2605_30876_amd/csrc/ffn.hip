@@ -429,7 +429,17 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
 }
 
 // ---- f32 path -------------------------------------------------------------
+//
+// Weights are reduction-major (w13[e][h][u], w2[e][i][j]), so the 64 lanes of
+// a wave, one output unit each, read 256 contiguous bytes per reduction
+// index.  The four waves of a workgroup split the reduction in quarters and
+// keep kF32Tok tokens' partial sums in registers; the token values are the
+// same for every lane (scalar loads).  Partial sums are added in wave order
+// through LDS.
 
+constexpr int kF32Tok = 8;  // tokens per pass
+
+// grid (ceil(max(I, I_s) / 64), groups): units 64*bx + lane of item g.
 __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
     const float* __restrict__ xk, const float* __restrict__ w13, const float* __restrict__ ws13,
     const int* __restrict__ n_work, const int* __restrict__ work, const int* __restrict__ row_token, int T, int H,
@@ -437,24 +447,68 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
   Group g;
   if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, g)) return;
   const int Iw = g.expert >= 0 ? I : I_s;
-  const int i = blockIdx.x * kThreads + threadIdx.x;
-  if (i >= Iw) return;
-  // stacked weights: [2][Iw][H], gate then up
+  if (static_cast<int>(blockIdx.x) * kWave >= Iw) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int u = blockIdx.x * kWave + lane;
+  const bool live = u < Iw;
+  const int uc = live ? u : Iw - 1;
   const float* W = g.expert >= 0 ? w13 + static_cast<size_t>(g.expert) * 2 * I * H : ws13;
-  const float* wgr = W + static_cast<size_t>(i) * H;
-  const float* wur = W + (static_cast<size_t>(Iw) + i) * H;
-  for (int col = 0; col < g.n; ++col) {
-    const int tok = g.tok ? g.tok[col] : g.t0 + col;
-    float a = 0.f, b = 0.f;
-    for (int h = 0; h < H; ++h) {
-      const float xv = xk[(static_cast<size_t>(h >> 2) * T + tok) * 4 + (h & 3)];
-      a = fmaf(xv, wgr[h], a);
-      b = fmaf(xv, wur[h], b);
+  const size_t ldw = 2 * static_cast<size_t>(Iw);
+  const int nch = H >> 2, per = (nch + 3) >> 2;  // 4-feature chunks, a quarter per wave
+  const int c0 = wave * per, c1 = min(nch, c0 + per);
+  __shared__ float red[3][2][kF32Tok][kWave];
+  for (int p0 = 0; p0 < g.n; p0 += kF32Tok) {
+    float ag[kF32Tok], au[kF32Tok];
+    int tok[kF32Tok];
+#pragma unroll
+    for (int t = 0; t < kF32Tok; ++t) {
+      ag[t] = au[t] = 0.f;
+      const int col = min(p0 + t, g.n - 1);
+      tok[t] = g.tok ? g.tok[col] : g.t0 + col;
     }
-    hbuf[static_cast<size_t>(g.r0 + col) * ldh + i] = silu_f32(a) * b;
+#pragma unroll 4
+    for (int c = c0; c < c1; ++c) {
+      float wg[4], wu[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float* wr = W + static_cast<size_t>(4 * c + q) * ldw;
+        wg[q] = wr[uc];
+        wu[q] = wr[Iw + uc];
+      }
+#pragma unroll
+      for (int t = 0; t < kF32Tok; ++t) {
+        const f32x4 xv = *reinterpret_cast<const f32x4*>(xk + (static_cast<size_t>(c) * T + tok[t]) * 4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          ag[t] = fmaf(xv[q], wg[q], ag[t]);
+          au[t] = fmaf(xv[q], wu[q], au[t]);
+        }
+      }
+    }
+    if (wave > 0) {
+#pragma unroll
+      for (int t = 0; t < kF32Tok; ++t) {
+        red[wave - 1][0][t][lane] = ag[t];
+        red[wave - 1][1][t][lane] = au[t];
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int t = 0; t < kF32Tok; ++t) {
+#pragma unroll
+        for (int ww = 0; ww < 3; ++ww) {
+          ag[t] += red[ww][0][t][lane];
+          au[t] += red[ww][1][t][lane];
+        }
+        if (live && p0 + t < g.n) hbuf[static_cast<size_t>(g.r0 + p0 + t) * ldh + u] = silu_f32(ag[t]) * au[t];
+      }
+    }
+    __syncthreads();  // red is reused by the next pass
   }
 }
 
+// grid (ceil(H / 64), groups): output features 64*bx + lane of item g.
 __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
     const float* __restrict__ w2, const float* __restrict__ ws2, const int* __restrict__ n_work,
     const int* __restrict__ work, const int* __restrict__ row_token, const int* __restrict__ row_slot, int T,
@@ -463,19 +517,49 @@ __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
   Group g;
   if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, g)) return;
   const int Kd = g.expert >= 0 ? I : I_s;
-  const int j = blockIdx.x * kThreads + threadIdx.x;
-  if (j >= H) return;
-  const float* wr = (g.expert >= 0 ? w2 + static_cast<size_t>(g.expert) * H * I : ws2) + static_cast<size_t>(j) * Kd;
-  for (int col = 0; col < g.n; ++col) {
-    const float* hr = hbuf + static_cast<size_t>(g.r0 + col) * ldh;
-    float acc = 0.f;
-    for (int i = 0; i < Kd; ++i) acc = fmaf(hr[i], wr[i], acc);
-    if (g.tok) {
-      const int r = g.r0 + col;
-      slot_out[(static_cast<size_t>(row_token[r]) * k + row_slot[r]) * H + j] = acc;
-    } else {
-      shared_out[static_cast<size_t>(g.t0 + col) * H + j] = acc;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j = blockIdx.x * kWave + lane;
+  const bool live = j < H;
+  const int jc = live ? j : H - 1;
+  const float* W = g.expert >= 0 ? w2 + static_cast<size_t>(g.expert) * H * I : ws2;
+  const int per = (Kd + 3) >> 2;
+  const int i0 = wave * per, i1 = min(Kd, i0 + per);
+  __shared__ float red[3][kF32Tok][kWave];
+  for (int p0 = 0; p0 < g.n; p0 += kF32Tok) {
+    float acc[kF32Tok];
+    const float* hr[kF32Tok];
+#pragma unroll
+    for (int t = 0; t < kF32Tok; ++t) {
+      acc[t] = 0.f;
+      hr[t] = hbuf + static_cast<size_t>(g.r0 + min(p0 + t, g.n - 1)) * ldh;
     }
+#pragma unroll 8
+    for (int i = i0; i < i1; ++i) {
+      const float wv = W[static_cast<size_t>(i) * H + jc];
+#pragma unroll
+      for (int t = 0; t < kF32Tok; ++t) acc[t] = fmaf(hr[t][i], wv, acc[t]);
+    }
+    if (wave > 0) {
+#pragma unroll
+      for (int t = 0; t < kF32Tok; ++t) red[wave - 1][t][lane] = acc[t];
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int t = 0; t < kF32Tok; ++t) {
+#pragma unroll
+        for (int ww = 0; ww < 3; ++ww) acc[t] += red[ww][t][lane];
+        const int col = p0 + t;
+        if (!live || col >= g.n) continue;
+        if (g.tok) {
+          const int r = g.r0 + col;
+          slot_out[(static_cast<size_t>(row_token[r]) * k + row_slot[r]) * H + j] = acc[t];
+        } else {
+          shared_out[static_cast<size_t>(g.t0 + col) * H + j] = acc[t];
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -569,7 +653,7 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
     }
   }
   float* hbuf = static_cast<float*>(a.workspace);
-  dim3 g_gu((ldh + kThreads - 1) / kThreads, items), g_dn((a.H + kThreads - 1) / kThreads, items);
+  dim3 g_gu((ldh + kWave - 1) / kWave, items), g_dn((a.H + kWave - 1) / kWave, items);
   ffn_gateup_f32_kernel<<<g_gu, kThreads, 0, s>>>(
       static_cast<const float*>(a.x), static_cast<const float*>(a.w13), static_cast<const float*>(a.ws13),
       a.sched.n_work, a.sched.work, a.sched.row_token, a.T, a.H, a.I, a.I_s, Tk, a.max_work, ldh, hbuf);

@@ -11,8 +11,9 @@
 //            + c%2, so a result lane holds (g_i, g_i+1, u_i, u_i+1) of a token.
 //   down     w2[e][jt][ks][lane][8], jt < H/16, ks < I/32: row c of tile jt is
 //            output feature 16*jt + c.
-// f32: gate and up stacked row-major, w13[e][0] = gate, w13[e][1] = up, each
-// [I][H]; w2 = w_down.
+// f32: reduction-major, so that consecutive lanes (consecutive output units)
+// read consecutive weights: w13[e][h][u], u < 2I, is the gate (u < I) or up
+// (u - I) weight of unit u at feature h; w2[e][i][j] = w_down[e][j][i].
 //
 // Activations: chunk-major [H/c][T][c] with c elements per 16-byte chunk
 // (c = 8 for bf16, 4 for f32), so the 16 tokens of a matrix-core column tile
@@ -61,7 +62,8 @@ __global__ __launch_bounds__(kPackThreads) void pack_down_bf16_kernel(
   *reinterpret_cast<u16x8*>(out + p * 8) = *reinterpret_cast<const u16x8*>(src);
 }
 
-// f32 gate/up: w13[e][0] = gate, w13[e][1] = up; one thread per element.
+// f32 gate/up: out[e][h][u] = u < I ? wg[e][u][h] : wu[e][u - I][h]; one
+// thread per output element.
 __global__ __launch_bounds__(kPackThreads) void stack_gateup_f32_kernel(
     const float* __restrict__ wg, const float* __restrict__ wu, int E, int I, int H,
     float* __restrict__ out) {
@@ -70,7 +72,20 @@ __global__ __launch_bounds__(kPackThreads) void stack_gateup_f32_kernel(
   const size_t p = static_cast<size_t>(blockIdx.x) * kPackThreads + threadIdx.x;
   if (p >= n) return;
   const size_t e = p / (2 * per), r = p % (2 * per);
-  out[p] = r < per ? wg[e * per + r] : wu[e * per + (r - per)];
+  const size_t h = r / (2 * static_cast<size_t>(I)), u = r % (2 * static_cast<size_t>(I));
+  out[p] = u < static_cast<size_t>(I) ? wg[e * per + u * H + h] : wu[e * per + (u - I) * H + h];
+}
+
+// f32 down: out[e][i][j] = wd[e][j][i]; one thread per output element.
+__global__ __launch_bounds__(kPackThreads) void transpose_down_f32_kernel(const float* __restrict__ wd, int E,
+                                                                          int H, int I, float* __restrict__ out) {
+  const size_t per = static_cast<size_t>(H) * I;
+  const size_t n = static_cast<size_t>(E) * per;
+  const size_t p = static_cast<size_t>(blockIdx.x) * kPackThreads + threadIdx.x;
+  if (p >= n) return;
+  const size_t e = p / per, r = p % per;
+  const size_t i = r / H, j = r % H;
+  out[p] = wd[e * per + j * I + i];
 }
 
 // Row-major [T][nc] -> chunk-major [nc][T] of 16-byte chunks (nc chunks per
@@ -105,7 +120,10 @@ hipError_t launch_pack_weights(const void* wg, const void* wu, const void* wd, d
       static_cast<const float*>(wg), static_cast<const float*>(wu), E, I, H, static_cast<float*>(w13));
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  return hipMemcpyAsync(w2, wd, static_cast<size_t>(E) * H * I * sizeof(float), hipMemcpyDeviceToDevice, s);
+  const size_t nd = static_cast<size_t>(E) * H * I;
+  transpose_down_f32_kernel<<<blocks_for(nd), kPackThreads, 0, s>>>(static_cast<const float*>(wd), E, H, I,
+                                                                    static_cast<float*>(w2));
+  return hipGetLastError();
 }
 
 hipError_t launch_pack_activations(const void* x, dmoe_dtype dt, int T, int H, void* x_chunked,

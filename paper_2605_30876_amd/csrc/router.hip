@@ -120,19 +120,28 @@ __global__ __launch_bounds__(256) void router_logits_bf16_kernel(
   }
 }
 
+// fp32 router: grid (ceil(E / 16), T).  Wave w of a workgroup computes the
+// logits of experts 16*bx + w, + 4, ... for token t: each lane accumulates
+// the features h = lane, lane + 64, ... of x[t] . w[e] (coalesced row reads),
+// then the wave sums its lanes in a fixed order (dev::wave_sum).
+constexpr int kF32RouterExperts = 16;
+
 __global__ __launch_bounds__(256) void router_logits_f32_kernel(
     const float* __restrict__ x, const float* __restrict__ w, int T, int H, int E,
     float* __restrict__ part, float* __restrict__ xk) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
   const int t = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const float* xr = x + static_cast<size_t>(t) * H;
   if (xk && blockIdx.x == 0)
     for (int h = threadIdx.x; h < H; h += blockDim.x) xk[(static_cast<size_t>(h >> 2) * T + t) * 4 + (h & 3)] = xr[h];
-  if (e >= E) return;
-  const float* wr = w + static_cast<size_t>(e) * H;
-  float acc = 0.f;
-  for (int h = 0; h < H; ++h) acc = fmaf(xr[h], wr[h], acc);
-  part[static_cast<size_t>(t) * E + e] = acc;
+  const int e1 = min(E, static_cast<int>(blockIdx.x + 1) * kF32RouterExperts);
+  for (int e = blockIdx.x * kF32RouterExperts + wave; e < e1; e += 4) {
+    const float* wr = w + static_cast<size_t>(e) * H;
+    float acc = 0.f;
+    for (int h = lane; h < H; h += kWave) acc = fmaf(xr[h], wr[h], acc);
+    acc = dev::wave_sum(acc);
+    if (lane == 0) part[static_cast<size_t>(t) * E + e] = acc;
+  }
 }
 
 // One wave per token row, four rows per workgroup.  Up to 512 experts the
@@ -198,7 +207,7 @@ hipError_t launch_router_partials(const void* x, const void* w, dmoe_dtype dt, i
                                                     static_cast<const bf16_t*>(w), T, H, E, S, part,
                                                     static_cast<bf16_t*>(x_chunked));
   } else {
-    dim3 grid((E + 255) / 256, T);
+    dim3 grid((E + kF32RouterExperts - 1) / kF32RouterExperts, T);
     router_logits_f32_kernel<<<grid, 256, 0, s>>>(static_cast<const float*>(x),
                                                    static_cast<const float*>(w), T, H, E, part,
                                                    static_cast<float*>(x_chunked));

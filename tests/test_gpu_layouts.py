@@ -63,8 +63,19 @@ def test_pack_expert_weights_f32(gpu_lib):
     w2 = torch.empty(E * H * I, device="cuda")
     lib.dmoe_pack_expert_weights(wg.cuda(), wu.cuda(), wd.cuda(), E, H, I, w13, w2)
     torch.cuda.synchronize()
-    assert torch.equal(w13.cpu(), torch.stack([wg, wu], 1).reshape(-1))
-    assert torch.equal(w2.cpu(), wd.reshape(-1))
+    # w13[e][h][u]: gate units then up units at feature h; w2[e][i][j] = w_down[e][j][i]
+    exp13 = torch.empty((E, H, 2 * I))
+    for e in range(E):
+        for h in range(H):
+            for u in range(2 * I):
+                exp13[e, h, u] = wg[e, u, h] if u < I else wu[e, u - I, h]
+    exp2 = torch.empty((E, I, H))
+    for e in range(E):
+        for i in range(I):
+            for j in range(H):
+                exp2[e, i, j] = wd[e, j, i]
+    assert torch.equal(w13.cpu(), exp13.reshape(-1))
+    assert torch.equal(w2.cpu(), exp2.reshape(-1))
 
 
 @pytest.mark.parametrize("dtype,T,H", [(torch.bfloat16, 72, 512), (torch.bfloat16, 1, 128),
