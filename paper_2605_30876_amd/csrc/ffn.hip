@@ -299,16 +299,19 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 
 // ---- tile kernels: many tokens per work item --------------------------------
 //
-// A workgroup covers 64 weight rows (wave w: packed 16-row tile 4*bx + w,
-// over the whole reduction) x up to 128 tokens of one work item (8 token
-// tiles).  The reduction runs in stages of kStageSteps K-steps: the
-// stage's token fragments are loaded from global memory once per workgroup
-// into a double-buffered LDS stage and read by all four waves, while each
-// wave streams its own weight tile into registers one stage ahead.
-// Accumulation order (K ascending) and the epilogues match the decode
-// kernels.
+// A workgroup covers 4 * kRowTiles 16-row weight tiles (wave w: packed tiles
+// kRowTiles * (4*bx + w) + m, m < kRowTiles, over the whole reduction) x up
+// to 128 tokens of one work item (8 token tiles).  The reduction runs in
+// stages of kStageSteps K-steps: the stage's token fragments are loaded from
+// global memory once per workgroup into a double-buffered LDS stage read by
+// all four waves, each fragment read once per wave and applied to the
+// wave's kRowTiles weight tiles, while each wave streams its own weight tiles
+// into registers one stage ahead.  Accumulation order (K ascending) and the
+// epilogues match the decode kernels.
 constexpr int kTileTok = 8;       // token tiles per workgroup (128 tokens)
 constexpr int kStageSteps = 4;    // K-steps per LDS stage
+constexpr int kRowTiles = 2;      // weight tiles per wave
+constexpr int kTileRows = 4 * kRowTiles;  // weight tiles per workgroup
 static_assert(kTileTok * 16 == DMOE_WORK_ROWS, "a tile workgroup covers one work item's rows");
 
 template <bool kGateUp>
@@ -319,16 +322,18 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int Kd = kGateUp ? H : Iw;                    // reduction length
   const int tiles = kGateUp ? Iw / 8 : H / 16;        // packed 16-row tiles of the matrix
-  if (blockIdx.x * 4 >= tiles) return;                // uniform: the whole workgroup is past the matrix
+  if (static_cast<int>(blockIdx.x) * kTileRows >= tiles) return;  // uniform: past the matrix
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int tile = blockIdx.x * 4 + wave;             // tiles % 4 == 0 (H, I, I_s multiples of 128)
+  // tiles % kTileRows == 0 (H, I, I_s multiples of 128)
+  const int tile0 = (blockIdx.x * 4 + wave) * kRowTiles;
   const int ksteps = Kd >> 5;                         // multiple of kStageSteps
   const bf16_t* W;
   if (kGateUp)
     W = g.expert >= 0 ? p.w13 + static_cast<size_t>(g.expert) * 2 * p.I * H : p.ws13;
   else
     W = g.expert >= 0 ? p.w2 + static_cast<size_t>(g.expert) * H * p.I : p.ws2;
-  const bf16_t* pa = W + static_cast<size_t>(tile) * ksteps * kFrag + lane * 8;
+  const bf16_t* pa = W + static_cast<size_t>(tile0) * ksteps * kFrag + lane * 8;
+  const size_t tstride = static_cast<size_t>(ksteps) * kFrag;  // next packed tile
   const int nt = (g.n + 15) >> 4;  // live token tiles
 
   // Token-fragment producer: thread t loads pieces (tile t/64, lane t%64) and
@@ -354,16 +359,19 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   }
 
   __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 64 KiB
-  f32x4 acc[kTileTok];
+  f32x4 acc[kRowTiles][kTileTok];
 #pragma unroll
-  for (int ct = 0; ct < kTileTok; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 a_cur[kStageSteps], a_nxt[kStageSteps], b_nxt[kStageSteps][2];
+  for (int m = 0; m < kRowTiles; ++m)
+#pragma unroll
+    for (int ct = 0; ct < kTileTok; ++ct) acc[m][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 a_cur[kStageSteps][kRowTiles], a_nxt[kStageSteps][kRowTiles], b_nxt[kStageSteps][2];
 
   auto load_stage = [&](int st) {
 #pragma unroll
     for (int s = 0; s < kStageSteps; ++s) {
       const int ks = st * kStageSteps + s;
-      a_nxt[s] = ld_bf16x8(pa + ks * kFrag);
+#pragma unroll
+      for (int m = 0; m < kRowTiles; ++m) a_nxt[s][m] = ld_bf16x8(pa + m * tstride + ks * kFrag);
 #pragma unroll
       for (int h = 0; h < 2; ++h)
         if (pl_live[h]) b_nxt[s][h] = ld_bf16x8(pb[h] + ks * bstep);
@@ -381,7 +389,9 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   load_stage(0);
   store_stage(0);
 #pragma unroll
-  for (int s = 0; s < kStageSteps; ++s) a_cur[s] = a_nxt[s];
+  for (int s = 0; s < kStageSteps; ++s)
+#pragma unroll
+    for (int m = 0; m < kRowTiles; ++m) a_cur[s][m] = a_nxt[s][m];
   __syncthreads();
   for (int st = 0; st < nstages; ++st) {
     const int buf = st & 1;
@@ -392,38 +402,48 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
     for (int s = 0; s < kStageSteps; ++s)
 #pragma unroll
       for (int ct = 0; ct < kTileTok; ++ct)
-        if (ct < nt)
-          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur[s], stage[buf][s][ct][lane], acc[ct], 0, 0, 0);
+        if (ct < nt) {
+          const bf16x8 b = stage[buf][s][ct][lane];
+#pragma unroll
+          for (int m = 0; m < kRowTiles; ++m)
+            acc[m][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur[s][m], b, acc[m][ct], 0, 0, 0);
+        }
     if (more) {
       store_stage(buf ^ 1);
 #pragma unroll
-      for (int s = 0; s < kStageSteps; ++s) a_cur[s] = a_nxt[s];
+      for (int s = 0; s < kStageSteps; ++s)
+#pragma unroll
+        for (int m = 0; m < kRowTiles; ++m) a_cur[s][m] = a_nxt[s][m];
     }
     __syncthreads();
   }
 
   const int q = lane >> 4, c = lane & 15;
 #pragma unroll
-  for (int ct = 0; ct < kTileTok; ++ct) {
-    const int col = ct * 16 + c;
-    if (ct >= nt || col >= g.n) continue;
-    const f32x4 v = acc[ct];
-    if (kGateUp) {
-      // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*tile + 2q
-      const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
-      const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3]);
-      bf16_t* dst = p.hk + (static_cast<size_t>(tile) * p.R + g.r0 + col) * 8 + 2 * q;
-      *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
-    } else {
-      const int j = tile * 16 + 4 * q;
-      float* dst;
-      if (g.tok) {
-        const int r = g.r0 + col;
-        dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H + j;
+  for (int m = 0; m < kRowTiles; ++m) {
+    const int tile = tile0 + m;
+#pragma unroll
+    for (int ct = 0; ct < kTileTok; ++ct) {
+      const int col = ct * 16 + c;
+      if (ct >= nt || col >= g.n) continue;
+      const f32x4 v = acc[m][ct];
+      if (kGateUp) {
+        // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*tile + 2q
+        const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
+        const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3]);
+        bf16_t* dst = p.hk + (static_cast<size_t>(tile) * p.R + g.r0 + col) * 8 + 2 * q;
+        *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
       } else {
-        dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H + j;
+        const int j = tile * 16 + 4 * q;
+        float* dst;
+        if (g.tok) {
+          const int r = g.r0 + col;
+          dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H + j;
+        } else {
+          dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H + j;
+        }
+        *reinterpret_cast<f32x4*>(dst) = v;
       }
-      *reinterpret_cast<f32x4*>(dst) = v;
     }
   }
 }
@@ -640,10 +660,10 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
     if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
-      ffn_tile_bf16_kernel<true><<<dim3(ldh / 32, items), kThreads, 0, s>>>(p);
+      ffn_tile_bf16_kernel<true><<<dim3(ldh / (8 * kTileRows), items), kThreads, 0, s>>>(p);
       hipError_t err = hipGetLastError();
       if (err != hipSuccess) return err;
-      ffn_tile_bf16_kernel<false><<<dim3(a.H / 64, items), kThreads, 0, s>>>(p);
+      ffn_tile_bf16_kernel<false><<<dim3(a.H / (16 * kTileRows), items), kThreads, 0, s>>>(p);
       return hipGetLastError();
     }
     switch (pick_ntiles(a.T, a.k, a.max_work)) {
