@@ -13,13 +13,18 @@
         plain copy kernel of N bytes.  Writes markdown to stdout and, with
         --json, the figures bench.py reports as ``roofline.traffic``.
 
-    python -m paper_2605_30876_amd.prof_summary mfma --csv CSV --kernel PATTERN ...
-        MFMA busy fraction and bf16 MFMA throughput per dispatch from a
+    python -m paper_2605_30876_amd.prof_summary mfma --csv CSV --kernel PATTERN ... [--avg-us US ...]
+        bf16 MFMA work per dispatch (SQ_INSTS_VALU_MFMA_MOPS_BF16 of a
         ``--pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16
-        GRBM_GUI_ACTIVE`` run.
+        GRBM_GUI_ACTIVE`` run) and, given each kernel's average duration from
+        a kernel trace, the achieved TFLOP/s against the dense bf16 peak.
 
     python -m paper_2605_30876_amd.prof_summary sweep --json OUT.json --cmd C
         The JSON line of ``bench.py --sweep`` as markdown tables.
+
+    python -m paper_2605_30876_amd.prof_summary configs --json A.json B.json ... --cmd C
+        The JSON lines of ``bench.py --config CFG`` runs as one table (every
+        routing mode of every configuration).
 """
 from __future__ import annotations
 
@@ -121,15 +126,19 @@ def cmd_mfma(a):
     busy = read_counters(a.csv, "SQ_VALU_MFMA_BUSY_CYCLES")
     mops = read_counters(a.csv, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
     gui = read_counters(a.csv, "GRBM_GUI_ACTIVE")
-    print("| kernel | dispatches | MFMA busy % of SIMD cycles | bf16 MFMA MOPs per dispatch |\n|---|---|---|---|")
+    avg = dict(zip(a.kernel, a.avg_us)) if a.avg_us else {}
+    print("| kernel | dispatches | bf16 MFMA MOPs per dispatch | GFLOP | avg µs (trace) | TFLOP/s | of 2.5 PFLOP/s "
+          "|\n|---|---|---|---|---|---|---|")
     for pat in a.kernel:
         b, n = mean_per_dispatch(busy, pat)
         m, _ = mean_per_dispatch(mops, pat)
         g, _ = mean_per_dispatch(gui, pat)
         if b is None:
             continue
-        util = 100.0 * b / (g * a.simds) if g else float("nan")
-        print(f"| `{pat}` | {n} | {util:.1f} | {m:.0f} |")
+        gflop = m * 512 / 1e9  # a bf16 MFMA MOP is 512 flops
+        us = avg.get(pat)
+        rate = f"{gflop / us * 1e3:.0f} | {100 * gflop / us * 1e3 / 2500:.1f}%" if us else "— | —"
+        print(f"| `{pat}` | {n} | {m:.0f} | {gflop:.1f} | {us if us else '—'} | {rate} |")
 
 
 def cmd_sweep(a):
@@ -161,6 +170,27 @@ def cmd_sweep(a):
           f"the slope streams one expert's 6 MiB at {f['marginal_gbps']} GB/s.")
 
 
+def cmd_configs(a):
+    print("# Bench, every configuration (one MI355X)\n\nCommand, per configuration (from the repository root on the "
+          f"GPU box):\n\n```\n{a.cmd}\n```\n")
+    print("Graph-replayed steps rotating over distinct layers (experts streamed from HBM, not the 256 MB "
+          "memory-side cache). `bytes` = algorithmic HBM bytes per step (selected experts once + shared expert + "
+          "router + x in/y out); GB/s = bytes / wall time. Top-P routing uses p = 0.6.\n")
+    print("| config | routing | µs/step | tokens/s | unique experts | bytes (MB) | layer GB/s | of 8 TB/s "
+          "| expert FFN µs | FFN GB/s |\n|---|---|---|---|---|---|---|---|---|---|")
+    for path in a.json:
+        with open(path) as fh:
+            d = json.loads(fh.read().strip().splitlines()[-1])
+        name = d["config"]["workload"].split(":")[0]
+        for mode in ("block", "token", "topp"):
+            r = d.get(f"{mode}_routing")
+            if not r:
+                continue
+            print(f"| {name} | {mode} | {r['us_per_step']} | {r['tokens_per_s']:.0f} | {r['unique_experts_per_forward']} "
+                  f"| {r['hbm_bytes_per_step'] / 1e6:.1f} | {r['hbm_gbps']:.0f} | {100 * r['frac_peak']:.1f}% "
+                  f"| {r['expert_ffn_us']} | {r['expert_ffn_gbps']:.0f} |")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="what", required=True)
@@ -183,7 +213,12 @@ def main(argv=None):
     m.add_argument("--csv", required=True)
     m.add_argument("--kernel", nargs="+", required=True)
     m.add_argument("--simds", type=int, default=1024, help="SIMDs on the chip (256 CUs x 4)")
+    m.add_argument("--avg-us", type=float, nargs="*", help="average duration of each --kernel (kernel trace)")
     m.set_defaults(fn=cmd_mfma)
+    c = sub.add_parser("configs")
+    c.add_argument("--json", nargs="+", required=True)
+    c.add_argument("--cmd", required=True)
+    c.set_defaults(fn=cmd_configs)
     w = sub.add_parser("sweep")
     w.add_argument("--json", required=True)
     w.add_argument("--cmd", required=True)
