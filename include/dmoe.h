@@ -324,7 +324,8 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
  * It needs no routing, so a caller can run it on a second stream while the
  * routing of the same forward runs, then call dmoe_expert_ffn with the
  * shared expert left out (ws13 = ws2 = shared_out = NULL, I_s = 0); the
- * results are those of one dmoe_expert_ffn call with the shared expert.
+ * results are those of one dmoe_expert_ffn call with the shared expert, up
+ * to the fp32 summation order (the two calls may tile its rows differently).
  * x_chunked [T][H] chunk-major (see above); ws13, ws2: the shared expert
  * packed by dmoe_pack_expert_weights (n_experts = 1, I = I_s); shared_out
  * [T][H] float32.  workspace: device scratch of at least

@@ -94,6 +94,8 @@ struct FfnParams {
   const int* row_slot;
   int T, H, I, I_s, k, Tk, R, max_work;  // R: rows of the h buffer
   int shared_items;                        // grid rows of the shared expert's pieces (0: none)
+  int split_rows;                          // > 0: decode kernels take items of <= split_rows rows,
+                                           // the tile kernels the larger ones
   bf16_t* hk;                              // SwiGLU activations, chunk-major [ldh/8][R][8]
   float* slot_out;
   float* shared_out;
@@ -152,17 +154,18 @@ __device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC>& w, const bf16_t
 
 // acc[ct] += A . B_ct^T over this wave's `steps` K-steps, in bursts of KMAX
 // steps: token chunk 0, the weight burst, then the remaining token chunks.
+// With a_held (the slice is one burst, steps <= KMAX, already in w.a from
+// the previous pass over the same weights) the weights are not loaded again.
 template <int NT, int KMAX, int BC>
-__device__ __forceinline__ void wave_dot(const bf16_t* pa, const bf16_t* const* pb, int bstep, int steps,
-                                         f32x4 (&acc)[NT]) {
-  WaveOps<NT, KMAX, BC> w;
+__device__ __forceinline__ void wave_dot(WaveOps<NT, KMAX, BC>& w, const bf16_t* pa, const bf16_t* const* pb,
+                                         int bstep, int steps, f32x4 (&acc)[NT], bool a_held) {
   for (int sc = 0; sc < steps; sc += KMAX) {
     const int ns = min(KMAX, steps - sc);
     const bf16_t* pbs[NT];
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) pbs[ct] = pb[ct] + sc * bstep;
     issue_b<0>(w, pbs, bstep, 0, ns);
-    issue_a(w, pa + sc * kFrag, ns);
+    if (!a_held) issue_a(w, pa + sc * kFrag, ns);
     __builtin_amdgcn_sched_barrier(0);
     mma_chunk<0>(w, pbs, bstep, ns, acc);
   }
@@ -203,6 +206,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
                                  p.Tk, g))
     return;
+  if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int it = blockIdx.x;
   if (it * 8 >= Iw) return;
@@ -216,6 +220,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
   const int chunk0 = wave * steps * 4 + q;
 
   __shared__ f32x4 red[3][NT][kWave];
+  WaveOps<NT, KMAX, BC> w;  // a one-burst weight slice stays here across passes
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
     const bf16_t* pb[NT];
 #pragma unroll
@@ -226,7 +231,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
     }
     f32x4 acc[NT];
     zero(acc);
-    wave_dot<NT, KMAX, BC>(pa, pb, bstep, steps, acc);
+    wave_dot(w, pa, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -253,6 +258,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
                                  p.Tk, g))
     return;
+  if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
   const int jt = blockIdx.x;
@@ -265,6 +271,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   const int chunk0 = wave * steps * 4 + q;
 
   __shared__ f32x4 red[3][NT][kWave];
+  WaveOps<NT, KMAX, BC> w;  // a one-burst weight slice stays here across passes
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
     const bf16_t* pb[NT];
 #pragma unroll
@@ -274,7 +281,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
     }
     f32x4 acc[NT];
     zero(acc);
-    wave_dot<NT, KMAX, BC>(pa, pb, bstep, steps, acc);
+    wave_dot(w, pa, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -318,6 +325,7 @@ template <bool kGateUp>
 __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_item(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g)) return;
+  if (g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
   const int H = p.H;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int Kd = kGateUp ? H : Iw;                    // reduction length
@@ -609,7 +617,7 @@ template <int NT>
 struct Shape;
 template <>
 struct Shape<1> {
-  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 1, kDnMax = 8, kDnChunk = 4, kDnWaves = 1;
+  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 4, kDnMax = 8, kDnChunk = 4, kDnWaves = 5;
   static constexpr bool kSharedFirst = true;
 };
 template <>
@@ -635,6 +643,27 @@ hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   return hipGetLastError();
 }
 
+constexpr int kSplitRows = 32;  // one-tile schedules: larger items go to the tile kernels
+
+// One-tile decode kernels for the items of <= p.split_rows rows and the tile
+// kernels for the others; each gate/up half runs before either down half.
+hipError_t launch_hybrid_bf16(const FfnParams& p, int ldh, int items, hipStream_t s) {
+  using S = Shape<1>;
+  ffn_gateup_bf16_kernel<1, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst>
+      <<<dim3(ldh / 8, items), kThreads, 0, s>>>(p);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  ffn_tile_bf16_kernel<true><<<dim3(ldh / (8 * kTileRows), items), kThreads, 0, s>>>(p);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  ffn_down_bf16_kernel<1, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst>
+      <<<dim3(p.H / 16, items), kThreads, 0, s>>>(p);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  ffn_tile_bf16_kernel<false><<<dim3(p.H / (16 * kTileRows), items), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
 bool use_tile_kernels(int T, int k, int max_work, int items, int ldh) {
   return rows_per_item(T, k, max_work) >= 32 && static_cast<long>(ldh / 32) * items >= 512;
 }
@@ -657,7 +686,7 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
     FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w13),
                 static_cast<const bf16_t*>(a.w2), static_cast<const bf16_t*>(a.ws13),
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
-                a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items,
+                a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
     if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
       ffn_tile_bf16_kernel<true><<<dim3(ldh / (8 * kTileRows), items), kThreads, 0, s>>>(p);
@@ -667,7 +696,19 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
       return hipGetLastError();
     }
     switch (pick_ntiles(a.T, a.k, a.max_work)) {
-      case 1: return launch_bf16<1>(p, ldh, items, s);
+      case 1:
+        // Items of a one-tile schedule average few rows, but an expert can
+        // still collect many (a popular expert, a small Top-P coreset, the
+        // shared expert over more than 32 tokens).  The decode kernels keep a
+        // wave's weight slice in registers across 16-row passes when it is
+        // one burst; when it is not, they would stream the weights once per
+        // pass, so items past 32 rows go to the tile kernels, launched beside
+        // them.
+        if (a.T > kSplitRows && (a.H / 128 > Shape<1>::kGuMax || ldh / 128 > Shape<1>::kDnMax)) {
+          p.split_rows = kSplitRows;
+          return launch_hybrid_bf16(p, ldh, items, s);
+        }
+        return launch_bf16<1>(p, ldh, items, s);
       case 2: return launch_bf16<2>(p, ldh, items, s);
       default: return launch_bf16<4>(p, ldh, items, s);
     }

@@ -54,7 +54,8 @@ class MoELayer:
 
         overlap_shared: run the shared expert (dmoe_shared_expert_ffn) on a
         second stream, concurrently with the routing and the routed experts;
-        the results are bitwise those of the single dmoe_expert_ffn call.  Off
+        the results are those of the single dmoe_expert_ffn call up to the
+        fp32 summation order of the shared expert.  Off
         by default: replayed from a HIP graph, the two-stream forward of a
         32-token decode step is slower (53 vs 40 us) than the one-stream one."""
         self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
