@@ -106,8 +106,14 @@ typedef enum dmoe_dtype {
  *                       of at most DMOE_WORK_ROWS rows; items are ordered by
  *                       expert id, then row.  max_work: dmoe_schedule_max_work.
  * Within one expert, rows are ordered by token.
+ *   scratch  optional (NULL: not used); with group_size 1 and at least
+ *            DMOE_SCHED_SPLIT_MIN entries (n_groups*k), a schedule with
+ *            scratch is built by many workgroups instead of one; it needs
+ *            (ceil(n_groups*k / 512) + 1) * E ints (dmoe_schedule_scratch_ints).
+ *            The results are identical either way.
  */
 #define DMOE_WORK_ROWS 128
+#define DMOE_SCHED_SPLIT_MIN 2048
 
 typedef struct dmoe_schedule {
   int32_t* n_unique;
@@ -117,6 +123,7 @@ typedef struct dmoe_schedule {
   int32_t* row_slot;
   int32_t* n_work;
   int32_t* work;
+  int32_t* scratch;
 } dmoe_schedule;
 
 /*
@@ -126,6 +133,10 @@ typedef struct dmoe_schedule {
  * dmoe_expert_ffn.  0 on invalid sizes.
  */
 int dmoe_schedule_max_work(int n_groups, int group_size, int k, int E);
+
+/* Ints of dmoe_schedule.scratch for n_groups expert lists of k among E
+ * experts: (ceil(n_groups*k / 512) + 1) * E.  0 on invalid sizes. */
+size_t dmoe_schedule_scratch_ints(int n_groups, int k, int E);
 
 /*
  * Bytes of optional workspace that let dmoe_router_logits split the hidden

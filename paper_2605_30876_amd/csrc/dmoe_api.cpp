@@ -171,6 +171,7 @@ dmoe_status dmoe_build_expert_schedule(const int32_t* experts, int n_groups, int
   ALIGNED(sched.n_unique);
   ALIGNED(sched.unique);
   ALIGNED(sched.offsets);
+  ALIGNED(sched.scratch);
   ALIGNED(sched.row_token);
   ALIGNED(sched.row_slot);
   ALIGNED(sched.n_work);
@@ -212,6 +213,7 @@ dmoe_status dmoe_route_block(const void* x, const void* w_router, const float* b
   ALIGNED(sched.n_unique);
   ALIGNED(sched.unique);
   ALIGNED(sched.offsets);
+  ALIGNED(sched.scratch);
   ALIGNED(sched.row_token);
   ALIGNED(sched.row_slot);
   ALIGNED(sched.n_work);
@@ -258,6 +260,7 @@ dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* b
   ALIGNED(sched.n_unique);
   ALIGNED(sched.unique);
   ALIGNED(sched.offsets);
+  ALIGNED(sched.scratch);
   ALIGNED(sched.row_token);
   ALIGNED(sched.row_slot);
   ALIGNED(sched.n_work);
@@ -315,6 +318,11 @@ int dmoe_schedule_max_work(int n_groups, int group_size, int k, int E) {
   if (n_groups < 1 || group_size < 1 || k < 1 || E < 1 || k > E) return 0;
   const long n = dmoe::schedule_max_work(n_groups, group_size, k, E);
   return n <= kIntLimit ? static_cast<int>(n) : 0;
+}
+
+size_t dmoe_schedule_scratch_ints(int n_groups, int k, int E) {
+  if (n_groups < 1 || k < 1 || E < 1) return 0;
+  return dmoe::schedule_scratch_ints(n_groups, k, E);
 }
 
 size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {

@@ -124,6 +124,7 @@ struct FfnArgs {
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
 long schedule_max_work(long n_groups, long group_size, long k, long E);
+size_t schedule_scratch_ints(long n_groups, long k, long E);
 
 hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
                           dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);

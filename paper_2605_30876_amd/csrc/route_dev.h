@@ -502,56 +502,18 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Builds the schedule of n_groups expert lists of k (experts: global or LDS,
-// [n_groups][k]; group g covers tokens g*gs .. g*gs+gs-1).  Called by all
-// kSchedThreads threads of the workgroup; lds holds schedule_lds_ints(E) ints
-// (16-byte aligned).
-//   1. counts the selections of every expert (LDS integer atomics),
-//   2. scans the counts: ascending unique ids, their row offsets, n_unique,
-//   3. places the (group, slot) entries in rounds of kSchedThreads, in index
-//      order: an entry's rank among earlier entries of its expert is a
-//      running count plus the entries below it in the round's per-expert
-//      bitmask (read as four 128-bit words), so each expert's rows come out
-//      in token order and the schedule is identical on every run; then all
-//      threads write the round's rows.
-__device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs, int k, int E, int* lds,
-                                   const dmoe_schedule& sched) {
-  int32_t* const n_unique = sched.n_unique;
-  int32_t* const unique = sched.unique;
-  int32_t* const offsets = sched.offsets;
-  int32_t* const row_token = sched.row_token;
-  int32_t* const row_slot = sched.row_slot;
-  const int Ep = pad4(E);
-  int* cnt = lds;                                          // [E] selections
-  int* base = cnt + Ep;                                    // [E] first row
-  int* run = base + Ep;                                    // [E] entries placed so far
-  unsigned* mask = reinterpret_cast<unsigned*>(run + Ep);  // [E][kMaskWords]
-  int* pos = reinterpret_cast<int*>(mask + static_cast<size_t>(Ep) * kMaskWords);  // [kSchedThreads]
+// Totals of the schedule from the per-expert selection counts (thread e of
+// the kSchedThreads passes c = the count of expert e, 0 for e >= E; E <=
+// kSchedThreads): ascending unique ids, their row offsets, n_unique, the
+// work items and n_work; base[e] (LDS or global) receives expert e's first
+// row.  Called by all threads of the workgroup.
+__device__ inline void schedule_totals(int c, int gs, int E, const dmoe_schedule& sched, int* base) {
   __shared__ int wrows[kSchedThreads / kWave];
   __shared__ int wuniq[kSchedThreads / kWave];
   __shared__ int wchunk[kSchedThreads / kWave];
-
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  for (int e = tid; e < E; e += kSchedThreads) {
-    cnt[e] = 0;
-    run[e] = 0;
-    uint4* m4 = reinterpret_cast<uint4*>(mask + e * kMaskWords);
-#pragma unroll
-    for (int w = 0; w < kMaskWords / 4; ++w) m4[w] = make_uint4(0u, 0u, 0u, 0u);
-  }
-  __syncthreads();
-
-  const int n_entries = n_groups * k;
-  for (int i = tid; i < n_entries; i += kSchedThreads) {
-    const int e = experts[i];
-    if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
-  }
-  __syncthreads();
-
-  // Exclusive scans over experts (E <= kSchedThreads: one expert per thread).
-  const int c = tid < E ? cnt[tid] : 0;
   const int rows = c * gs;
   const int pres = c > 0 ? 1 : 0;
   const int chunks = (rows + DMOE_WORK_ROWS - 1) / DMOE_WORK_ROWS;  // work items of this expert
@@ -576,18 +538,61 @@ __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs,
   if (tid < E) {
     base[tid] = r_excl;
     if (pres) {
-      unique[u_excl] = tid;
-      offsets[u_excl] = r_excl;
+      sched.unique[u_excl] = tid;
+      sched.offsets[u_excl] = r_excl;
     }
     int4* work = reinterpret_cast<int4*>(sched.work) + c_excl;
-    for (int c = 0; c < chunks; ++c)
-      work[c] = make_int4(tid, r_excl + c * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, rows - c * DMOE_WORK_ROWS), 0);
+    for (int q = 0; q < chunks; ++q)
+      work[q] = make_int4(tid, r_excl + q * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, rows - q * DMOE_WORK_ROWS), 0);
   }
   if (tid == kSchedThreads - 1) {
-    offsets[u_excl + pres] = r_excl + rows;
-    *n_unique = u_excl + pres;
+    sched.offsets[u_excl + pres] = r_excl + rows;
+    *sched.n_unique = u_excl + pres;
     *sched.n_work = c_excl + chunks;
   }
+}
+
+// Builds the schedule of n_groups expert lists of k (experts: global or LDS,
+// [n_groups][k]; group g covers tokens g*gs .. g*gs+gs-1).  Called by all
+// kSchedThreads threads of the workgroup; lds holds schedule_lds_ints(E) ints
+// (16-byte aligned).
+//   1. counts the selections of every expert (LDS integer atomics),
+//   2. scans the counts: ascending unique ids, their row offsets, n_unique,
+//   3. places the (group, slot) entries in rounds of kSchedThreads, in index
+//      order: an entry's rank among earlier entries of its expert is a
+//      running count plus the entries below it in the round's per-expert
+//      bitmask (read as four 128-bit words), so each expert's rows come out
+//      in token order and the schedule is identical on every run; then all
+//      threads write the round's rows.
+__device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs, int k, int E, int* lds,
+                                   const dmoe_schedule& sched) {
+  int32_t* const row_token = sched.row_token;
+  int32_t* const row_slot = sched.row_slot;
+  const int Ep = pad4(E);
+  int* cnt = lds;                                          // [E] selections
+  int* base = cnt + Ep;                                    // [E] first row
+  int* run = base + Ep;                                    // [E] entries placed so far
+  unsigned* mask = reinterpret_cast<unsigned*>(run + Ep);  // [E][kMaskWords]
+  int* pos = reinterpret_cast<int*>(mask + static_cast<size_t>(Ep) * kMaskWords);  // [kSchedThreads]
+
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += kSchedThreads) {
+    cnt[e] = 0;
+    run[e] = 0;
+    uint4* m4 = reinterpret_cast<uint4*>(mask + e * kMaskWords);
+#pragma unroll
+    for (int w = 0; w < kMaskWords / 4; ++w) m4[w] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  __syncthreads();
+
+  const int n_entries = n_groups * k;
+  for (int i = tid; i < n_entries; i += kSchedThreads) {
+    const int e = experts[i];
+    if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+
+  schedule_totals(tid < E ? cnt[tid] : 0, gs, E, sched, base);
   __syncthreads();
 
   const int word = tid >> 5;

@@ -29,7 +29,8 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 
 # Every symbol include/dmoe.h declares.
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
-           "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work", "dmoe_route_block",
+           "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work",
+           "dmoe_schedule_scratch_ints", "dmoe_route_block",
            "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
            "dmoe_expert_ffn", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
            "dmoe_last_error", "dmoe_version")
@@ -47,7 +48,8 @@ WORK_ROWS = 128  # DMOE_WORK_ROWS: rows of one expert per work item at most
 class dmoe_schedule(ctypes.Structure):
     _fields_ = [("n_unique", ctypes.c_void_p), ("unique", ctypes.c_void_p),
                 ("offsets", ctypes.c_void_p), ("row_token", ctypes.c_void_p),
-                ("row_slot", ctypes.c_void_p), ("n_work", ctypes.c_void_p), ("work", ctypes.c_void_p)]
+                ("row_slot", ctypes.c_void_p), ("n_work", ctypes.c_void_p), ("work", ctypes.c_void_p),
+                ("scratch", ctypes.c_void_p)]
 
 
 _P = ctypes.c_void_p
@@ -61,6 +63,7 @@ _SIGS = {
     "dmoe_block_topp_route": ([_P, _I, _I, _I, _I, ctypes.c_float, _I, _P, _P, _P, _P, _P, _P, _P], _I),
     "dmoe_build_expert_schedule": ([_P, _I, _I, _I, _I, dmoe_schedule, _P], _I),
     "dmoe_schedule_max_work": ([_I, _I, _I, _I], _I),
+    "dmoe_schedule_scratch_ints": ([_I, _I, _I], _S),
     "dmoe_route_block": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S,
                           _P], _I),
     "dmoe_route_token": ([_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S, _P], _I),
@@ -169,17 +172,26 @@ class Schedule:
     row_slot: torch.Tensor
     n_work: torch.Tensor
     work: torch.Tensor  # [max_work, 4]: expert id, first row, row count, 0
+    scratch: torch.Tensor | None = None  # lets a large token schedule use many workgroups
 
     @staticmethod
-    def empty(E: int, n_rows: int, device, max_work: int | None = None) -> "Schedule":
+    def empty(E: int, n_rows: int, device, max_work: int | None = None, scratch: bool = True) -> "Schedule":
+        """Arrays for schedules of up to n_rows rows (a token schedule of
+        n_rows / k tokens needs n_rows entries of scratch capacity)."""
         z = lambda n: torch.zeros(max(n, 4), dtype=torch.int32, device=device)  # noqa: E731
         mw = max(max_work if max_work is not None else n_rows, 1)
+        sc = z(dmoe_schedule_scratch_ints(n_rows, 1, E)) if scratch else None
         return Schedule(z(1), z(E), z(E + 1), z(n_rows), z(n_rows), z(1),
-                        torch.zeros((mw, 4), dtype=torch.int32, device=device))
+                        torch.zeros((mw, 4), dtype=torch.int32, device=device), sc)
 
     def as_c(self) -> dmoe_schedule:
         return dmoe_schedule(ptr(self.n_unique), ptr(self.unique), ptr(self.offsets),
-                             ptr(self.row_token), ptr(self.row_slot), ptr(self.n_work), ptr(self.work))
+                             ptr(self.row_token), ptr(self.row_slot), ptr(self.n_work), ptr(self.work),
+                             ptr(self.scratch))
+
+
+def dmoe_schedule_scratch_ints(n_groups, k, E) -> int:
+    return int(load().dmoe_schedule_scratch_ints(n_groups, k, E))
 
 
 def dmoe_schedule_max_work(n_groups, group_size, k, E) -> int:

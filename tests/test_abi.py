@@ -314,3 +314,12 @@ def test_last_error_cleared_per_thread(L, buf):
     _, p = buf
     L.dmoe_combine(None, p, None, 1, 32, 2048, 8, p, None)
     assert L.dmoe_last_error().decode().startswith("dmoe_combine")
+
+
+def test_schedule_scratch_ints():
+    # (ceil(n_groups*k / 512) + 1) * E
+    assert lib.dmoe_schedule_scratch_ints(512, 8, 256) == (8 + 1) * 256
+    assert lib.dmoe_schedule_scratch_ints(4096, 8, 256) == (64 + 1) * 256
+    assert lib.dmoe_schedule_scratch_ints(1, 1, 16) == 2 * 16
+    assert lib.dmoe_schedule_scratch_ints(0, 8, 256) == 0
+    assert lib.dmoe_schedule_scratch_ints(8, 8, 0) == 0
