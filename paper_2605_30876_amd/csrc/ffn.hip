@@ -37,6 +37,7 @@
 //    row in both operands, which is all the matrix instruction needs.
 // f32 path: plain per-thread dot products (small fp32 layers).
 #include <algorithm>
+#include <type_traits>
 
 #include "dmoe_common.h"
 
@@ -313,8 +314,9 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 // global memory once per workgroup into a double-buffered LDS stage read by
 // all four waves, each fragment read once per wave and applied to the
 // wave's kRowTiles weight tiles, while each wave streams its own weight tiles
-// into registers one stage ahead.  Accumulation order (K ascending) and the
-// epilogues match the decode kernels.
+// into registers two stages ahead (HBM latency spans more than one stage's
+// matrix work).  Accumulation order (K ascending) and the epilogues match the
+// decode kernels.
 constexpr int kTileTok = 8;       // token tiles per workgroup (128 tokens)
 constexpr int kStageSteps = 4;    // K-steps per LDS stage
 constexpr int kRowTiles = 2;      // weight tiles per wave
@@ -345,14 +347,16 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   const int nt = (g.n + 15) >> 4;  // live token tiles
 
   // Token-fragment producer: thread t loads pieces (tile t/64, lane t%64) and
-  // (tile t/64 + 4, same lane) of every K-step of a stage.
+  // (tile t/64 + 4, same lane) of every K-step of a stage.  Tiles past the
+  // item's last token load its last row again (straight-line code; those
+  // fragments are never used).
   const int tid = threadIdx.x;
-  const int pl = tid & 63, pq = pl >> 4, pc = pl & 15, pct = tid >> 6;
+  const int pl = tid & 63, pq = pl >> 4, pc = pl & 15;
+  const int pct = __builtin_amdgcn_readfirstlane(tid >> 6);  // the wave (uniform)
   const int rows_b = kGateUp ? p.T : p.R;  // rows of the chunk-major source
   const bf16_t* src = kGateUp ? p.xk : p.hk;
   const int bstep = 32 * rows_b;
   const bf16_t* pb[2];
-  bool pl_live[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int ct = pct + 4 * h;
@@ -363,7 +367,6 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
     else
       row = g.r0 + col;
     pb[h] = src + (static_cast<size_t>(pq) * rows_b + row) * 8;
-    pl_live[h] = ct < nt;
   }
 
   __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 64 KiB
@@ -372,58 +375,74 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   for (int m = 0; m < kRowTiles; ++m)
 #pragma unroll
     for (int ct = 0; ct < kTileTok; ++ct) acc[m][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 a_cur[kStageSteps][kRowTiles], a_nxt[kStageSteps][kRowTiles], b_nxt[kStageSteps][2];
+  // Weights (from HBM) run two stages ahead in a three-slot register ring,
+  // token fragments (mostly from L2) one stage ahead through registers into
+  // the LDS double buffer.  Loads are issued tokens first, then weights, so
+  // waiting for the next stage's tokens never waits for the newest weights.
+  bf16x8 a_reg[3][kStageSteps][kRowTiles], b_nxt[kStageSteps][2];
 
-  auto load_stage = [&](int st) {
-#pragma unroll
-    for (int s = 0; s < kStageSteps; ++s) {
-      const int ks = st * kStageSteps + s;
-#pragma unroll
-      for (int m = 0; m < kRowTiles; ++m) a_nxt[s][m] = ld_bf16x8(pa + m * tstride + ks * kFrag);
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        if (pl_live[h]) b_nxt[s][h] = ld_bf16x8(pb[h] + ks * bstep);
-    }
-  };
-  auto store_stage = [&](int buf) {
+  auto load_a = [&](int st, bf16x8 (&a)[kStageSteps][kRowTiles]) {
 #pragma unroll
     for (int s = 0; s < kStageSteps; ++s)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-        if (pl_live[h]) stage[buf][s][pct + 4 * h][pl] = b_nxt[s][h];
+      for (int m = 0; m < kRowTiles; ++m) a[s][m] = ld_bf16x8(pa + m * tstride + (st * kStageSteps + s) * kFrag);
+  };
+  auto load_b = [&](int st) {
+#pragma unroll
+    for (int s = 0; s < kStageSteps; ++s)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) b_nxt[s][h] = ld_bf16x8(pb[h] + (st * kStageSteps + s) * bstep);
+  };
+  auto store_b = [&](int buf) {
+#pragma unroll
+    for (int s = 0; s < kStageSteps; ++s)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) stage[buf][s][pct + 4 * h][pl] = b_nxt[s][h];
   };
 
   const int nstages = ksteps / kStageSteps;
-  load_stage(0);
-  store_stage(0);
-#pragma unroll
-  for (int s = 0; s < kStageSteps; ++s)
-#pragma unroll
-    for (int m = 0; m < kRowTiles; ++m) a_cur[s][m] = a_nxt[s][m];
+  load_b(0);
+  load_a(0, a_reg[0]);
+  if (nstages > 1) load_a(1, a_reg[1]);
+  store_b(0);
   __syncthreads();
-  for (int st = 0; st < nstages; ++st) {
-    const int buf = st & 1;
+  // stage st uses ring slot R = st % 3 (a compile-time index: the loop runs
+  // three stages per trip)
+  auto run_stage = [&](auto slot, int st) {
+    constexpr int R = decltype(slot)::value;
     const bool more = st + 1 < nstages;
-    if (more) load_stage(st + 1);
+    if (more) load_b(st + 1);
+    __builtin_amdgcn_sched_barrier(0);  // tokens before weights
+    if (st + 2 < nstages) load_a(st + 2, a_reg[(R + 2) % 3]);
     __builtin_amdgcn_sched_barrier(0);
+    const int buf = st & 1;
+    // token tile by token tile: the next tile's fragments are read from LDS
+    // (always in bounds; tiles past nt are read but not used) while this
+    // tile's matrix instructions run.  Each accumulator still sums K in order.
+    bf16x8 bc[kStageSteps], bn[kStageSteps];
 #pragma unroll
-    for (int s = 0; s < kStageSteps; ++s)
+    for (int s = 0; s < kStageSteps; ++s) bc[s] = stage[buf][s][0][lane];
 #pragma unroll
-      for (int ct = 0; ct < kTileTok; ++ct)
-        if (ct < nt) {
-          const bf16x8 b = stage[buf][s][ct][lane];
+    for (int ct = 0; ct < kTileTok; ++ct) {
+      if (ct + 1 < kTileTok)
+#pragma unroll
+        for (int s = 0; s < kStageSteps; ++s) bn[s] = stage[buf][s][ct + 1][lane];
+      if (ct < nt)
+#pragma unroll
+        for (int s = 0; s < kStageSteps; ++s)
 #pragma unroll
           for (int m = 0; m < kRowTiles; ++m)
-            acc[m][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur[s][m], b, acc[m][ct], 0, 0, 0);
-        }
-    if (more) {
-      store_stage(buf ^ 1);
+            acc[m][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_reg[R][s][m], bc[s], acc[m][ct], 0, 0, 0);
 #pragma unroll
-      for (int s = 0; s < kStageSteps; ++s)
-#pragma unroll
-        for (int m = 0; m < kRowTiles; ++m) a_cur[s][m] = a_nxt[s][m];
+      for (int s = 0; s < kStageSteps; ++s) bc[s] = bn[s];
     }
+    if (more) store_b(buf ^ 1);
     __syncthreads();
+  };
+  for (int st = 0; st < nstages; st += 3) {
+    run_stage(std::integral_constant<int, 0>{}, st);
+    if (st + 1 < nstages) run_stage(std::integral_constant<int, 1>{}, st + 1);
+    if (st + 2 < nstages) run_stage(std::integral_constant<int, 2>{}, st + 2);
   }
 
   const int q = lane >> 4, c = lane & 15;
