@@ -306,6 +306,10 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  *   shared_out[t][:] = Ws_down (silu(Ws_gate x_t) * (Ws_up x_t))
  * Each selected expert's weights are streamed once per call.
  * x_chunked: the hidden states x [T][H] in the chunk-major layout above.
+ * x: the same hidden states row-major [T][H], optional (NULL: not used).
+ * With it, bf16 rows whose tokens are not consecutive (token-level routing)
+ * are read from x, one 64-byte piece per token and reduction step, instead
+ * of four 16-byte chunks of x_chunked; results are identical either way.
  * w13, w2: all E routed experts packed by dmoe_pack_expert_weights (I);
  * ws13, ws2: the shared expert packed the same way (n_experts = 1, I = I_s),
  * both NULL with I_s == 0 or both set with I_s > 0.  All of type dt.
@@ -323,10 +327,10 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  * DMOE_BF16: H % 128 == 0, I % 128 == 0, I_s % 128 == 0 (matrix-core tiles).
  * DMOE_F32: any I, I_s >= 1.
  */
-dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* w2, const void* ws13,
-                            const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
-                            int max_work, dmoe_schedule sched, float* slot_out, float* shared_out,
-                            void* workspace, size_t ws_bytes, void* stream);
+dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w13, const void* w2,
+                            const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
+                            int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
+                            float* shared_out, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn): for every

@@ -330,10 +330,10 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
   return dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
 }
 
-dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* w2, const void* ws13,
-                            const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
-                            int max_work, dmoe_schedule sched, float* slot_out, float* shared_out,
-                            void* workspace, size_t ws_bytes, void* stream) {
+dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w13, const void* w2,
+                            const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
+                            int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
+                            float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
   REQUIRE(x_chunked && w13 && w2 && slot_out && workspace,
           "x_chunked, w13, w2, slot_out and workspace must not be NULL");
   REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
@@ -357,6 +357,7 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
   const size_t need = dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
   REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
   ALIGNED(x_chunked);
+  ALIGNED(x);
   ALIGNED(w13);
   ALIGNED(w2);
   ALIGNED(sched.n_work);
@@ -373,7 +374,7 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* w13, const void* 
     SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
             "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
   }
-  dmoe::FfnArgs a{x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
+  dmoe::FfnArgs a{x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
                   sched, slot_out, shared_out, workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }
@@ -405,7 +406,7 @@ dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, cons
             "bf16 experts need H and I_s to be multiples of 128 (H=%d, I_s=%d)", H, I_s);
   }
   const dmoe_schedule none{};
-  dmoe::FfnArgs a{x_chunked, nullptr, nullptr, ws13, ws2, T, H, 1, 0, I_s, 0, 0, none, nullptr, shared_out,
+  dmoe::FfnArgs a{x_chunked, nullptr, nullptr, nullptr, ws13, ws2, T, H, 1, 0, I_s, 0, 0, none, nullptr, shared_out,
                   workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }

@@ -111,6 +111,7 @@ hipError_t launch_pack_activations(const void* x, dmoe_dtype dt, int T, int H, v
 
 struct FfnArgs {
   const void* x;     // activations, chunk-major [H/c][T][c]
+  const void* xr;    // the same activations row-major [T][H], or nullptr
   const void* w13;   // packed routed gate/up weights
   const void* w2;    // packed routed down weights
   const void* ws13;  // packed shared-expert gate/up (or nullptr)

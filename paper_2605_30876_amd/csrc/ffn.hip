@@ -83,8 +83,25 @@ __device__ __forceinline__ bool decode_item(int y, int shared_items, int max_wor
 
 // ---- bf16 kernels ----------------------------------------------------------
 
+// Which copy of x serves a token tile's B loads better.  Lane (q, c) of
+// each 16-lane row holds the token of column c (ascending within an item).
+// Per K-step the chunk-major copy touches 4 * D8 cache lines (D8: distinct
+// groups of 8 consecutive tokens among the 16; one group per line and chunk),
+// the row-major copy D lines (D: distinct tokens, one 64-byte piece each).
+// Tiles of fewer than 4 distinct tokens stay chunk-major (measured slightly
+// faster there: 32-token decode steps under token routing).  Wave-uniform.
+__device__ __forceinline__ bool tile_gathered(int tok) {
+  // token of lane c - 1 in the same row (lane c = 0 sees its own)
+  const int prev = __builtin_amdgcn_update_dpp(tok, tok, 0x111, 0xF, 0xF, false);  // row_shr:1
+  const uint32_t new_tok = static_cast<uint32_t>(__builtin_amdgcn_ballot_w64(tok != prev)) & 0xFFFFu;
+  const uint32_t new_grp = static_cast<uint32_t>(__builtin_amdgcn_ballot_w64((tok >> 3) != (prev >> 3))) & 0xFFFFu;
+  const int d = 1 + __builtin_popcount(new_tok), d8 = 1 + __builtin_popcount(new_grp);
+  return d >= 4 && d < 4 * d8;
+}
+
 struct FfnParams {
   const bf16_t* xk;    // activations, chunk-major [H/8][T][8]
+  const bf16_t* xr;    // the same row-major [T][H] (gathered rows read it), or nullptr
   const bf16_t* w13;   // routed gate/up, fragment-packed
   const bf16_t* w2;    // routed down, fragment-packed
   const bf16_t* ws13;  // shared gate/up, fragment-packed
@@ -224,15 +241,21 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
   WaveOps<NT, KMAX, BC> w;  // a one-burst weight slice stays here across passes
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
     const bf16_t* pb[NT];
+    int tok[NT];
+    bool gathered = false;
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
       const int col = min(p0 + ct * 16 + c, g.n - 1);
-      const int tok = g.tok ? g.tok[col] : g.t0 + col;
-      pb[ct] = p.xk + (static_cast<size_t>(chunk0) * p.T + tok) * 8;
+      tok[ct] = g.tok ? g.tok[col] : g.t0 + col;
+      if (p.xr && g.tok) gathered |= tile_gathered(tok[ct]);
     }
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct)
+      pb[ct] = gathered ? p.xr + static_cast<size_t>(tok[ct]) * H + chunk0 * 8
+                        : p.xk + (static_cast<size_t>(chunk0) * p.T + tok[ct]) * 8;
     f32x4 acc[NT];
     zero(acc);
-    wave_dot(w, pa, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
+    wave_dot(w, pa, pb, gathered ? 32 : bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -355,19 +378,25 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   const int pct = __builtin_amdgcn_readfirstlane(tid >> 6);  // the wave (uniform)
   const int rows_b = kGateUp ? p.T : p.R;  // rows of the chunk-major source
   const bf16_t* src = kGateUp ? p.xk : p.hk;
-  const int bstep = 32 * rows_b;
   const bf16_t* pb[2];
+  int row[2];
+  bool gathered = false;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int ct = pct + 4 * h;
     const int col = min(ct * 16 + pc, g.n - 1);
-    int row;
-    if (kGateUp)
-      row = g.tok ? g.tok[col] : g.t0 + col;
-    else
-      row = g.r0 + col;
-    pb[h] = src + (static_cast<size_t>(pq) * rows_b + row) * 8;
+    if (kGateUp) {
+      row[h] = g.tok ? g.tok[col] : g.t0 + col;
+      if (p.xr && g.tok) gathered |= tile_gathered(row[h]);
+    } else {
+      row[h] = g.r0 + col;
+    }
   }
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    pb[h] = gathered ? p.xr + static_cast<size_t>(row[h]) * H + pq * 8
+                     : src + (static_cast<size_t>(pq) * rows_b + row[h]) * 8;
+  const int bstep = gathered ? 32 : 32 * rows_b;
 
   __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 64 KiB
   f32x4 acc[kRowTiles][kTileTok];
@@ -702,8 +731,9 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
   const int shared_items = a.I_s > 0 ? (a.T + DMOE_WORK_ROWS - 1) / DMOE_WORK_ROWS : 0;
   const int items = a.max_work + shared_items;
   if (dt == DMOE_BF16) {
-    FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w13),
-                static_cast<const bf16_t*>(a.w2), static_cast<const bf16_t*>(a.ws13),
+    FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.xr),
+                static_cast<const bf16_t*>(a.w13), static_cast<const bf16_t*>(a.w2),
+                static_cast<const bf16_t*>(a.ws13),
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
                 a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};

@@ -89,6 +89,7 @@ class MoELayer:
         rbytes = lib.dmoe_router_workspace_size(T, H, E, dt)
         self.router_ws = torch.empty((rbytes,), dtype=torch.uint8, device=device) if rbytes else None
         self.overlap_shared = overlap_shared and I_s > 0
+        self._x = None  # hidden states of the last route() call
         nbytes = lib.dmoe_ffn_workspace_size(T, I, 0 if self.overlap_shared else I_s, k, dt)
         self.workspace = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=device)
         if self.overlap_shared:
@@ -108,6 +109,7 @@ class MoELayer:
         the separate entry points; both give identical results.  "topp" runs
         the router, dmoe_block_topp_route and a token-level schedule."""
         T, H, E, k = self.T, self.H, self.E, self.k
+        self._x = x  # the expert FFN reads gathered token rows from the row-major x
         if routing not in ("block", "token", "topp"):
             raise ValueError(f"routing must be 'block', 'token' or 'topp', not {routing!r}")
         if fused and routing == "block":
@@ -138,7 +140,7 @@ class MoELayer:
 
     def _routed_ffn(self, w: dict, routing: str, stream):
         shared = not self.overlap_shared and self.I_s > 0
-        lib.dmoe_expert_ffn(self.x_chunked, w["w13"], w["w2"], w.get("ws13") if shared else None,
+        lib.dmoe_expert_ffn(self.x_chunked, self._x, w["w13"], w["w2"], w.get("ws13") if shared else None,
                             w.get("ws2") if shared else None, self.T, self.H, self.E, self.I,
                             self.I_s if shared else 0, self.k, self.max_work(routing), self.sched, self.slot_out,
                             self.shared_out if shared else None, self.workspace, stream)

@@ -70,7 +70,7 @@ _SIGS = {
     "dmoe_pack_activations": ([_P, _I, _I, _I, _P, _P], _I),
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
-    "dmoe_expert_ffn": ([_P] * 5 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
+    "dmoe_expert_ffn": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
     "dmoe_shared_ffn_workspace_size": ([_I, _I, _I], _S),
     "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
@@ -245,9 +245,10 @@ def dmoe_shared_expert_ffn(x_chunked, ws13, ws2, T, H, I_s, shared_out, workspac
                                          workspace.numel() * workspace.element_size(), stream_handle(stream)))
 
 
-def dmoe_expert_ffn(x_chunked, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work, sched: Schedule,
+def dmoe_expert_ffn(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work, sched: Schedule,
                     slot_out, shared_out, workspace, stream=None):
-    _check(load().dmoe_expert_ffn(ptr(x_chunked), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
+    """x: the row-major hidden states (or None); gathered token rows are read from it."""
+    _check(load().dmoe_expert_ffn(ptr(x_chunked), ptr(x), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
                                   dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
                                   ptr(slot_out), ptr(shared_out), ptr(workspace),
                                   workspace.numel() * workspace.element_size(), stream_handle(stream)))

@@ -113,10 +113,10 @@ def test_schedule_validation(L, buf):
 
 
 def _ffn(L, p, **over):
-    a = dict(x=p, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512, k=8,
+    a = dict(x=p, xr=p, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512, k=8,
              max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, shared=p, ws=p, ws_bytes=1 << 30)
     a.update(over)
-    return status(L, "dmoe_expert_ffn", a["x"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"], a["T"],
+    return status(L, "dmoe_expert_ffn", a["x"], a["xr"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"], a["T"],
                   a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"],
                   a["shared"], a["ws"], a["ws_bytes"], None)
 
@@ -125,6 +125,7 @@ def test_ffn_validation(L, buf):
     _, p = buf
     INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
     assert _ffn(L, p, x=None)[0] == INV
+    assert _ffn(L, p, xr=p + 4)[0] == INV            # the optional row-major copy must be aligned too
     assert _ffn(L, p, w13=None)[0] == INV
     assert _ffn(L, p, ws=None)[0] == INV
     assert _ffn(L, p, dt=5)[0] == INV
