@@ -210,7 +210,6 @@ def main():
             "expert_ffn_us": round(ffn_us, 3),
             "expert_ffn_gbps": round(ffn_bytes / (ffn_us * 1e-6) / 1e9, 1),
             "expert_ffn_bytes": int(ffn_bytes),
-            "expert_ffn_includes_combine": layers[0][2].fused(routing),
         }
         log(f"[bench] {routing}: {us:.2f} us/step (events {gpu_s / steps * 1e6:.2f}), U={U:.1f}, "
             f"{results[routing]['hbm_gbps']} GB/s layer; expert FFN {ffn_us:.2f} us = "
@@ -251,8 +250,7 @@ def main():
                                f"SwiGLU intermediate {cfg.I} + shared {cfg.I_s}, top-{cfg.k}, "
                                f"{cfg.NB} sequence(s) x block {cfg.bs} = {cfg.T} tokens per forward",
                    "routing": main_mode, "layers_rotated": NL, "graph": not args.no_graph},
-        "roofline": {"bound": "hbm", "kernel": FFN_KERNEL_FUSED if r.get("expert_ffn_includes_combine")
-                     else "expert FFN (gate/up+SwiGLU and down launches)",
+        "roofline": {"bound": "hbm", "kernel": "expert FFN (gate/up+SwiGLU and down launches)",
                      "achieved": r["expert_ffn_gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(r["expert_ffn_gbps"] / PEAK_HBM_GBPS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
@@ -264,10 +262,6 @@ def main():
         out["token_over_block_time"] = round(results["token"]["us_per_step"] / results["block"]["us_per_step"], 3)
     print(json.dumps(out))
     return 0
-
-
-FFN_KERNEL_FUSED = ("expert FFN + combine of one block (gate/up+SwiGLU launch, then the down projection of "
-                    "all experts weighted and summed into y)")
 
 
 def graph_timer(torch, NL: int):

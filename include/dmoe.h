@@ -22,8 +22,6 @@
  *                              rows, plus the always-on shared expert
  *   dmoe_shared_expert_ffn     the shared expert alone (to overlap it with
  *                              the routing of the same forward)
- *   dmoe_expert_ffn_block_combine  expert FFN and combine of one block-routed
- *                              block in one call (y directly)
  *   dmoe_combine               y_t = sum_j w[t,j] * FFN_{e_tj}(x_t) + FFN_s(x_t)
  *
  * dmoe_route_block / dmoe_route_token run the first three (or the token
@@ -333,30 +331,6 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w1
                             const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
                             int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
                             float* shared_out, void* workspace, size_t ws_bytes, void* stream);
-
-/*
- * Expert execution and combine of ONE block under block routing (Sec. 4.2,
- * Alg. 1 with |C| = k; every token of the forward uses the block's k
- * experts), in one call:
- *   y[t][:] = sum_j combine_w[t][j] * FFN_{block_experts[j]}(x_t) + FFN_s(x_t)
- * the result of dmoe_expert_ffn followed by dmoe_combine, up to the fp32
- * summation order (each expert's down projection is weighted per reduction
- * slice before the slices are summed).  Two launches instead of three: the
- * down projection of all k + 1 experts and the weighted sum run together, so
- * slot_out and shared_out are neither needed nor written.
- * block_experts [k] int32: the block's experts (dmoe_block_aggregate_topk or
- * dmoe_route_block with n_blocks = 1); sched: the schedule built from them
- * (n_groups = 1, group_size = T); combine_w [T][k] float32; y [T][H] of
- * type y_dt.  The other arguments are those of dmoe_expert_ffn (workspace:
- * dmoe_ffn_workspace_size bytes).
- * Limits: those of dmoe_expert_ffn, and DMOE_BF16, T <= 64, k <= 8,
- * I <= 512, I_s <= 512 (DMOE_ERR_UNSUPPORTED otherwise).
- */
-dmoe_status dmoe_expert_ffn_block_combine(const void* x_chunked, const void* x, const void* w13, const void* w2,
-                                          const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H,
-                                          int E, int I, int I_s, int k, int max_work, dmoe_schedule sched,
-                                          const int32_t* block_experts, const float* combine_w, dmoe_dtype y_dt,
-                                          void* y, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn): for every

@@ -16,8 +16,10 @@ __device__ __forceinline__ void store4(bf16_t* dst, const f32x4& v) {
   *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
 }
 
+constexpr int kCombineThreads = 64;  // small workgroups spread a decode step's combine over more CUs
+
 template <typename OutT>
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ slot_out,
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(const float* __restrict__ slot_out,
                                                       const float* __restrict__ w,
                                                       const float* __restrict__ shared_out, int T,
                                                       int H, int k, OutT* __restrict__ y) {
@@ -53,11 +55,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
                           dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s) {
   const size_t n = static_cast<size_t>(T) * (H >> 2);
-  const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
+  const unsigned blocks = static_cast<unsigned>((n + kCombineThreads - 1) / kCombineThreads);
   if (dt == DMOE_BF16)
-    combine_kernel<bf16_t><<<blocks, 256, 0, s>>>(slot_out, w, shared_out, T, H, k, static_cast<bf16_t*>(y));
+    combine_kernel<bf16_t>
+        <<<blocks, kCombineThreads, 0, s>>>(slot_out, w, shared_out, T, H, k, static_cast<bf16_t*>(y));
   else
-    combine_kernel<float><<<blocks, 256, 0, s>>>(slot_out, w, shared_out, T, H, k, static_cast<float*>(y));
+    combine_kernel<float><<<blocks, kCombineThreads, 0, s>>>(slot_out, w, shared_out, T, H, k, static_cast<float*>(y));
   return hipGetLastError();
 }
 

@@ -50,68 +50,6 @@ constexpr long kIntLimit = 0x7fffffffL;
   } while (0)
 #define ALIGNED(p) REQUIRE(!misaligned(p), #p " is not 16-byte aligned")
 
-#define REQUIRE_FN(cond, ...)                                    \
-  do {                                                           \
-    if (!(cond)) return fail(DMOE_ERR_INVALID_ARG, fn, __VA_ARGS__); \
-  } while (0)
-#define SUPPORT_FN(cond, ...)                                    \
-  do {                                                           \
-    if (!(cond)) return fail(DMOE_ERR_UNSUPPORTED, fn, __VA_ARGS__); \
-  } while (0)
-#define ALIGNED_FN(p) REQUIRE_FN(!misaligned(p), #p " is not 16-byte aligned")
-
-// Arguments of dmoe_expert_ffn, shared with dmoe_expert_ffn_block_combine
-// (fn names the entry point in the error message; outputs: slot_out and
-// shared_out are written, so they are checked).
-dmoe_status check_expert_ffn(const char* fn, const void* x_chunked, const void* x, const void* w13,
-                             const void* w2, const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H,
-                             int E, int I, int I_s, int k, int max_work, const dmoe_schedule& sched,
-                             const float* slot_out, const float* shared_out, const void* workspace,
-                             size_t ws_bytes, bool outputs) {
-  REQUIRE_FN(x_chunked && w13 && w2 && (slot_out || !outputs) && workspace,
-             "x_chunked, w13, w2, slot_out and workspace must not be NULL");
-  REQUIRE_FN(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
-                 sched.work,
-             "every schedule array must be set");
-  REQUIRE_FN(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
-  REQUIRE_FN(T >= 1 && H >= 1 && I >= 1 && I_s >= 0, "T=%d, H=%d, I=%d must be >= 1 and I_s=%d >= 0",
-             T, H, I, I_s);
-  REQUIRE_FN(E >= 1, "E=%d must be >= 1", E);
-  REQUIRE_FN(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
-  REQUIRE_FN(max_work >= 1 && static_cast<long>(max_work) <= static_cast<long>(T) * k,
-             "max_work=%d must be in [1, T*k]", max_work);
-  REQUIRE_FN(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
-  const bool shared = I_s > 0;
-  REQUIRE_FN(shared == (ws13 != nullptr) && shared == (ws2 != nullptr) &&
-                 (!outputs || shared == (shared_out != nullptr)),
-             "ws13, ws2 and shared_out must all be set iff I_s > 0");
-  const long rows = static_cast<long>(T) * k + (shared ? T : 0);
-  REQUIRE_FN(rows < kIntLimit && rows * (I > I_s ? I : I_s) <= kIntLimit && static_cast<long>(T) * H <= kIntLimit &&
-                 static_cast<long>(T) * k * H <= kIntLimit * 4L,
-             "T*k*H, T*H or the SwiGLU buffer is too large");
-  const size_t need = dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
-  REQUIRE_FN(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
-  ALIGNED_FN(x_chunked);
-  ALIGNED_FN(x);
-  ALIGNED_FN(w13);
-  ALIGNED_FN(w2);
-  ALIGNED_FN(sched.n_work);
-  ALIGNED_FN(sched.work);
-  ALIGNED_FN(sched.row_token);
-  ALIGNED_FN(sched.row_slot);
-  ALIGNED_FN(ws13);
-  ALIGNED_FN(ws2);
-  ALIGNED_FN(slot_out);
-  ALIGNED_FN(shared_out);
-  ALIGNED_FN(workspace);
-  SUPPORT_FN(E <= kMaxScheduleE, "E <= %d is supported (E=%d)", kMaxScheduleE, E);
-  if (dt == DMOE_BF16) {
-    SUPPORT_FN(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
-            "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
-  }
-  return DMOE_OK;
-}
-
 }  // namespace
 
 extern "C" {
@@ -396,34 +334,49 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w1
                             const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
                             int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
                             float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
-  const dmoe_status st = check_expert_ffn(__func__, x_chunked, x, w13, w2, ws13, ws2, dt, T, H, E, I, I_s, k,
-                                          max_work, sched, slot_out, shared_out, workspace, ws_bytes, true);
-  if (st != DMOE_OK) return st;
+  REQUIRE(x_chunked && w13 && w2 && slot_out && workspace,
+          "x_chunked, w13, w2, slot_out and workspace must not be NULL");
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
+          "every schedule array must be set");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(T >= 1 && H >= 1 && I >= 1 && I_s >= 0, "T=%d, H=%d, I=%d must be >= 1 and I_s=%d >= 0",
+          T, H, I, I_s);
+  REQUIRE(E >= 1, "E=%d must be >= 1", E);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(max_work >= 1 && static_cast<long>(max_work) <= static_cast<long>(T) * k,
+          "max_work=%d must be in [1, T*k]", max_work);
+  REQUIRE(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
+  const bool shared = I_s > 0;
+  REQUIRE(shared == (ws13 != nullptr) && shared == (ws2 != nullptr) && shared == (shared_out != nullptr),
+          "ws13, ws2 and shared_out must all be set iff I_s > 0");
+  const long rows = static_cast<long>(T) * k + (shared ? T : 0);
+  REQUIRE(rows < kIntLimit && rows * (I > I_s ? I : I_s) <= kIntLimit && static_cast<long>(T) * H <= kIntLimit &&
+              static_cast<long>(T) * k * H <= kIntLimit * 4L,
+          "T*k*H, T*H or the SwiGLU buffer is too large");
+  const size_t need = dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
+  REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
+  ALIGNED(x_chunked);
+  ALIGNED(x);
+  ALIGNED(w13);
+  ALIGNED(w2);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
+  ALIGNED(ws13);
+  ALIGNED(ws2);
+  ALIGNED(slot_out);
+  ALIGNED(shared_out);
+  ALIGNED(workspace);
+  SUPPORT(E <= kMaxScheduleE, "E <= %d is supported (E=%d)", kMaxScheduleE, E);
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
+            "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
+  }
   dmoe::FfnArgs a{x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
                   sched, slot_out, shared_out, workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
-}
-
-dmoe_status dmoe_expert_ffn_block_combine(const void* x_chunked, const void* x, const void* w13, const void* w2,
-                                          const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H,
-                                          int E, int I, int I_s, int k, int max_work, dmoe_schedule sched,
-                                          const int32_t* block_experts, const float* combine_w, dmoe_dtype y_dt,
-                                          void* y, void* workspace, size_t ws_bytes, void* stream) {
-  REQUIRE(block_experts && combine_w && y, "block_experts, combine_w and y must not be NULL");
-  REQUIRE(valid_dtype(y_dt), "unknown y dtype %d", static_cast<int>(y_dt));
-  ALIGNED(combine_w);
-  ALIGNED(y);
-  const dmoe_status st = check_expert_ffn(__func__, x_chunked, x, w13, w2, ws13, ws2, dt, T, H, E, I, I_s, k,
-                                          max_work, sched, nullptr, nullptr, workspace, ws_bytes, false);
-  if (st != DMOE_OK) return st;
-  SUPPORT(dmoe::block_combine_supported(T, I, I_s, k, dt),
-          "one fused block needs DMOE_BF16, T <= 64, k <= 8 and I, I_s <= 512 (T=%d, k=%d, I=%d, I_s=%d)", T, k,
-          I, I_s);
-  dmoe::FfnArgs a{x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
-                  sched, nullptr, nullptr, workspace};
-  return hip_status(
-      dmoe::launch_ffn_block_combine(a, block_experts, combine_w, y_dt, y, static_cast<hipStream_t>(stream)),
-      __func__);
 }
 
 size_t dmoe_shared_ffn_workspace_size(int T, int I_s, dmoe_dtype dt) {

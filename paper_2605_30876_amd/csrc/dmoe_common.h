@@ -123,10 +123,6 @@ struct FfnArgs {
   void* workspace;  // SwiGLU activations of T*k (+ T) rows, max(I, I_s) wide, storage type
 };
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
-// Expert FFN and combine of one block under block routing (bf16): y directly.
-bool block_combine_supported(int T, int I, int I_s, int k, dmoe_dtype dt);
-hipError_t launch_ffn_block_combine(const FfnArgs& a, const int* experts, const float* combine_w,
-                                    dmoe_dtype y_dt, void* y, hipStream_t s);
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
 long schedule_max_work(long n_groups, long group_size, long k, long E);
 size_t schedule_scratch_ints(long n_groups, long k, long E);

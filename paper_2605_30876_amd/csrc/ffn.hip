@@ -504,108 +504,6 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   }
 }
 
-// ---- down projection and combine of one block-routed block ----------------
-//
-// Under block routing with one block every token uses the same k experts, so
-// one workgroup can apply all of them: workgroup (jt, ct) owns output
-// features 16*jt .. 16*jt+15 of the 16 tokens of token tile ct.  Its 16 waves
-// split the reduction (wave w: K-step w of every expert, I <= 512); each wave
-// loads the packed down tile slice and the h fragment of all k routed experts
-// and of the shared expert at once (k and the shared expert are template
-// parameters, so the loads are straight-line code), multiplies each expert's partial tile by
-// the token's combine weight (1 for the shared expert) and adds it to one
-// accumulator.  The 16 partial accumulators are summed in wave order through
-// LDS and written to y: no per-slot outputs, no separate combine launch.
-constexpr int kDcWaves = 16;
-constexpr int kDcMaxK = 8;  // routed experts per block (+ the shared expert)
-
-struct DcParams {
-  const bf16_t* w2;
-  const bf16_t* ws2;
-  const bf16_t* hk;      // SwiGLU activations, chunk-major [ldh/8][R][8]
-  const int* experts;    // the block's k experts
-  const float* cw;       // combine weights [T][k]
-  int T, H, E, I, I_s, k, R, Tk;
-  void* y;
-};
-
-__device__ __forceinline__ void store_out4(float* dst, const f32x4& v) { *reinterpret_cast<f32x4*>(dst) = v; }
-__device__ __forceinline__ void store_out4(bf16_t* dst, const f32x4& v) {
-  const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-  const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-  *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
-}
-
-template <int KE, bool kShared, typename OutT>
-__global__ __launch_bounds__(kDcWaves * kWave) void ffn_down_combine_bf16_kernel(DcParams p) {
-  const int jt = blockIdx.x, ct = blockIdx.y;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
-  const int H = p.H, T = p.T;
-  const int t = min(ct * 16 + c, T - 1);  // this lane's token (clamped; stored only if in range)
-  const int steps = p.I >> 5, steps_s = p.I_s >> 5;
-  // K-step of this wave (waves past an expert's K-steps load a valid step
-  // and drop its product)
-  const int s = min(wave, steps - 1), s_s = kShared ? min(wave, steps_s - 1) : 0;
-  bf16x8 a[KE + 1], b[KE + 1];
-  float wt[KE];
-#pragma unroll
-  for (int j = 0; j < KE; ++j) {
-    const int e = min(max(p.experts[j], 0), p.E - 1);
-    // h rows of expert e: the schedule of one block gives the u-th smallest
-    // selected expert rows u*T .. u*T+T-1
-    int rank = 0;
-#pragma unroll
-    for (int i = 0; i < KE; ++i) rank += p.experts[i] < p.experts[j];
-    a[j] = ld_bf16x8(p.w2 + static_cast<size_t>(e) * H * p.I + (static_cast<size_t>(jt) * steps + s) * kFrag +
-                     lane * 8);
-    b[j] = ld_bf16x8(p.hk + (static_cast<size_t>(4 * s + q) * p.R + rank * T + t) * 8);
-    wt[j] = p.cw[static_cast<size_t>(t) * KE + j];
-  }
-  if constexpr (kShared) {
-    a[KE] = ld_bf16x8(p.ws2 + (static_cast<size_t>(jt) * steps_s + s_s) * kFrag + lane * 8);
-    b[KE] = ld_bf16x8(p.hk + (static_cast<size_t>(4 * s_s + q) * p.R + p.Tk + t) * 8);
-  }
-  __builtin_amdgcn_sched_barrier(0);  // every load is in flight before the first product
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (wave < steps) {
-#pragma unroll
-    for (int j = 0; j < KE; ++j) {
-      const f32x4 part = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], b[j], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-      acc += wt[j] * part;  // slot order
-    }
-  }
-  if constexpr (kShared)
-    if (wave < steps_s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[KE], b[KE], acc, 0, 0, 0);
-
-  __shared__ f32x4 red[kDcWaves][kWave];
-  red[wave][lane] = acc;
-  __syncthreads();
-  if (wave == 0) {
-    f32x4 v = red[0][lane];
-#pragma unroll
-    for (int w = 1; w < kDcWaves; ++w) v += red[w][lane];
-    if (ct * 16 + c < T)
-      store_out4(static_cast<OutT*>(p.y) + static_cast<size_t>(ct * 16 + c) * H + jt * 16 + 4 * q, v);
-  }
-}
-
-template <int KE, bool kShared>
-void launch_down_combine(const DcParams& d, dmoe_dtype y_dt, dim3 grid, hipStream_t s) {
-  if (y_dt == DMOE_F32)
-    ffn_down_combine_bf16_kernel<KE, kShared, float><<<grid, kDcWaves * kWave, 0, s>>>(d);
-  else
-    ffn_down_combine_bf16_kernel<KE, kShared, bf16_t><<<grid, kDcWaves * kWave, 0, s>>>(d);
-}
-
-template <int KE>
-void launch_down_combine_k(const DcParams& d, dmoe_dtype y_dt, dim3 grid, hipStream_t s) {
-  if (d.I_s > 0)
-    launch_down_combine<KE, true>(d, y_dt, grid, s);
-  else
-    launch_down_combine<KE, false>(d, y_dt, grid, s);
-}
-
 // ---- f32 path -------------------------------------------------------------
 //
 // Weights are reduction-major (w13[e][h][u], w2[e][i][j]), so the 64 lanes of
@@ -782,17 +680,11 @@ struct Shape<4> {
 };
 
 template <int NT>
-hipError_t launch_gateup_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
+hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   using S = Shape<NT>;
   ffn_gateup_bf16_kernel<NT, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst>
       <<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
-  return hipGetLastError();
-}
-
-template <int NT>
-hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
-  using S = Shape<NT>;
-  hipError_t err = launch_gateup_bf16<NT>(p, ldh, groups, s);
+  hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_down_bf16_kernel<NT, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst>
       <<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
@@ -825,47 +717,6 @@ bool use_tile_kernels(int T, int k, int max_work, int items, int ldh) {
 }
 
 }  // namespace
-
-bool block_combine_supported(int T, int I, int I_s, int k, dmoe_dtype dt) {
-  return dt == DMOE_BF16 && T >= 1 && T <= 64 && k >= 1 && k <= kDcMaxK && I <= 32 * kDcWaves &&
-         I_s <= 32 * kDcWaves;
-}
-
-hipError_t launch_ffn_block_combine(const FfnArgs& a, const int* experts, const float* combine_w,
-                                    dmoe_dtype y_dt, void* y, hipStream_t s) {
-  const int Tk = a.T * a.k;
-  const int R = Tk + (a.I_s > 0 ? a.T : 0);
-  const int ldh = std::max(a.I, a.I_s);
-  const int shared_items = a.I_s > 0 ? (a.T + DMOE_WORK_ROWS - 1) / DMOE_WORK_ROWS : 0;
-  const int items = a.max_work + shared_items;
-  FfnParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.xr),
-              static_cast<const bf16_t*>(a.w13), static_cast<const bf16_t*>(a.w2),
-              static_cast<const bf16_t*>(a.ws13), static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work,
-              a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
-              static_cast<bf16_t*>(a.workspace), nullptr, nullptr};
-  hipError_t err;
-  switch (pick_ntiles(a.T, a.k, a.max_work)) {
-    case 1: err = launch_gateup_bf16<1>(p, ldh, items, s); break;
-    case 2: err = launch_gateup_bf16<2>(p, ldh, items, s); break;
-    default: err = launch_gateup_bf16<4>(p, ldh, items, s); break;
-  }
-  if (err != hipSuccess) return err;
-  DcParams d{static_cast<const bf16_t*>(a.w2), static_cast<const bf16_t*>(a.ws2),
-             static_cast<const bf16_t*>(a.workspace), experts, combine_w, a.T, a.H, a.E, a.I, a.I_s, a.k, R, Tk,
-             y};
-  const dim3 grid(a.H / 16, (a.T + 15) / 16);
-  switch (a.k) {
-    case 1: launch_down_combine_k<1>(d, y_dt, grid, s); break;
-    case 2: launch_down_combine_k<2>(d, y_dt, grid, s); break;
-    case 3: launch_down_combine_k<3>(d, y_dt, grid, s); break;
-    case 4: launch_down_combine_k<4>(d, y_dt, grid, s); break;
-    case 5: launch_down_combine_k<5>(d, y_dt, grid, s); break;
-    case 6: launch_down_combine_k<6>(d, y_dt, grid, s); break;
-    case 7: launch_down_combine_k<7>(d, y_dt, grid, s); break;
-    default: launch_down_combine_k<8>(d, y_dt, grid, s); break;
-  }
-  return hipGetLastError();
-}
 
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt) {
   const size_t rows = static_cast<size_t>(T) * k + (I_s > 0 ? T : 0);

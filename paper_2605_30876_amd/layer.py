@@ -6,8 +6,7 @@
     -> dmoe_build_expert_schedule -> dmoe_expert_ffn -> dmoe_combine
 
 on the current stream (the routing steps as one dmoe_route_block /
-dmoe_route_token call by default; a block-routed forward of one block runs
-the expert FFN and the combine as one dmoe_expert_ffn_block_combine call).  It allocates only in its constructor, so a forward
+dmoe_route_token call by default).  It allocates only in its constructor, so a forward
 can be captured in a HIP graph.  Nothing is computed on the host.
 
 Expert weights are used in the library's packed layout: :func:`pack_weights`
@@ -47,7 +46,7 @@ class MoELayer:
     def __init__(self, H: int, E: int, I: int, I_s: int, k: int, n_blocks: int, block_size: int,
                  dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False,
                  out_dtype: torch.dtype = torch.float32, top_p: float = 0.6, min_coreset: int | None = None,
-                 overlap_shared: bool = False, fuse_block_combine: bool = True):
+                 overlap_shared: bool = False):
         """Routing modes: "block" (block top-k), "token" (token top-k, the
         baseline) and "topp" (Alg. 1: a Top-P coreset per block with mass
         ``top_p`` and at least ``min_coreset`` (default k) experts, each token's
@@ -58,11 +57,7 @@ class MoELayer:
         the results are those of the single dmoe_expert_ffn call up to the
         fp32 summation order of the shared expert.  Off
         by default: replayed from a HIP graph, the two-stream forward of a
-        32-token decode step is slower (53 vs 40 us) than the one-stream one.
-
-        fuse_block_combine: block routing of a single block (n_blocks == 1)
-        writes y with dmoe_expert_ffn_block_combine (bf16, T <= 64, k <= 8,
-        I and I_s <= 512; slot_out and shared_out are then not written)."""
+        32-token decode step is slower (53 vs 40 us) than the one-stream one."""
         self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
         self.NB, self.bs = n_blocks, block_size
         self.T = T = n_blocks * block_size
@@ -104,8 +99,6 @@ class MoELayer:
             self._side = torch.cuda.Stream(device=device)
         # The layer output is accumulated in fp32; it is stored as out_dtype.
         self.y = torch.empty((T, H), dtype=out_dtype, device=device)
-        self.fuse_block_combine = (fuse_block_combine and n_blocks == 1 and dtype == torch.bfloat16 and T <= 64
-                                   and k <= 8 and I <= 512 and I_s <= 512 and not self.overlap_shared)
 
     def max_work(self, routing: str) -> int:
         """Work items the expert FFN's grid is sized for (dmoe_schedule_max_work)."""
@@ -158,21 +151,10 @@ class MoELayer:
         lib.dmoe_shared_expert_ffn(xk, w["ws13"], w["ws2"], self.T, self.H, self.I_s, self.shared_out,
                                    self.workspace_s, self._side)
 
-    def fused(self, routing: str) -> bool:
-        """Whether the expert FFN of this routing also writes y (one block)."""
-        return routing == "block" and self.fuse_block_combine
-
     def experts_ffn(self, w: dict, routing: str = "block", stream=None):
         """Expert FFN (routed experts and the shared expert) on the chunk-major
-        copy of x that :meth:`route` stored; for a fused routing (see
-        :meth:`fused`) the combine too, into y."""
+        copy of x that :meth:`route` stored."""
         main = stream if stream is not None else torch.cuda.current_stream()
-        if self.fused(routing):
-            lib.dmoe_expert_ffn_block_combine(self.x_chunked, self._x, w["w13"], w["w2"], w.get("ws13"),
-                                              w.get("ws2"), self.T, self.H, self.E, self.I, self.I_s, self.k,
-                                              self.max_work(routing), self.sched, self.block_experts,
-                                              self.combine_w, self.y, self.workspace, main)
-            return
         if self.overlap_shared:
             self._side.wait_stream(main)  # x_chunked and the previous call's readers
             self._shared_ffn(self.x_chunked, w)
@@ -195,9 +177,6 @@ class MoELayer:
             lib.dmoe_pack_activations(x, self.T, self.H, self.x_chunked_s, self._side)
             self._shared_ffn(self.x_chunked_s, w)
         self.route(x, w["w_router"], w.get("bias"), routing, main, fused=fused_routing)
-        if self.fused(routing):
-            self.experts_ffn(w, routing, main)
-            return self.y
         self._routed_ffn(w, routing, main)
         if self.overlap_shared:
             main.wait_stream(self._side)

@@ -32,8 +32,7 @@ EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggre
            "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work",
            "dmoe_schedule_scratch_ints", "dmoe_route_block",
            "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
-           "dmoe_expert_ffn", "dmoe_expert_ffn_block_combine", "dmoe_shared_ffn_workspace_size",
-           "dmoe_shared_expert_ffn", "dmoe_combine",
+           "dmoe_expert_ffn", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
            "dmoe_last_error", "dmoe_version")
 
 
@@ -72,7 +71,6 @@ _SIGS = {
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
     "dmoe_expert_ffn": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
-    "dmoe_expert_ffn_block_combine": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _I, _P, _P, _S, _P], _I),
     "dmoe_shared_ffn_workspace_size": ([_I, _I, _I], _S),
     "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
@@ -254,16 +252,6 @@ def dmoe_expert_ffn(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_wo
                                   dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
                                   ptr(slot_out), ptr(shared_out), ptr(workspace),
                                   workspace.numel() * workspace.element_size(), stream_handle(stream)))
-
-
-def dmoe_expert_ffn_block_combine(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
-                                  sched: Schedule, block_experts, combine_w, y, workspace, stream=None):
-    _check(load().dmoe_expert_ffn_block_combine(ptr(x_chunked), ptr(x), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
-                                                dtype_code(x_chunked), T, H, E, I, I_s, k, max_work,
-                                                sched.as_c(), ptr(block_experts), ptr(combine_w),
-                                                dtype_code(y), ptr(y), ptr(workspace),
-                                                workspace.numel() * workspace.element_size(),
-                                                stream_handle(stream)))
 
 
 def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):

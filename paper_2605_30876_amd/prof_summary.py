@@ -37,8 +37,8 @@ import sqlite3
 import statistics
 import sys
 
-FFN_KERNELS = ("ffn_gateup_bf16_kernel", "ffn_down_bf16_kernel", "ffn_down_combine_bf16_kernel",
-               "ffn_tile_bf16_kernel", "ffn_gateup_f32_kernel", "ffn_down_f32_kernel")
+FFN_KERNELS = ("ffn_gateup_bf16_kernel", "ffn_down_bf16_kernel", "ffn_tile_bf16_kernel", "ffn_gateup_f32_kernel",
+               "ffn_down_f32_kernel")
 
 
 def short(name: str) -> str:

@@ -324,33 +324,3 @@ def test_schedule_scratch_ints():
     assert lib.dmoe_schedule_scratch_ints(1, 1, 16) == 2 * 16
     assert lib.dmoe_schedule_scratch_ints(0, 8, 256) == 0
     assert lib.dmoe_schedule_scratch_ints(8, 8, 0) == 0
-
-
-def _bc(L, p, **over):
-    a = dict(x=p, xr=None, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512,
-             k=8, max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), be=p, cw=p, ydt=lib.DMOE_F32, y=p,
-             ws=p, ws_bytes=1 << 30)
-    a.update(over)
-    return status(L, "dmoe_expert_ffn_block_combine", a["x"], a["xr"], a["w13"], a["w2"], a["ws13"], a["ws2"],
-                  a["dt"], a["T"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["be"],
-                  a["cw"], a["ydt"], a["y"], a["ws"], a["ws_bytes"], None)
-
-
-def test_block_combine_validation(L, buf):
-    _, p = buf
-    INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
-    assert _bc(L, p, be=None)[0] == INV
-    assert _bc(L, p, cw=None)[0] == INV
-    assert _bc(L, p, y=None)[0] == INV
-    assert _bc(L, p, y=p + 4)[0] == INV
-    assert _bc(L, p, ydt=7)[0] == INV
-    assert _bc(L, p, x=None)[0] == INV
-    assert _bc(L, p, ws2=None)[0] == INV           # shared pair inconsistent
-    st, msg = _bc(L, p, ws_bytes=100)
-    assert st == INV and "workspace" in msg
-    assert _bc(L, p, T=65, max_work=8)[0] == UNS   # more than four token tiles
-    assert _bc(L, p, k=9, max_work=9)[0] == UNS
-    assert _bc(L, p, I=640)[0] == UNS
-    assert _bc(L, p, I_s=640)[0] == UNS
-    st, msg = _bc(L, p, dt=lib.DMOE_F32)
-    assert st == UNS and "DMOE_BF16" in msg

@@ -23,7 +23,7 @@ def test_shared_expert_overlap_matches(gpu_lib, name):
     w = pack_weights(d)
     dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
     mk = lambda ov: MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt, device="cuda",
-                             overlap_shared=ov, fuse_block_combine=False)
+                             overlap_shared=ov)
     a, b = mk(True), mk(False)
     assert a.overlap_shared == (cfg.I_s > 0)
     for routing in ("block", "token", "topp"):
