@@ -122,27 +122,30 @@ struct FfnParams {
 constexpr int kFrag = 512;  // bf16 elements of one packed 16 x 32 weight tile (1 KiB)
 
 // Operands of one wave for up to KMAX K-steps (32 each) of its K-slice.
-// A: one 16-row weight tile, all steps issued at once; B: NT 16-column token
+// A: RT 16-row weight tiles, all steps issued at once; B: NT 16-column token
 // tiles in chunks of BC steps, double-buffered when a burst has more than one
-// chunk.
-template <int NT, int KMAX, int BC>
+// chunk.  Each B fragment feeds RT matrix instructions.
+template <int NT, int KMAX, int BC, int RT = 1>
 struct WaveOps {
   static constexpr int kChunks = KMAX / BC;
-  bf16x8 a[KMAX];
+  bf16x8 a[RT][KMAX];
   bf16x8 b[kChunks > 1 ? 2 : 1][BC][NT];
 };
 
-// A: packed tiles, step s at pa + s*kFrag (one contiguous burst per wave).
-template <int NT, int KMAX, int BC>
-__device__ __forceinline__ void issue_a(WaveOps<NT, KMAX, BC>& w, const bf16_t* pa, int ns) {
+// A: packed tiles, step s of tile r at pa + r*tstride + s*kFrag (one
+// contiguous burst per tile).
+template <int NT, int KMAX, int BC, int RT>
+__device__ __forceinline__ void issue_a(WaveOps<NT, KMAX, BC, RT>& w, const bf16_t* pa, size_t tstride, int ns) {
 #pragma unroll
-  for (int s = 0; s < KMAX; ++s)
-    if (s < ns) w.a[s] = ld_bf16x8(pa + s * kFrag);
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int s = 0; s < KMAX; ++s)
+      if (s < ns) w.a[r][s] = ld_bf16x8(pa + r * tstride + s * kFrag);
 }
 
 // B: chunk-major rows, step s at pb[ct] + s*bstep.
-template <int BUF, int NT, int KMAX, int BC>
-__device__ __forceinline__ void issue_b(WaveOps<NT, KMAX, BC>& w, const bf16_t* const* pb, int bstep, int chunk,
+template <int BUF, int NT, int KMAX, int BC, int RT>
+__device__ __forceinline__ void issue_b(WaveOps<NT, KMAX, BC, RT>& w, const bf16_t* const* pb, int bstep, int chunk,
                                         int ns) {
 #pragma unroll
   for (int s = 0; s < BC; ++s)
@@ -151,9 +154,9 @@ __device__ __forceinline__ void issue_b(WaveOps<NT, KMAX, BC>& w, const bf16_t* 
       for (int ct = 0; ct < NT; ++ct) w.b[BUF][s][ct] = ld_bf16x8(pb[ct] + (chunk * BC + s) * bstep);
 }
 
-template <int C, int NT, int KMAX, int BC>
-__device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC>& w, const bf16_t* const* pb, int bstep, int ns,
-                                          f32x4 (&acc)[NT]) {
+template <int C, int NT, int KMAX, int BC, int RT>
+__device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC, RT>& w, const bf16_t* const* pb, int bstep, int ns,
+                                          f32x4 (&acc)[RT][NT]) {
   constexpr int NCH = KMAX / BC;
   if constexpr (C < NCH) {
     if (C * BC < ns) {
@@ -164,7 +167,10 @@ __device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC>& w, const bf16_t
         if (C * BC + s < ns)
 #pragma unroll
           for (int ct = 0; ct < NT; ++ct)
-            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.a[C * BC + s], w.b[C & 1][s][ct], acc[ct], 0, 0, 0);
+#pragma unroll
+            for (int r = 0; r < RT; ++r)
+              acc[r][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w.a[r][C * BC + s], w.b[C & 1][s][ct], acc[r][ct],
+                                                                   0, 0, 0);
       mma_chunk<C + 1>(w, pb, bstep, ns, acc);
     }
   }
@@ -174,51 +180,59 @@ __device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC>& w, const bf16_t
 // steps: token chunk 0, the weight burst, then the remaining token chunks.
 // With a_held (the slice is one burst, steps <= KMAX, already in w.a from
 // the previous pass over the same weights) the weights are not loaded again.
-template <int NT, int KMAX, int BC>
-__device__ __forceinline__ void wave_dot(WaveOps<NT, KMAX, BC>& w, const bf16_t* pa, const bf16_t* const* pb,
-                                         int bstep, int steps, f32x4 (&acc)[NT], bool a_held) {
+template <int NT, int KMAX, int BC, int RT>
+__device__ __forceinline__ void wave_dot(WaveOps<NT, KMAX, BC, RT>& w, const bf16_t* pa, size_t tstride,
+                                         const bf16_t* const* pb, int bstep, int steps, f32x4 (&acc)[RT][NT],
+                                         bool a_held) {
   for (int sc = 0; sc < steps; sc += KMAX) {
     const int ns = min(KMAX, steps - sc);
     const bf16_t* pbs[NT];
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) pbs[ct] = pb[ct] + sc * bstep;
     issue_b<0>(w, pbs, bstep, 0, ns);
-    if (!a_held) issue_a(w, pa + sc * kFrag, ns);
+    if (!a_held) issue_a(w, pa + sc * kFrag, tstride, ns);
     __builtin_amdgcn_sched_barrier(0);
     mma_chunk<0>(w, pbs, bstep, ns, acc);
   }
 }
 
 // Sum the four waves' partial tiles into wave 0's registers (wave order).
-template <int NT>
-__device__ __forceinline__ void reduce_waves(f32x4 (&acc)[NT], f32x4 (*red)[NT][kWave], int wave, int lane) {
+template <int RT, int NT>
+__device__ __forceinline__ void reduce_waves(f32x4 (&acc)[RT][NT], f32x4 (*red)[RT][NT][kWave], int wave,
+                                             int lane) {
   if (wave > 0) {
 #pragma unroll
-    for (int ct = 0; ct < NT; ++ct) red[wave - 1][ct][lane] = acc[ct];
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int ct = 0; ct < NT; ++ct) red[wave - 1][r][ct][lane] = acc[r][ct];
   }
   __syncthreads();
   if (wave == 0) {
 #pragma unroll
-    for (int ct = 0; ct < NT; ++ct)
+    for (int r = 0; r < RT; ++r)
 #pragma unroll
-      for (int ww = 0; ww < 3; ++ww) acc[ct] += red[ww][ct][lane];
+      for (int ct = 0; ct < NT; ++ct)
+#pragma unroll
+        for (int ww = 0; ww < 3; ++ww) acc[r][ct] += red[ww][r][ct][lane];
   }
 }
 
-template <int NT>
-__device__ __forceinline__ void zero(f32x4 (&acc)[NT]) {
+template <int RT, int NT>
+__device__ __forceinline__ void zero(f32x4 (&acc)[RT][NT]) {
 #pragma unroll
-  for (int ct = 0; ct < NT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
 // Occupancy floors (waves per SIMD) for the two-tile variants, which serve
-// block-routed decode steps: 3 (gate/up) and 5 (down, with 4-step weight
-// bursts) keep every workgroup of such a launch resident at once instead of
-// leaving a second partial round.
-// grid (ldh / 8, groups): packed gate/up tile `it` = 8 intermediate units.
+// block-routed decode steps: 3 (gate/up and down) keep every workgroup of
+// such a launch resident at once instead of leaving a second partial round.
+// grid (ldh / (8 RT), groups): packed gate/up tiles it .. it + RT - 1, tile
+// `it` = 8 intermediate units.
 // Wave w reduces over hidden chunks [w*H/32, (w+1)*H/32) (K-steps
 // [w*H/128, (w+1)*H/128)).
-template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst>
+template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst, int RT>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
@@ -226,7 +240,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
     return;
   if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
-  const int it = blockIdx.x;
+  const int it = blockIdx.x * RT;  // first of the RT packed tiles (Iw / 8 is a multiple of 16)
   if (it * 8 >= Iw) return;
   const int H = p.H;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -234,11 +248,12 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
   const int ksteps = H >> 5, steps = ksteps >> 2;
   const bf16_t* W = g.expert >= 0 ? p.w13 + static_cast<size_t>(g.expert) * 2 * p.I * H : p.ws13;
   const bf16_t* pa = W + (static_cast<size_t>(it) * ksteps + wave * steps) * kFrag + lane * 8;
+  const size_t tstride = static_cast<size_t>(ksteps) * kFrag;  // next packed tile
   const int bstep = 32 * p.T;  // 4 chunks of T tokens per K-step
   const int chunk0 = wave * steps * 4 + q;
 
-  __shared__ f32x4 red[3][NT][kWave];
-  WaveOps<NT, KMAX, BC> w;  // a one-burst weight slice stays here across passes
+  __shared__ f32x4 red[3][RT][NT][kWave];
+  WaveOps<NT, KMAX, BC, RT> w;  // a one-burst weight slice stays here across passes
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
     const bf16_t* pb[NT];
     int tok[NT];
@@ -253,30 +268,33 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
     for (int ct = 0; ct < NT; ++ct)
       pb[ct] = gathered ? p.xr + static_cast<size_t>(tok[ct]) * H + chunk0 * 8
                         : p.xk + (static_cast<size_t>(chunk0) * p.T + tok[ct]) * 8;
-    f32x4 acc[NT];
+    f32x4 acc[RT][NT];
     zero(acc);
-    wave_dot(w, pa, pb, gathered ? 32 : bstep, steps, acc, p0 > 0 && steps <= KMAX);
+    wave_dot(w, pa, tstride, pb, gathered ? 32 : bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
-      for (int ct = 0; ct < NT; ++ct) {
-        const int col = p0 + ct * 16 + c;
-        if (col < g.n) {
-          // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*it + 2q
-          const f32x4 v = acc[ct];
-          const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
-          const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3]);
-          bf16_t* dst = p.hk + (static_cast<size_t>(it) * p.R + g.r0 + col) * 8 + 2 * q;
-          *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
+      for (int r = 0; r < RT; ++r)
+#pragma unroll
+        for (int ct = 0; ct < NT; ++ct) {
+          const int col = p0 + ct * 16 + c;
+          if (col < g.n) {
+            // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*(it + r) + 2q
+            const f32x4 v = acc[r][ct];
+            const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
+            const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3]);
+            bf16_t* dst = p.hk + (static_cast<size_t>(it + r) * p.R + g.r0 + col) * 8 + 2 * q;
+            *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
+          }
         }
-      }
     }
     __syncthreads();  // red is reused by the next pass
   }
 }
 
-// grid (H / 16, groups): packed down tile `jt` = 16 output features.
-template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst>
+// grid (H / (16 RT), groups): packed down tiles jt .. jt + RT - 1, tile `jt`
+// = 16 output features.
+template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst, int RT>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
@@ -285,17 +303,18 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
-  const int jt = blockIdx.x;
+  const int jt = blockIdx.x * RT;  // first of the RT packed tiles (H / 16 is a multiple of 8)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = lane >> 4, c = lane & 15;
   const int ksteps = Kd >> 5, steps = ksteps >> 2;
   const bf16_t* W = g.expert >= 0 ? p.w2 + static_cast<size_t>(g.expert) * H * p.I : p.ws2;
   const bf16_t* pa = W + (static_cast<size_t>(jt) * ksteps + wave * steps) * kFrag + lane * 8;
+  const size_t tstride = static_cast<size_t>(ksteps) * kFrag;  // next packed tile
   const int bstep = 32 * p.R;
   const int chunk0 = wave * steps * 4 + q;
 
-  __shared__ f32x4 red[3][NT][kWave];
-  WaveOps<NT, KMAX, BC> w;  // a one-burst weight slice stays here across passes
+  __shared__ f32x4 red[3][RT][NT][kWave];
+  WaveOps<NT, KMAX, BC, RT> w;  // a one-burst weight slice stays here across passes
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
     const bf16_t* pb[NT];
 #pragma unroll
@@ -303,24 +322,24 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
       const int col = min(p0 + ct * 16 + c, g.n - 1);
       pb[ct] = p.hk + (static_cast<size_t>(chunk0) * p.R + g.r0 + col) * 8;
     }
-    f32x4 acc[NT];
+    f32x4 acc[RT][NT];
     zero(acc);
-    wave_dot(w, pa, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
+    wave_dot(w, pa, tstride, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
       for (int ct = 0; ct < NT; ++ct) {
         const int col = p0 + ct * 16 + c;
         if (col < g.n) {
-          const int j = jt * 16 + 4 * q;
           float* dst;
           if (g.tok) {
             const int r = g.r0 + col;
-            dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H + j;
+            dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H;
           } else {
-            dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H + j;
+            dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H;
           }
-          *reinterpret_cast<f32x4*>(dst) = acc[ct];
+#pragma unroll
+          for (int r = 0; r < RT; ++r) *reinterpret_cast<f32x4*>(dst + (jt + r) * 16 + 4 * q) = acc[r][ct];
         }
       }
     }
@@ -657,37 +676,44 @@ int pick_ntiles(int T, int k, int max_work) {
 }
 
 // Launch shapes per token-tile count NT: weight burst KMAX steps, token
-// chunks of BC steps, occupancy floor MINW (waves per SIMD), and the order of
-// the grid rows (kSharedFirst, see the top of the file).  The two-tile
-// variants serve block-routed decode steps, whose launches are small enough
-// that a higher floor keeps every workgroup resident at once.
+// chunks of BC steps, occupancy floor MINW (waves per SIMD), weight tiles
+// per wave (kGuRows / kDnRows: each token fragment feeds that many matrix
+// instructions), and the order of the grid rows (kSharedFirst, see the top
+// of the file).  The two-tile variants serve block-routed decode steps, whose
+// launches are small enough that a higher floor keeps every workgroup
+// resident at once; their down kernel applies each h fragment to two weight
+// tiles (half the h reads from L2; measured 0.4 us faster per step than one
+// tile, while two gate/up tiles per wave measured 1.2 us slower).
 template <int NT>
 struct Shape;
 template <>
 struct Shape<1> {
   static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 4, kDnMax = 8, kDnChunk = 4, kDnWaves = 5;
+  static constexpr int kGuRows = 1, kDnRows = 1;
   static constexpr bool kSharedFirst = true;
 };
 template <>
 struct Shape<2> {
-  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 3, kDnMax = 4, kDnChunk = 4, kDnWaves = 5;
+  static constexpr int kGuMax = 16, kGuChunk = 4, kGuWaves = 3, kDnMax = 4, kDnChunk = 4, kDnWaves = 3;
+  static constexpr int kGuRows = 1, kDnRows = 2;
   static constexpr bool kSharedFirst = false;
 };
 template <>
 struct Shape<4> {
   static constexpr int kGuMax = 8, kGuChunk = 4, kGuWaves = 1, kDnMax = 8, kDnChunk = 4, kDnWaves = 1;
+  static constexpr int kGuRows = 1, kDnRows = 1;
   static constexpr bool kSharedFirst = false;
 };
 
 template <int NT>
 hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   using S = Shape<NT>;
-  ffn_gateup_bf16_kernel<NT, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst>
-      <<<dim3(ldh / 8, groups), kThreads, 0, s>>>(p);
+  ffn_gateup_bf16_kernel<NT, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst, S::kGuRows>
+      <<<dim3(ldh / (8 * S::kGuRows), groups), kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_down_bf16_kernel<NT, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst>
-      <<<dim3(p.H / 16, groups), kThreads, 0, s>>>(p);
+  ffn_down_bf16_kernel<NT, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst, S::kDnRows>
+      <<<dim3(p.H / (16 * S::kDnRows), groups), kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -697,15 +723,15 @@ constexpr int kSplitRows = 32;  // one-tile schedules: larger items go to the ti
 // kernels for the others; each gate/up half runs before either down half.
 hipError_t launch_hybrid_bf16(const FfnParams& p, int ldh, int items, hipStream_t s) {
   using S = Shape<1>;
-  ffn_gateup_bf16_kernel<1, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst>
-      <<<dim3(ldh / 8, items), kThreads, 0, s>>>(p);
+  ffn_gateup_bf16_kernel<1, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst, S::kGuRows>
+      <<<dim3(ldh / (8 * S::kGuRows), items), kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_tile_bf16_kernel<true><<<dim3(ldh / (8 * kTileRows), items), kThreads, 0, s>>>(p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_down_bf16_kernel<1, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst>
-      <<<dim3(p.H / 16, items), kThreads, 0, s>>>(p);
+  ffn_down_bf16_kernel<1, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst, S::kDnRows>
+      <<<dim3(p.H / (16 * S::kDnRows), items), kThreads, 0, s>>>(p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_tile_bf16_kernel<false><<<dim3(p.H / (16 * kTileRows), items), kThreads, 0, s>>>(p);
