@@ -26,14 +26,18 @@ ARCH = os.environ.get("DMOE_OFFLOAD_ARCH", "gfx950")
 
 
 def ffn_source_hash() -> str:
-    """Hash of the sources of the expert-FFN kernels: hardware-counter figures
-    taken on other sources are stale."""
+    """Hash of the code of the expert-FFN kernels (line comments and blank
+    lines left out): hardware-counter figures taken on other code are stale."""
     import hashlib
+    import re
 
     h = hashlib.sha256()
     for f in ("ffn.hip", "pack.hip"):
-        with open(os.path.join(CSRC, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
+            for line in fh:
+                code = re.sub(r"//.*", "", line).rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

@@ -10,9 +10,11 @@
 // DMOE_WORK_ROWS.  One-tile launches (schedules of many small items, whose
 // max_work bound is loose) put the shared pieces first so that the rows that
 // exit at once are dispatched last; the others put them last (measured
-// faster for block-routed decode steps).  A workgroup owns one 16-row weight tile of one item,
-// streams it from HBM and applies it to the item's rows (tokens): each
-// selected expert's weights are read once per forward per piece of its rows.
+// faster for block-routed decode steps).  A decode workgroup owns one or two
+// 16-row weight tiles of one item, streams them from HBM and applies them to
+// the item's rows (tokens); a tile workgroup owns 128 rows and up to 128
+// tokens.  Each selected expert's weights are read once per forward per piece
+// of its rows.
 //
 // bf16 path (matrix cores, v_mfma_f32_16x16x32_bf16, fp32 accumulation):
 //  * A operand = weight rows, B operand = token rows, C = [weight row][token].
@@ -35,7 +37,10 @@
 //    [K/8][rows][8], so 16 consecutive rows read 256 contiguous bytes per
 //    8-element chunk.  Lane (q, c) of a K-step holds chunk 4*step + q of its
 //    row in both operands, which is all the matrix instruction needs.
-// f32 path: plain per-thread dot products (small fp32 layers).
+//    Scattered token rows (token-level routing) may instead be read from the
+//    row-major x, one 64-byte piece per token and K-step (tile_gathered).
+// f32 path: reduction-major weights, each lane one output unit, the waves
+// splitting the reduction (small fp32 layers).
 #include <algorithm>
 #include <type_traits>
 
