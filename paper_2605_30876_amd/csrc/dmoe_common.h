@@ -70,6 +70,11 @@ hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, f
                              int32_t* experts, float* w, float* gap, hipStream_t s);
 hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* experts, float* w,
                              float* gap, hipStream_t s);
+// Softmax of the router's S partial logit planes and token top-k in one
+// launch (E <= 512); probs, weights and selections as the two-step chain.
+bool softmax_token_topk_fits(int E);
+hipError_t launch_softmax_token_topk(const float* part, int S, const float* bias, int T, int E, int k, float* probs,
+                                     float* logits, int32_t* experts, float* w, float* gap, hipStream_t s);
 hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, int E,
                            dmoe_schedule sched, hipStream_t s);
 hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, float p, int min_c,

@@ -10,8 +10,9 @@
 // single round trip: all partial logits are loaded at once, then softmax
 // rows (into LDS), block sums, radix-select top-k per block, combine weights
 // and the schedule run on chip.  (Token routing has T rows to select; spread
-// over T/4 workgroups by the separate kernels it is faster, so it is not
-// fused.)  The arithmetic is that of
+// over T/4 workgroups it is faster, so it runs the softmax and each token's
+// selection in one launch of T/4 workgroups, then the schedule.)  The
+// arithmetic is that of
 // the separate kernels (same device routines, same summation orders), so the
 // results are bit-identical to dmoe_router_logits +
 // dmoe_block_aggregate_topk / dmoe_token_topk + dmoe_build_expert_schedule.
@@ -186,8 +187,21 @@ hipError_t launch_route(const RouteArgs& a, dmoe_dtype dt, hipStream_t s) {
                                                      a.block_scores, a.experts, a.combine_w, a.gap, a.sched);
     return hipGetLastError();
   }
-  hipError_t err = launch_router(a.x, a.w, a.bias, dt, a.T, a.H, a.E, a.logits, a.probs, a.x_chunked,
-                                 a.workspace, a.ws_bytes, s);
+  hipError_t err;
+  if (!a.block && dt == DMOE_BF16 && softmax_token_topk_fits(a.E)) {
+    // token routing: the softmax and each token's selection in one launch
+    float* part = nullptr;
+    int S = 1;
+    err = launch_router_partials(a.x, a.w, dt, a.T, a.H, a.E, a.probs, a.x_chunked, a.workspace, a.ws_bytes, s,
+                                 &part, &S);
+    if (err != hipSuccess) return err;
+    err = launch_softmax_token_topk(part, S, a.bias, a.T, a.E, a.k, a.probs, a.logits, a.experts, a.combine_w,
+                                    a.gap, s);
+    if (err != hipSuccess) return err;
+    return launch_schedule(a.experts, G, 1, a.k, a.E, a.sched, s);
+  }
+  err = launch_router(a.x, a.w, a.bias, dt, a.T, a.H, a.E, a.logits, a.probs, a.x_chunked, a.workspace,
+                      a.ws_bytes, s);
   if (err != hipSuccess) return err;
   if (a.block)
     err = launch_block_topk(a.probs, G, a.gs, a.E, a.k, a.block_scores, a.experts, a.combine_w, a.gap, s);

@@ -168,7 +168,70 @@ __global__ __launch_bounds__(256) void token_topk_kernel(const float* __restrict
   }
 }
 
+// Token routing straight from the router's partial logits: one wave per
+// token sums the partials, takes the softmax in registers (the routine the
+// separate softmax kernel uses, so probs are bit-identical), stages the row in
+// LDS and selects from it as token_topk_kernel does (one launch instead of
+// two).  E <= 512.
+template <int NQ>
+__global__ __launch_bounds__(256) void softmax_token_topk_kernel(const float* part, int S,
+                                                                 const float* __restrict__ bias, int T, int E, int k,
+                                                                 float* probs, float* __restrict__ logits,
+                                                                 int32_t* __restrict__ experts,
+                                                                 float* __restrict__ w, float* __restrict__ gap) {
+  extern __shared__ float rows[];
+  __shared__ int sel[4][kMaxK + 1];
+  __shared__ float selv[4][kMaxK + 1];
+  __shared__ float bufv[4][kMaxK + 1];
+  __shared__ int bufi[4][kMaxK + 1];
+  __shared__ float denom_s[4];
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + wave;
+  // Waves past the last token skip the work but still reach the barriers.
+  const bool live = t < T;
+  float* row = rows + static_cast<size_t>(wave) * E;
+  if (live) {
+    dev::RowPartials<NQ> r[1];
+    dev::load_row<NQ>(part, static_cast<size_t>(T) * E, S, bias, E, t, r[0]);
+    const bool lv[1] = {true};
+    float* const out[1] = {probs + static_cast<size_t>(t) * E};
+    float* const lds[1] = {row};
+    float* const lo[1] = {logits ? logits + static_cast<size_t>(t) * E : nullptr};
+    dev::softmax_loaded<NQ, 1>(r, lv, S, bias != nullptr, E, out, lds, lo);
+  }
+  __syncthreads();  // the staged rows (and, with S == 1, part aliasing probs) are complete
+
+  const int rounds = k < E ? k + 1 : k;
+  if (live) dev::wave_topk_radix(row, E, rounds, sel[wave], selv[wave], bufv[wave], bufi[wave]);
+  __syncthreads();
+  if (live && lane == 0) {
+    float denom = 0.f;
+    for (int j = 0; j < k; ++j) denom += selv[wave][j];
+    if (gap) gap[t] = k < E ? selv[wave][k - 1] - selv[wave][k] : INFINITY;
+    denom_s[wave] = denom;
+  }
+  __syncthreads();
+  if (live && lane < k) {
+    experts[static_cast<size_t>(t) * k + lane] = sel[wave][lane];
+    w[static_cast<size_t>(t) * k + lane] = selv[wave][lane] / denom_s[wave];
+  }
+}
+
 }  // namespace
+
+bool softmax_token_topk_fits(int E) { return E <= dev::kRegSoftmaxMaxE && E <= kRadixMaxE; }
+
+hipError_t launch_softmax_token_topk(const float* part, int S, const float* bias, int T, int E, int k, float* probs,
+                                     float* logits, int32_t* experts, float* w, float* gap, hipStream_t s) {
+  const unsigned blocks = (T + 3) / 4;
+  const size_t lds = static_cast<size_t>(4) * E * sizeof(float);
+  if (E <= 256)
+    softmax_token_topk_kernel<1><<<blocks, 256, lds, s>>>(part, S, bias, T, E, k, probs, logits, experts, w, gap);
+  else
+    softmax_token_topk_kernel<2><<<blocks, 256, lds, s>>>(part, S, bias, T, E, k, probs, logits, experts, w, gap);
+  return hipGetLastError();
+}
 
 hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, float* scores,
                              int32_t* experts, float* w, float* gap, hipStream_t s) {
