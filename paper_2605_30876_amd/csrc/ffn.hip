@@ -448,9 +448,10 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
   };
   auto store_b = [&](int buf) {
 #pragma unroll
-    for (int s = 0; s < kStageSteps; ++s)
+    for (int h = 0; h < 2; ++h)
+      if (pct + 4 * h < nt)  // uniform: the wave's tile holds tokens
 #pragma unroll
-      for (int h = 0; h < 2; ++h) stage[buf][s][pct + 4 * h][pl] = b_nxt[s][h];
+        for (int s = 0; s < kStageSteps; ++s) stage[buf][s][pct + 4 * h][pl] = b_nxt[s][h];
   };
 
   const int nstages = ksteps / kStageSteps;
@@ -469,23 +470,23 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p)
     if (st + 2 < nstages) load_a(st + 2, a_reg[(R + 2) % 3]);
     __builtin_amdgcn_sched_barrier(0);
     const int buf = st & 1;
-    // token tile by token tile: the next tile's fragments are read from LDS
-    // (always in bounds; tiles past nt are read but not used) while this
-    // tile's matrix instructions run.  Each accumulator still sums K in order.
+    // token tile by token tile over the item's nt live tiles: the next
+    // tile's fragments are read from LDS while this tile's matrix
+    // instructions run.  Each accumulator still sums K in order.
     bf16x8 bc[kStageSteps], bn[kStageSteps];
 #pragma unroll
     for (int s = 0; s < kStageSteps; ++s) bc[s] = stage[buf][s][0][lane];
 #pragma unroll
     for (int ct = 0; ct < kTileTok; ++ct) {
-      if (ct + 1 < kTileTok)
+      if (ct >= nt) break;  // uniform
+      if (ct + 1 < nt)
 #pragma unroll
         for (int s = 0; s < kStageSteps; ++s) bn[s] = stage[buf][s][ct + 1][lane];
-      if (ct < nt)
 #pragma unroll
-        for (int s = 0; s < kStageSteps; ++s)
+      for (int s = 0; s < kStageSteps; ++s)
 #pragma unroll
-          for (int m = 0; m < kRowTiles; ++m)
-            acc[m][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_reg[R][s][m], bc[s], acc[m][ct], 0, 0, 0);
+        for (int m = 0; m < kRowTiles; ++m)
+          acc[m][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_reg[R][s][m], bc[s], acc[m][ct], 0, 0, 0);
 #pragma unroll
       for (int s = 0; s < kStageSteps; ++s) bc[s] = bn[s];
     }
