@@ -354,7 +354,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 
 // ---- tile kernels: many tokens per work item --------------------------------
 //
-// A workgroup covers 4 * kRowTiles 16-row weight tiles (wave w: packed tiles
+// A workgroup covers 4 * kRowTiles (one or two) 16-row weight tiles (wave w: packed tiles
 // kRowTiles * (4*bx + w) + m, m < kRowTiles, over the whole reduction) x up
 // to 128 tokens of one work item (8 token tiles).  The reduction runs in
 // stages of kStageSteps K-steps: the stage's token fragments are loaded from
@@ -365,13 +365,12 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 // matrix work).  Accumulation order (K ascending) and the epilogues match the
 // decode kernels.
 constexpr int kTileTok = 8;       // token tiles per workgroup (128 tokens)
-constexpr int kStageSteps = 4;    // K-steps per LDS stage
-constexpr int kRowTiles = 2;      // weight tiles per wave
-constexpr int kTileRows = 4 * kRowTiles;  // weight tiles per workgroup
+constexpr int kStageSteps = 2;    // K-steps per LDS stage (two: 32 KB of LDS, three workgroups per CU)
 static_assert(kTileTok * 16 == DMOE_WORK_ROWS, "a tile workgroup covers one work item's rows");
 
-template <bool kGateUp>
+template <bool kGateUp, int kRowTiles>
 __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p) {
+  constexpr int kTileRows = 4 * kRowTiles;  // weight tiles per workgroup
   Group g;
   if (!decode_item(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g)) return;
   if (g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
@@ -723,6 +722,23 @@ hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Tile kernels.  Two weight tiles per wave halve the LDS reads per weight
+// byte; one tile per wave doubles the workgroups.  A gate/up grid of fewer than
+// two rounds of the chip (three resident workgroups on each of 256 CUs) ends
+// in a long partial round, which the finer split shortens; both halves of the
+// FFN take the gate/up choice.
+constexpr long kTileRound = 3L * 256;
+template <bool kGateUp>
+hipError_t launch_tile_bf16(const FfnParams& p, int ldh, int items, hipStream_t s) {
+  const bool fine = static_cast<long>(ldh / 64) * items < 2 * kTileRound;
+  const int rows = kGateUp ? ldh / 8 : p.H / 16;  // packed 16-row tiles
+  if (fine)
+    ffn_tile_bf16_kernel<kGateUp, 1><<<dim3(rows / 4, items), kThreads, 0, s>>>(p);
+  else
+    ffn_tile_bf16_kernel<kGateUp, 2><<<dim3(rows / 8, items), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
 constexpr int kSplitRows = 32;  // one-tile schedules: larger items go to the tile kernels
 
 // One-tile decode kernels for the items of <= p.split_rows rows and the tile
@@ -733,15 +749,13 @@ hipError_t launch_hybrid_bf16(const FfnParams& p, int ldh, int items, hipStream_
       <<<dim3(ldh / (8 * S::kGuRows), items), kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_tile_bf16_kernel<true><<<dim3(ldh / (8 * kTileRows), items), kThreads, 0, s>>>(p);
-  err = hipGetLastError();
+  err = launch_tile_bf16<true>(p, ldh, items, s);
   if (err != hipSuccess) return err;
   ffn_down_bf16_kernel<1, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst, S::kDnRows>
       <<<dim3(p.H / (16 * S::kDnRows), items), kThreads, 0, s>>>(p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_tile_bf16_kernel<false><<<dim3(p.H / (16 * kTileRows), items), kThreads, 0, s>>>(p);
-  return hipGetLastError();
+  return launch_tile_bf16<false>(p, ldh, items, s);
 }
 
 bool use_tile_kernels(int T, int k, int max_work, int items, int ldh) {
@@ -770,11 +784,9 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
     if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
-      ffn_tile_bf16_kernel<true><<<dim3(ldh / (8 * kTileRows), items), kThreads, 0, s>>>(p);
-      hipError_t err = hipGetLastError();
+      const hipError_t err = launch_tile_bf16<true>(p, ldh, items, s);
       if (err != hipSuccess) return err;
-      ffn_tile_bf16_kernel<false><<<dim3(a.H / (16 * kTileRows), items), kThreads, 0, s>>>(p);
-      return hipGetLastError();
+      return launch_tile_bf16<false>(p, ldh, items, s);
     }
     switch (pick_ntiles(a.T, a.k, a.max_work)) {
       case 1:
