@@ -24,8 +24,9 @@
  *                              the routing of the same forward)
  *   dmoe_combine               y_t = sum_j w[t,j] * FFN_{e_tj}(x_t) + FFN_s(x_t)
  *
- * dmoe_route_block / dmoe_route_token run the first three (or the token
- * variant) as one call with fewer kernel launches; and two layout conversions for the expert FFN's operands:
+ * dmoe_route_block / dmoe_route_token / dmoe_route_topp run the routing steps
+ * and the schedule of one routing mode as one call with fewer kernel
+ * launches; and two layout conversions for the expert FFN's operands:
  *
  *   dmoe_pack_expert_weights   expert weights -> the FFN's packed layout
  *                              (once, when the model is loaded)
@@ -257,6 +258,21 @@ dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* b
                              int T, int H, int E, int k, float* logits, float* probs, void* x_chunked,
                              int32_t* token_experts, float* combine_w, float* gap, dmoe_schedule sched,
                              void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * The same for Alg. 1 with the Top-P coreset (Sec. 4.2):
+ *   dmoe_router_logits, dmoe_block_topp_route(probs, n_blocks, block_size, E,
+ *   k, p, min_coreset, ...), dmoe_build_expert_schedule(token_experts,
+ *   n_blocks*block_size, 1, k, E, sched)
+ * bit-identical to that sequence (the router's softmax and every token's own
+ * top-k run as one launch where the separate calls take two).
+ * Limits: the union of the three calls' limits.
+ */
+dmoe_status dmoe_route_topp(const void* x, const void* w_router, const float* bias, dmoe_dtype dt, int n_blocks,
+                            int block_size, int H, int E, int k, float p, int min_coreset, float* logits,
+                            float* probs, void* x_chunked, float* block_scores, int32_t* coreset,
+                            int32_t* coreset_size, int32_t* token_experts, float* combine_w, float* gap,
+                            dmoe_schedule sched, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Hidden states x [T][H] (row-major, type dt) -> x_chunked [T*H] in the

@@ -277,6 +277,67 @@ dmoe_status dmoe_route_token(const void* x, const void* w_router, const float* b
   return hip_status(dmoe::launch_route(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }
 
+dmoe_status dmoe_route_topp(const void* x, const void* w_router, const float* bias, dmoe_dtype dt, int n_blocks,
+                            int block_size, int H, int E, int k, float p, int min_coreset, float* logits,
+                            float* probs, void* x_chunked, float* block_scores, int32_t* coreset,
+                            int32_t* coreset_size, int32_t* token_experts, float* combine_w, float* gap,
+                            dmoe_schedule sched, void* workspace, size_t ws_bytes, void* stream) {
+  REQUIRE(x && w_router && probs && coreset && coreset_size && token_experts && combine_w,
+          "x, w_router, probs, coreset, coreset_size, token_experts and combine_w must not be NULL");
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
+          "every schedule array must be set");
+  REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
+  REQUIRE(block_size >= 1 && block_size <= 4096, "block_size=%d must be in [1, 4096]", block_size);
+  REQUIRE(H >= 1, "H=%d must be >= 1", H);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  REQUIRE(min_coreset >= k && min_coreset <= E, "min_coreset=%d must be in [k, E]", min_coreset);
+  REQUIRE(p > 0.f && p <= 1.f, "p=%g must be in (0, 1]", static_cast<double>(p));
+  const long T = static_cast<long>(n_blocks) * block_size;
+  REQUIRE(T * E <= kIntLimit && T * H <= kIntLimit && T * k < kIntLimit, "T*E, T*H and T*k must fit in int32");
+  ALIGNED(x);
+  ALIGNED(w_router);
+  ALIGNED(bias);
+  ALIGNED(logits);
+  ALIGNED(probs);
+  ALIGNED(x_chunked);
+  ALIGNED(block_scores);
+  ALIGNED(coreset);
+  ALIGNED(coreset_size);
+  ALIGNED(token_experts);
+  ALIGNED(combine_w);
+  ALIGNED(gap);
+  ALIGNED(workspace);
+  ALIGNED(sched.n_unique);
+  ALIGNED(sched.unique);
+  ALIGNED(sched.offsets);
+  ALIGNED(sched.scratch);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
+  if (x_chunked) {
+    REQUIRE(H % dmoe::chunk_elems(dt) == 0, "x_chunked needs H %% %d == 0 (H=%d)", dmoe::chunk_elems(dt), H);
+  }
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0, "bf16 router needs H %% 128 == 0 (H=%d)", H);
+  }
+  SUPPORT(E <= kMaxScheduleE, "the schedule supports E <= %d (E=%d)", kMaxScheduleE, E);
+  SUPPORT(dmoe::topp_supported(block_size, E, k), "the Top-P kernels do not support block_size=%d, E=%d, k=%d",
+          block_size, E, k);
+  dmoe::RouteArgs a{x, w_router, bias, static_cast<int>(T), H, E, k, block_size, false, logits, probs,
+                    x_chunked, block_scores, token_experts, combine_w, gap, sched, workspace,
+                    workspace ? ws_bytes : 0};
+  a.topp = true;
+  a.top_p = p;
+  a.min_coreset = min_coreset;
+  a.coreset = coreset;
+  a.coreset_size = coreset_size;
+  return hip_status(dmoe::launch_route(a, dt, static_cast<hipStream_t>(stream)), __func__);
+}
+
 dmoe_status dmoe_pack_activations(const void* x, dmoe_dtype dt, int T, int H, void* x_chunked,
                                   void* stream) {
   REQUIRE(x && x_chunked, "x and x_chunked must not be NULL");

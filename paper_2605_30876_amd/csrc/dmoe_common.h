@@ -79,7 +79,7 @@ hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, 
                            dmoe_schedule sched, hipStream_t s);
 hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, float p, int min_c,
                              float* block_scores, int32_t* coreset, int32_t* coreset_size, int32_t* experts,
-                             float* w, float* gap, hipStream_t s);
+                             float* w, float* gap, hipStream_t s, bool own_done = false);
 bool topp_supported(int bs, int E, int k);
 
 // The whole routing stage: router, selection (blocks of gs tokens when block,
@@ -102,6 +102,12 @@ struct RouteArgs {
   dmoe_schedule sched;
   void* workspace;
   size_t ws_bytes;
+  // Alg. 1 with the Top-P coreset (block = false; gs is the block size)
+  bool topp = false;
+  float top_p = 0.f;
+  int min_coreset = 0;
+  int32_t* coreset = nullptr;
+  int32_t* coreset_size = nullptr;
 };
 hipError_t launch_route(const RouteArgs& a, dmoe_dtype dt, hipStream_t s);
 bool route_fused_fits(int T, int E, int k, int gs, bool block);

@@ -170,7 +170,35 @@ bool route_fused_fits(int T, int E, int k, int gs, bool block) {
   return fused_layout(T, E, k, T / gs).total * sizeof(float) <= kMaxLdsBytes;
 }
 
+// Alg. 1 with the Top-P coreset: the router, every token's own top-k (with
+// the softmax in one launch when the router's partial logits allow it), the
+// coreset of each block, each token's top-k inside it, then the token-level
+// schedule.
+hipError_t launch_route_topp(const RouteArgs& a, dmoe_dtype dt, hipStream_t s) {
+  hipError_t err;
+  bool own_done = false;
+  if (dt == DMOE_BF16 && softmax_token_topk_fits(a.E)) {
+    float* part = nullptr;
+    int S = 1;
+    err = launch_router_partials(a.x, a.w, dt, a.T, a.H, a.E, a.probs, a.x_chunked, a.workspace, a.ws_bytes, s,
+                                 &part, &S);
+    if (err != hipSuccess) return err;
+    err = launch_softmax_token_topk(part, S, a.bias, a.T, a.E, a.k, a.probs, a.logits, a.experts, a.combine_w,
+                                    nullptr, s);
+    own_done = true;
+  } else {
+    err = launch_router(a.x, a.w, a.bias, dt, a.T, a.H, a.E, a.logits, a.probs, a.x_chunked, a.workspace,
+                        a.ws_bytes, s);
+  }
+  if (err != hipSuccess) return err;
+  err = launch_block_topp(a.probs, a.T / a.gs, a.gs, a.E, a.k, a.top_p, a.min_coreset, a.block_scores, a.coreset,
+                          a.coreset_size, a.experts, a.combine_w, a.gap, s, own_done);
+  if (err != hipSuccess) return err;
+  return launch_schedule(a.experts, a.T, 1, a.k, a.E, a.sched, s);
+}
+
 hipError_t launch_route(const RouteArgs& a, dmoe_dtype dt, hipStream_t s) {
+  if (a.topp) return launch_route_topp(a, dt, s);
   const int G = a.block ? a.T / a.gs : a.T;
   if (route_fused_fits(a.T, a.E, a.k, a.gs, a.block)) {
     float* part = nullptr;

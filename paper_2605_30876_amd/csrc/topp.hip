@@ -241,12 +241,16 @@ bool topp_supported(int bs, int E, int k) {
 
 hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, float p, int min_c,
                              float* block_scores, int32_t* coreset, int32_t* coreset_size, int32_t* experts,
-                             float* w, float* gap, hipStream_t s) {
+                             float* w, float* gap, hipStream_t s, bool own_done) {
   if (!topp_supported(bs, E, k)) return hipErrorInvalidValue;
   const int T = nb * bs;
-  // 1. every token's own top-k, into `experts` (overwritten by step 3)
-  hipError_t err = launch_token_topk(probs, T, E, k, experts, w, nullptr, s);
-  if (err != hipSuccess) return err;
+  hipError_t err;
+  // 1. every token's own top-k, into `experts` (overwritten by step 3;
+  //    own_done: the caller's launch already put it there)
+  if (!own_done) {
+    err = launch_token_topk(probs, T, E, k, experts, w, nullptr, s);
+    if (err != hipSuccess) return err;
+  }
   // 2. one workgroup per block
   block_coreset_kernel<<<nb, kCoreThreads, core_layout(bs, E).total * sizeof(float), s>>>(
       probs, experts, bs, E, k, p, min_c, block_scores, coreset, coreset_size);

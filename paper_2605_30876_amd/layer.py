@@ -107,7 +107,8 @@ class MoELayer:
     def route(self, x, w_router, bias=None, routing: str = "block", stream=None, fused: bool = True):
         """Routing stage: one dmoe_route_* call, or (fused=False) the chain of
         the separate entry points; both give identical results.  "topp" runs
-        the router, dmoe_block_topp_route and a token-level schedule."""
+        the router, dmoe_block_topp_route and a token-level schedule
+        (dmoe_route_topp when fused)."""
         T, H, E, k = self.T, self.H, self.E, self.k
         self._x = x  # the expert FFN reads gathered token rows from the row-major x
         if routing not in ("block", "token", "topp"):
@@ -116,6 +117,12 @@ class MoELayer:
             lib.dmoe_route_block(x, w_router, bias, self.NB, self.bs, H, E, k, self.logits, self.probs,
                                  self.x_chunked, self.block_scores, self.block_experts, self.combine_w,
                                  self.block_gap, self.sched, self.router_ws, stream)
+            return
+        if fused and routing == "topp":
+            lib.dmoe_route_topp(x, w_router, bias, self.NB, self.bs, H, E, k, self.top_p, self.min_coreset,
+                                self.logits, self.probs, self.x_chunked, self.block_scores, self.coreset,
+                                self.coreset_size, self.token_experts, self.combine_w, self.token_gap, self.sched,
+                                self.router_ws, stream)
             return
         if fused and routing == "token":
             lib.dmoe_route_token(x, w_router, bias, T, H, E, k, self.logits, self.probs, self.x_chunked,

@@ -31,7 +31,7 @@ STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG"
 EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggregate_topk", "dmoe_token_topk",
            "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work",
            "dmoe_schedule_scratch_ints", "dmoe_route_block",
-           "dmoe_route_token", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
+           "dmoe_route_token", "dmoe_route_topp", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
            "dmoe_expert_ffn", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
            "dmoe_last_error", "dmoe_version")
 
@@ -67,6 +67,8 @@ _SIGS = {
     "dmoe_route_block": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S,
                           _P], _I),
     "dmoe_route_token": ([_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, dmoe_schedule, _P, _S, _P], _I),
+    "dmoe_route_topp": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, ctypes.c_float, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                         dmoe_schedule, _P, _S, _P], _I),
     "dmoe_pack_activations": ([_P, _I, _I, _I, _P, _P], _I),
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
@@ -220,6 +222,15 @@ def dmoe_route_token(x, w_router, bias, T, H, E, k, logits, probs, x_chunked, to
     _check(load().dmoe_route_token(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), T, H, E, k, ptr(logits),
                                    ptr(probs), ptr(x_chunked), ptr(token_experts), ptr(combine_w), ptr(gap),
                                    sched.as_c(), ptr(workspace), _nbytes(workspace), stream_handle(stream)))
+
+
+def dmoe_route_topp(x, w_router, bias, n_blocks, block_size, H, E, k, p, min_coreset, logits, probs, x_chunked,
+                    block_scores, coreset, coreset_size, token_experts, combine_w, gap, sched: Schedule,
+                    workspace=None, stream=None):
+    _check(load().dmoe_route_topp(ptr(x), ptr(w_router), ptr(bias), dtype_code(x), n_blocks, block_size, H, E, k,
+                                  p, min_coreset, ptr(logits), ptr(probs), ptr(x_chunked), ptr(block_scores),
+                                  ptr(coreset), ptr(coreset_size), ptr(token_experts), ptr(combine_w), ptr(gap),
+                                  sched.as_c(), ptr(workspace), _nbytes(workspace), stream_handle(stream)))
 
 
 def dmoe_pack_activations(x, T, H, x_chunked, stream=None):

@@ -198,12 +198,20 @@ def _route(L, p, routing, **over):
         return status(L, "dmoe_route_block", a["x"], a["w"], a["bias"], a["dt"], a["nb"], a["bs"], a["H"], a["E"],
                       a["k"], a["logits"], a["probs"], a["xc"], a["scores"], a["experts"], a["cw"], a["gap"],
                       a["sched"], a["ws"], a["ws_bytes"], None)
+    if routing == "topp":
+        a.setdefault("top_p", 0.6)
+        a.setdefault("min_c", a["k"])
+        a.setdefault("core", p)
+        a.setdefault("size", p)
+        return status(L, "dmoe_route_topp", a["x"], a["w"], a["bias"], a["dt"], a["nb"], a["bs"], a["H"], a["E"],
+                      a["k"], a["top_p"], a["min_c"], a["logits"], a["probs"], a["xc"], a["scores"], a["core"],
+                      a["size"], a["experts"], a["cw"], a["gap"], a["sched"], a["ws"], a["ws_bytes"], None)
     return status(L, "dmoe_route_token", a["x"], a["w"], a["bias"], a["dt"], a["T"], a["H"], a["E"], a["k"],
                   a["logits"], a["probs"], a["xc"], a["experts"], a["cw"], a["gap"], a["sched"], a["ws"],
                   a["ws_bytes"], None)
 
 
-@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("routing", ["block", "token", "topp"])
 def test_route_validation(L, buf, routing):
     _, p = buf
     INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
@@ -220,12 +228,19 @@ def test_route_validation(L, buf, routing):
     assert _route(L, p, routing, H=2000)[0] == UNS
     st, msg = _route(L, p, routing, E=1024)
     assert st == UNS and "E <= 512" in msg
-    if routing == "block":
+    if routing in ("block", "topp"):
         assert _route(L, p, routing, nb=0)[0] == INV
         assert _route(L, p, routing, bs=5000)[0] == INV
         assert _route(L, p, routing, nb=2**20, bs=2**11)[0] == INV
     else:
         assert _route(L, p, routing, T=0)[0] == INV
+    if routing == "topp":
+        assert _route(L, p, routing, core=None)[0] == INV
+        assert _route(L, p, routing, size=None)[0] == INV
+        assert _route(L, p, routing, top_p=0.0)[0] == INV
+        assert _route(L, p, routing, top_p=1.5)[0] == INV
+        assert _route(L, p, routing, min_c=7)[0] == INV
+        assert _route(L, p, routing, min_c=300)[0] == INV
 
 
 @pytest.mark.parametrize("n_groups,gs,k,E,expect", [

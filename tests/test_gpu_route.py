@@ -1,4 +1,4 @@
-"""dmoe_route_block / dmoe_route_token (the routing stage in one call) give
+"""dmoe_route_block / dmoe_route_token / dmoe_route_topp (the routing stage in one call) give
 bit-identical results to the chain of separate entry points, on shapes that
 take the fused small-forward kernel and on shapes that do not.  Marked
 ``gpu``; the chain itself is checked against the oracle by the parity tests."""
@@ -30,8 +30,13 @@ def _snapshot(layer, routing):
                 "row_slot": layer.sched.row_slot[:rows].clone()})
     if routing == "block":
         out.pop("token_experts"), out.pop("token_gap")
-    else:
+    elif routing == "token":
         out.pop("block_scores"), out.pop("block_experts"), out.pop("block_gap")
+    else:
+        out.pop("block_experts"), out.pop("block_gap")
+        sizes = layer.coreset_size.clone()
+        out["coreset_size"] = sizes
+        out["coreset"] = torch.cat([layer.coreset[b, :int(c)] for b, c in enumerate(sizes.tolist())])
     return out
 
 
@@ -41,7 +46,7 @@ CASES = [("tiny_f32", {}), ("small_f32", {}), ("small_bf16", {}), ("small_bf16_z
          ("small_f32", {"NB": 15, "bs": 1}), ("small_bf16", {"k": 1})]
 
 
-@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("routing", ["block", "token", "topp"])
 @pytest.mark.parametrize("name,over", CASES)
 def test_route_call_equals_separate_calls(gpu_lib, name, over, routing):
     cfg = get_config(name)
