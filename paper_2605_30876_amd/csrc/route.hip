@@ -50,13 +50,26 @@ __host__ __device__ inline FusedLayout fused_layout(int T, int E, int k, int G) 
 
 constexpr int kWBatch = 8;  // selected probabilities of a token loaded together
 
-template <int NQ>
+// kPerBlock: workgroup b routes block b alone (T = gs rows of the forward's
+// T_all; the partial planes keep T_all rows) and the schedule is left to a
+// launch of its own.
+template <int NQ, bool kPerBlock = false>
 __global__ __launch_bounds__(kThreads) void route_small_kernel(
     const float* part, int S, const float* __restrict__ bias, int T, int E, int k, int gs,
     float* probs, float* __restrict__ logits, float* __restrict__ block_scores,
     int32_t* __restrict__ experts, float* __restrict__ cw, float* __restrict__ gap,
-    dmoe_schedule sched) {
+    dmoe_schedule sched, int T_all) {
   extern __shared__ float lds[];
+  if (kPerBlock) {
+    const size_t b = blockIdx.x;
+    part += b * gs * E;
+    probs += b * gs * E;
+    if (logits) logits += b * gs * E;
+    if (block_scores) block_scores += b * E;
+    experts += b * k;
+    cw += b * gs * k;
+    if (gap) gap += b;
+  }
   const int G = T / gs;
   const int K1 = k + 1;
   const FusedLayout L = fused_layout(T, E, k, G);
@@ -77,7 +90,7 @@ __global__ __launch_bounds__(kThreads) void route_small_kernel(
   //    is read only by the wave that writes it, before it writes it.)
   {
     constexpr int RB = 4 / NQ;
-    const size_t plane = static_cast<size_t>(T) * E;
+    const size_t plane = static_cast<size_t>(T_all) * E;
     for (int t0 = wave; t0 < T; t0 += kWaves * RB) {
       dev::RowPartials<NQ> r[RB];
 #pragma unroll
@@ -153,6 +166,7 @@ __global__ __launch_bounds__(kThreads) void route_small_kernel(
   __syncthreads();
 
   // 4. unique-expert schedule of the G expert lists (one block: closed form)
+  if (kPerBlock) return;
   if (G == 1 && k <= kWave)
     dev::schedule_one_group(expc, gs, k, slds, sched);
   else
@@ -168,6 +182,13 @@ bool route_fused_fits(int T, int E, int k, int gs, bool block) {
   if (E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
   if (static_cast<long>(T) * E > kFusedMaxTE) return false;
   return fused_layout(T, E, k, T / gs).total * sizeof(float) <= kMaxLdsBytes;
+}
+
+// One workgroup per block when a block's rows fit in LDS.
+bool route_block_fits(int gs, int E, int k, bool block) {
+  if (!block) return false;
+  if (E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
+  return fused_layout(gs, E, k, 1).total * sizeof(float) <= kMaxLdsBytes;
 }
 
 // Alg. 1 with the Top-P coreset: the router, every token's own top-k (with
@@ -209,11 +230,32 @@ hipError_t launch_route(const RouteArgs& a, dmoe_dtype dt, hipStream_t s) {
     const size_t lds = fused_layout(a.T, a.E, a.k, G).total * sizeof(float);
     if (a.E <= 256)
       route_small_kernel<1><<<1, kThreads, lds, s>>>(part, S, a.bias, a.T, a.E, a.k, a.gs, a.probs, a.logits,
-                                                     a.block_scores, a.experts, a.combine_w, a.gap, a.sched);
+                                                     a.block_scores, a.experts, a.combine_w, a.gap, a.sched, a.T);
     else
       route_small_kernel<2><<<1, kThreads, lds, s>>>(part, S, a.bias, a.T, a.E, a.k, a.gs, a.probs, a.logits,
-                                                     a.block_scores, a.experts, a.combine_w, a.gap, a.sched);
+                                                     a.block_scores, a.experts, a.combine_w, a.gap, a.sched, a.T);
     return hipGetLastError();
+  }
+  if (route_block_fits(a.gs, a.E, a.k, a.block)) {
+    // larger block-routed forwards: one workgroup per block (softmax rows,
+    // block mean, top-k, weights), then the schedule
+    float* part = nullptr;
+    int S = 1;
+    hipError_t err = launch_router_partials(a.x, a.w, dt, a.T, a.H, a.E, a.probs, a.x_chunked, a.workspace,
+                                            a.ws_bytes, s, &part, &S);
+    if (err != hipSuccess) return err;
+    const size_t lds = fused_layout(a.gs, a.E, a.k, 1).total * sizeof(float);
+    if (a.E <= 256)
+      route_small_kernel<1, true><<<G, kThreads, lds, s>>>(part, S, a.bias, a.gs, a.E, a.k, a.gs, a.probs,
+                                                           a.logits, a.block_scores, a.experts, a.combine_w,
+                                                           a.gap, a.sched, a.T);
+    else
+      route_small_kernel<2, true><<<G, kThreads, lds, s>>>(part, S, a.bias, a.gs, a.E, a.k, a.gs, a.probs,
+                                                           a.logits, a.block_scores, a.experts, a.combine_w,
+                                                           a.gap, a.sched, a.T);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    return launch_schedule(a.experts, G, a.gs, a.k, a.E, a.sched, s);
   }
   hipError_t err;
   if (!a.block && dt == DMOE_BF16 && softmax_token_topk_fits(a.E)) {

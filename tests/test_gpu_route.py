@@ -43,7 +43,9 @@ def _snapshot(layer, routing):
 CASES = [("tiny_f32", {}), ("small_f32", {}), ("small_bf16", {}), ("small_bf16_zipf", {}),
          ("small_bf16_corr", {}), ("decode_b1", {}), ("decode_b16", {}),
          ("small_bf16", {"E": 32, "k": 32, "NB": 2, "bs": 24}), ("small_bf16", {"NB": 1, "bs": 1}),
-         ("small_f32", {"NB": 15, "bs": 1}), ("small_bf16", {"k": 1})]
+         ("small_f32", {"NB": 15, "bs": 1}), ("small_bf16", {"k": 1}),
+         # more blocks than one workgroup holds: one workgroup per block
+         ("small_bf16", {"NB": 40}), ("small_f32", {"NB": 200})]
 
 
 @pytest.mark.parametrize("routing", ["block", "token", "topp"])
