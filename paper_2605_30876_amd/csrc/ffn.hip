@@ -743,7 +743,7 @@ hipError_t launch_tile_bf16(const FfnParams& p, int ldh, int items, hipStream_t 
   return hipGetLastError();
 }
 
-constexpr int kSplitRows = 32;  // one-tile schedules: larger items go to the tile kernels
+constexpr int kSplitRows = 16;  // one-tile schedules: items of more than one pass go to the tile kernels
 
 // One-tile decode kernels for the items of <= p.split_rows rows and the tile
 // kernels for the others; each gate/up half runs before either down half.
@@ -796,11 +796,11 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
       case 1:
         // Items of a one-tile schedule average few rows, but an expert can
         // still collect many (a popular expert, a small Top-P coreset, the
-        // shared expert over more than 32 tokens).  The decode kernels keep a
+        // shared expert over more than 16 tokens).  The decode kernels keep a
         // wave's weight slice in registers across 16-row passes when it is
         // one burst; when it is not, they would stream the weights once per
-        // pass, so items past 32 rows go to the tile kernels, launched beside
-        // them.
+        // pass, so items of more than one pass (16 rows) go to the tile
+        // kernels, launched beside them.
         if (a.T > kSplitRows && (a.H / 128 > Shape<1>::kGuMax || ldh / 128 > Shape<1>::kDnMax)) {
           p.split_rows = kSplitRows;
           return launch_hybrid_bf16(p, ldh, items, s);

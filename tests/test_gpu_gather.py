@@ -17,7 +17,7 @@ from paper_2605_30876_amd.layer import MoELayer, pack_weights
 pytestmark = pytest.mark.gpu
 
 # hidden 4096, popular experts (Zipf bias) and a one-tile token schedule with
-# items of more than 32 rows: the decode kernels and the tile kernels share
+# items of more than 16 rows: the decode kernels and the tile kernels share
 # one launch
 HYBRID = MoEConfig("gather_hybrid", "bf16", H=4096, E=64, I=256, I_s=256, k=4, NB=2, bs=48, bias="zipf")
 
