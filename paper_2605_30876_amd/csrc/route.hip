@@ -185,7 +185,7 @@ bool route_fused_fits(int T, int E, int k, int gs, bool block) {
 }
 
 // One workgroup per block when a block's rows fit in LDS.
-bool route_block_fits(int gs, int E, int k, bool block) {
+static bool route_block_fits(int gs, int E, int k, bool block) {
   if (!block) return false;
   if (E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
   return fused_layout(gs, E, k, 1).total * sizeof(float) <= kMaxLdsBytes;
@@ -195,7 +195,7 @@ bool route_block_fits(int gs, int E, int k, bool block) {
 // the softmax in one launch when the router's partial logits allow it), the
 // coreset of each block, each token's top-k inside it, then the token-level
 // schedule.
-hipError_t launch_route_topp(const RouteArgs& a, dmoe_dtype dt, hipStream_t s) {
+static hipError_t launch_route_topp(const RouteArgs& a, dmoe_dtype dt, hipStream_t s) {
   hipError_t err;
   bool own_done = false;
   if (dt == DMOE_BF16 && softmax_token_topk_fits(a.E)) {
