@@ -45,7 +45,7 @@ CASES = [("tiny_f32", {}), ("small_f32", {}), ("small_bf16", {}), ("small_bf16_z
          ("small_bf16", {"E": 32, "k": 32, "NB": 2, "bs": 24}), ("small_bf16", {"NB": 1, "bs": 1}),
          ("small_f32", {"NB": 15, "bs": 1}), ("small_bf16", {"k": 1}),
          # more blocks than one workgroup holds: one workgroup per block
-         ("small_bf16", {"NB": 40}), ("small_f32", {"NB": 200})]
+         ("small_bf16", {"NB": 40}), ("small_f32", {"NB": 200}), ("small_bf16", {"E": 320, "NB": 30})]
 
 
 @pytest.mark.parametrize("routing", ["block", "token", "topp"])
