@@ -40,7 +40,6 @@ gap is below ``NEAR_TIE`` is a near-tie and is not compared index by index.
 """
 from __future__ import annotations
 
-import itertools
 import math
 
 import numpy as np
@@ -172,20 +171,24 @@ def token_route(probs: np.ndarray, k: int):
     return experts, gaps, w
 
 
-def valid_topk_sets(scores: np.ndarray, k: int, tol: float = NEAR_TIE):
-    """All k-sets a top-k may return when scores within ``tol`` of the k-th
-    largest are treated as tied (used only for near-tie groups)."""
+def valid_topk_set(scores: np.ndarray, chosen, k: int, tol: float = NEAR_TIE) -> bool:
+    """True iff ``chosen`` is a top-k a selection may return when two scores
+    within ``tol`` of each other may be ranked either way (near-ties; used only
+    to accept a GPU selection at a near-tie).
+
+    That holds iff ``chosen`` has k distinct ids and no expert left out beats a
+    chosen one by more than tol:  max_{a not in C} s_a <= min_{b in C} s_b + tol.
+    """
     s = np.asarray(scores, dtype=np.float64)
-    order = ranked(s)
-    if k >= s.shape[0]:
-        return [frozenset(order.tolist())]
-    kth = s[order[k - 1]]
-    sure = [int(e) for e in order if s[e] > kth + tol]
-    amb = [int(e) for e in order if abs(s[e] - kth) <= tol]
-    need = k - len(sure)
-    if need <= 0:
-        return [frozenset(order[:k].tolist())]
-    return [frozenset(sure + list(c)) for c in itertools.combinations(amb, need)]
+    ids = [int(e) for e in chosen]
+    C = sorted(set(ids))
+    if len(C) != k or len(ids) != k or k < 1 or C[0] < 0 or C[-1] >= s.shape[0]:
+        return False
+    inside = np.zeros(s.shape[0], dtype=bool)
+    inside[C] = True
+    if inside.all():
+        return True
+    return bool(s[~inside].max() <= s[inside].min() + tol)
 
 
 def unique_experts(experts: np.ndarray) -> np.ndarray:
@@ -274,25 +277,35 @@ def alg1_route(token_scores: np.ndarray, k: int, p: float, min_coreset: int | No
     return S, C, R
 
 
-def alg1_valid_coresets(S_norm: np.ndarray, p: float, min_size: int, tol: float = NEAR_TIE):
-    """The coresets Top-P may return when values within ``tol`` are treated as
-    tied: the cut may move by one where the cumulative mass is within tol of
-    p, and at each admissible size any near-tied ranking at the cut is valid
-    (used only to accept a GPU decision at a near-tie)."""
-    s = np.asarray(S_norm, dtype=np.float32)
+def alg1_valid_coreset(S_norm: np.ndarray, p: float, min_size: int, chosen, tol: float = NEAR_TIE) -> bool:
+    """True iff ``chosen`` is a coreset Top-P may return on the normalised
+    scores when near-ties may go either way (used only to accept a GPU coreset
+    at a near-tie): two scores within ``tol`` may be ranked either way, and a
+    cumulative mass within ``tol`` of p may count as reaching p or not.
+
+    Top-P walks a ranking and stops at the first size n >= min_size whose
+    cumulative mass reaches p (at the end of the ranking if none does).  So C
+    of size n is returned by some admissible ranking iff
+      * C is a near-tie top-n (``valid_topk_set``): it can be the first n;
+      * the walk may stop at n: n = E, or the mass of C reaches p - tol;
+      * the walk need not have stopped earlier: n - 1 < min_size, or the mass
+        of C without its last-ranked member stays below p + tol.  Cumulative
+        masses only grow along the walk, so only the step before n matters,
+        and the last-ranked member can be any member within tol of C's
+        smallest score; the largest such one leaves the smallest mass.
+    """
+    s = np.asarray(S_norm, dtype=np.float64)
     E = s.shape[0]
-    n_ref = top_p(s, p, min_size).size
-    order = ranked(s)
-    acc = np.cumsum(s[order].astype(np.float64))
-    sizes = {n_ref}
-    if n_ref - 1 >= max(min_size, 1) and acc[n_ref - 2] >= p - tol:
-        sizes.add(n_ref - 1)
-    if n_ref + 1 <= E and acc[n_ref - 1] < p + tol:
-        sizes.add(n_ref + 1)
-    out = set()
-    for n in sizes:
-        out.update(valid_topk_sets(s, n, tol))
-    return out
+    C = sorted({int(e) for e in chosen})
+    n = len(C)
+    if n < max(min_size, 1) or not valid_topk_set(s, C, n, tol):
+        return False
+    vals = s[C]
+    mass = math.fsum(vals.tolist())
+    last = float(vals[vals <= vals.min() + tol].max())
+    may_stop = n == E or mass >= p - tol
+    not_before = n - 1 < min_size or mass - last < p + tol
+    return bool(may_stop and not_before)
 
 
 # ---------------------------------------------------------------------------
@@ -403,4 +416,4 @@ def max_rel_err(y, y_ref) -> float:
     return float(np.max(np.abs(y - r))) / rms if rms > 0 else float(np.max(np.abs(y - r)))
 
 
-__all__ = [n for n in dir() if not n.startswith("_") and n not in ("annotations", "itertools", "math", "np")]
+__all__ = [n for n in dir() if not n.startswith("_") and n not in ("annotations", "math", "np")]

@@ -42,9 +42,9 @@ def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: lis
                 f" (gap {gap:.3g})")
             out[g] = idx
         else:
-            cands = O.valid_topk_sets(scores[g], k)
             gs = frozenset(gpu_sel[g].tolist())
-            assert gs in cands, f"{what} group {g}: near-tie but GPU set {sorted(gs)} is not a valid top-{k}"
+            assert O.valid_topk_set(scores[g], gpu_sel[g].tolist(), k), (
+                f"{what} group {g}: near-tie but GPU set {sorted(gs)} is not a valid top-{k}")
             order = O.ranked(scores[g])
             out[g] = [e for e in order if e in gs][:k]
             log.append({"what": what, "group": g, "gap": float(gap), "oracle": sorted(idx.tolist()),
@@ -203,7 +203,7 @@ def run_and_check_topp(cfg, d_gpu: dict, layer, sample_tokens=None, check_determ
         if cores[b] == C.tolist():
             coreset = C
         else:
-            assert frozenset(cores[b]) in O.alg1_valid_coresets(sn, p_thr, min_c), (
+            assert O.alg1_valid_coreset(sn, p_thr, min_c, cores[b]), (
                 f"block {b}: coreset {sorted(cores[b])} is not a valid Top-P coreset (oracle {sorted(C.tolist())})")
             coreset = np.asarray(cores[b], dtype=np.int32)
             report["near_ties"].append({"what": "coreset", "block": b})

@@ -132,9 +132,14 @@ def test_tie_break_lower_id_wins():
 
 def test_valid_sets_under_near_tie():
     s = np.array([0.5, 0.2, 0.2 + 1e-8, 0.1], dtype=np.float32)
-    sets = O.valid_topk_sets(s, 2)
-    assert set(sets) == {frozenset({0, 1}), frozenset({0, 2})}
-    assert O.valid_topk_sets(np.array([0.5, 0.3, 0.2]), 2) == [frozenset({0, 1})]
+    assert O.valid_topk_set(s, [0, 1], 2) and O.valid_topk_set(s, [2, 0], 2)
+    assert not O.valid_topk_set(s, [0, 3], 2) and not O.valid_topk_set(s, [1, 2], 2)
+    s = np.array([0.5, 0.3, 0.2])
+    assert O.valid_topk_set(s, [0, 1], 2) and not O.valid_topk_set(s, [0, 2], 2)
+    # malformed selections: repeated id, wrong size, id out of range
+    assert not O.valid_topk_set(s, [0, 0], 2)
+    assert not O.valid_topk_set(s, [0], 2)
+    assert not O.valid_topk_set(s, [0, 3], 2)
 
 
 # --------------------------------------------------------------------------
@@ -409,6 +414,58 @@ def _combine_shared_dropped(*a, **kw):
     return _combine_ok(*a[:6], None, None, None, **kw)
 
 
+def _rel_err_over_max(y, y_ref):
+    y, r = np.asarray(y, dtype=np.float64), np.asarray(y_ref, dtype=np.float64)
+    return float(np.max(np.abs(y - r))) / float(np.max(np.abs(r)))
+
+
+def _rel_err_over_mean_abs(y, y_ref):
+    y, r = np.asarray(y, dtype=np.float64), np.asarray(y_ref, dtype=np.float64)
+    return float(np.max(np.abs(y - r))) / float(np.mean(np.abs(r)))
+
+
+def _rel_err_first_row(y, y_ref):
+    y, r = np.atleast_2d(np.asarray(y, dtype=np.float64)), np.atleast_2d(np.asarray(y_ref, dtype=np.float64))
+    return float(np.max(np.abs(y[0] - r[0]))) / math.sqrt(float(np.mean(r * r)))
+
+
+def _expand_tiled(block_experts, block_size):
+    return np.tile(np.asarray(block_experts), (block_size, 1))
+
+
+def _topk_set_kth_relative(scores, chosen, k, tol=O.NEAR_TIE):
+    # every member within tol of the k-th score, or above it by more than tol
+    # (ties chain through the k-th score: too permissive)
+    s = np.asarray(scores, dtype=np.float64)
+    C = sorted(set(int(e) for e in chosen))
+    if len(C) != k:
+        return False
+    kth = s[O.ranked(s)[k - 1]]
+    sure = {e for e in range(s.size) if s[e] > kth + tol}
+    amb = {e for e in range(s.size) if abs(s[e] - kth) <= tol}
+    return sure <= set(C) <= sure | amb
+
+
+
+def _coreset_no_stop_check(S_norm, p, min_size, chosen, tol=O.NEAR_TIE):
+    # any near-tie top-n of an admissible size, whether the walk may stop there or not
+    return OM.valid_topk_set(S_norm, chosen, len(set(chosen)), tol) and len(set(chosen)) >= min_size
+
+
+def _coreset_cut_moves_one(S_norm, p, min_size, chosen, tol=O.NEAR_TIE):
+    # the reference size or one more, whatever the masses
+    n = len(set(chosen))
+    n_ref = O.top_p(np.asarray(S_norm, dtype=np.float32), p, min_size).size
+    return n in (n_ref, n_ref + 1) and OM.valid_topk_set(S_norm, chosen, n, tol)
+
+
+def _all_seeds(fn):
+    def run():
+        for seed in range(12):
+            fn(seed)
+    return run
+
+
 @pytest.mark.parametrize("attr,bad,pin", [
     ("router_logits", _logits_bias_dropped, "test_zero_input_gives_zero_output"),
     ("combine", _combine_shared_dropped, "test_single_expert_scalar_loops"),
@@ -419,6 +476,14 @@ def _combine_shared_dropped(*a, **kw):
     ("topk", _topk_ascending, "test_golden_token_and_block_routing"),
     ("renormalised_weights", _unnormalised, "test_weights_and_distributions_sum_to_one"),
     ("block_scores", _block_sum_last_token_dropped, "test_golden_token_and_block_routing"),
+    ("max_rel_err", _rel_err_over_max, "test_max_rel_err_hand_values"),
+    ("max_rel_err", _rel_err_over_mean_abs, "test_max_rel_err_hand_values"),
+    ("max_rel_err", _rel_err_first_row, "test_max_rel_err_hand_values"),
+    ("expand_block_experts", _expand_tiled, "test_expand_block_experts_three_blocks"),
+    ("valid_topk_set", _topk_set_kth_relative, "test_valid_topk_set_equals_brute_force"),
+    ("alg1_valid_coreset", _coreset_no_stop_check, "test_alg1_valid_coreset_equals_brute_force"),
+    ("alg1_valid_coreset", _coreset_cut_moves_one, "test_alg1_valid_coreset_equals_brute_force"),
+    ("alg1_valid_coreset", _coreset_no_stop_check, "test_alg1_valid_coreset_hand_example"),
 ])
 def test_planted_mistake_is_caught(monkeypatch, attr, bad, pin):
     monkeypatch.setattr(O, attr, bad)
@@ -429,6 +494,8 @@ def test_planted_mistake_is_caught(monkeypatch, attr, bad, pin):
             fn("tiny_f32")
         elif pin == "test_zero_input_gives_zero_output":
             fn("block")
+        elif pin.endswith("_equals_brute_force"):
+            _all_seeds(fn)()
         else:
             fn()
 
@@ -503,9 +570,138 @@ def test_alg1_scores_are_topk_masked_sums():
     assert np.count_nonzero(S) <= bs * k
 
 
-def test_alg1_valid_coresets_contains_reference():
+def test_alg1_valid_coreset_contains_reference():
     rng = np.random.default_rng(3)
     probs = _probs(rng, 8, 32)
     S, C, _ = O.alg1_route(probs, 4, 0.6)
     Sn = O.normalize(S)
-    assert frozenset(C.tolist()) in O.alg1_valid_coresets(Sn, 0.6, 4)
+    assert O.alg1_valid_coreset(Sn, 0.6, 4, C.tolist())
+
+
+# ---- near-tie acceptance, pinned by brute force over admissible rankings ----
+#
+# Near-tie reading: two scores within tol may be ranked either way, and a
+# cumulative mass within tol of p may count as reaching p or not.  A ranking
+# is admissible when no expert is placed after one it beats by more than tol.
+# The brute force walks every admissible ranking of a small score vector (all
+# permutations, filtered) and collects what top-k and Top-P return on it,
+# with the mass comparison taken either way inside the tolerance band.  Scores
+# sit on a grid of 0.01 and tol = 0.0275, p = 0.003 + a multiple of 0.01, so
+# no comparison lands on a band edge and float64 decides each one exactly.
+
+_TOL = 0.0275
+
+
+def _admissible_rankings(s, tol):
+    E = len(s)
+    for perm in itertools.permutations(range(E)):
+        if all(not (s[perm[j]] > s[perm[i]] + tol) for i in range(E) for j in range(i + 1, E)):
+            yield perm
+
+
+def _brute_topk_sets(s, k, tol):
+    return {frozenset(perm[:k]) for perm in _admissible_rankings(s, tol)}
+
+
+def _brute_topp_sets(s, p, min_size, tol):
+    E = len(s)
+    out = set()
+    for perm in _admissible_rankings(s, tol):
+        acc = np.cumsum([s[e] for e in perm])
+        for n in range(min_size, E + 1):
+            may_stop = n == E or acc[n - 1] >= p - tol
+            forced_before = any(acc[m - 1] >= p + tol for m in range(min_size, n))
+            if may_stop and not forced_before:
+                out.add(frozenset(perm[:n]))
+    return out
+
+
+def _grid_scores(rng, E):
+    # values 0.00 .. 0.40 on a 0.01 grid, drawn from a few clusters so that
+    # near-ties (differences of 0.01 and 0.02) and exact ties are common
+    centres = rng.integers(0, 41, size=3)
+    v = centres[rng.integers(0, 3, size=E)] + rng.integers(-3, 4, size=E)
+    return np.clip(v, 0, 40).astype(np.float64) / 100.0
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_valid_topk_set_equals_brute_force(seed):
+    rng = np.random.default_rng(100 + seed)
+    E = int(rng.integers(3, 8))
+    s = _grid_scores(rng, E)
+    for k in range(1, E + 1):
+        ref = _brute_topk_sets(s, k, _TOL)
+        for r in range(1, E + 1):
+            for C in itertools.combinations(range(E), r):
+                assert O.valid_topk_set(s, C, k, _TOL) == (frozenset(C) in ref), (s.tolist(), k, C)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_alg1_valid_coreset_equals_brute_force(seed):
+    rng = np.random.default_rng(200 + seed)
+    E = int(rng.integers(3, 8))
+    s = _grid_scores(rng, E)
+    total = float(s.sum())
+    for min_size in (1, 2, 3):
+        if min_size > E:
+            continue
+        for p in (0.003 + 0.01 * np.arange(0, int(total * 100) + 2, 3)).tolist():
+            ref = _brute_topp_sets(s, p, min_size, _TOL)
+            for r in range(1, E + 1):
+                for C in itertools.combinations(range(E), r):
+                    got = O.alg1_valid_coreset(s, p, min_size, C, _TOL)
+                    assert got == (frozenset(C) in ref), (s.tolist(), p, min_size, C)
+
+
+def test_alg1_valid_coreset_hand_example():
+    """Hand-derived case: scores 0.30, 0.29, 0.20, 0.10, 0.11 (ids 0..4),
+    tol 0.0275, min size 1.  p = 0.493: the walk 0, 1, 2 reaches 0.79 at
+    three experts, 1, 0 reaches 0.59 at two (>= p + tol: stops there), so
+    {0, 1} is the coreset and no ranking can stop at one expert (0.30 and
+    0.29 are below p - tol = 0.4655) or go on to three.  p = 0.603: two
+    experts reach 0.59, inside the band [0.5755, 0.6305), so both {0, 1} and
+    {0, 1, 2} are valid; {0, 1, 4} is not, since 2 beats 4 by 0.09."""
+    s = np.array([0.30, 0.29, 0.20, 0.10, 0.11])
+    ok = lambda p, C: O.alg1_valid_coreset(s, p, 1, C, _TOL)  # noqa: E731
+    assert ok(0.493, [0, 1]) and not ok(0.493, [0]) and not ok(0.493, [1]) and not ok(0.493, [0, 1, 2])
+    assert ok(0.603, [0, 1]) and ok(0.603, [0, 1, 2]) and not ok(0.603, [0, 1, 4]) and not ok(0.603, [0, 2])
+    # min size 3 forces a third expert even when two reach p
+    assert not O.alg1_valid_coreset(s, 0.493, 3, [0, 1], _TOL) and O.alg1_valid_coreset(s, 0.493, 3, [0, 1, 2], _TOL)
+
+
+# ---- max_rel_err and expand_block_experts: hand-computed values -------------
+
+def test_max_rel_err_hand_values():
+    # y_ref = [3, 4]: RMS = sqrt((9 + 16) / 2) = 5 / sqrt(2); |dy| max = 1
+    assert O.max_rel_err([3.0, 5.0], [3.0, 4.0]) == pytest.approx(math.sqrt(2) / 5, rel=1e-12)
+    # RMS, max|.| and mean|.| of [1, 1, 1, 5] are sqrt(7), 5 and 2; the
+    # largest error (0.7, negative) sits in the last row, after a 0.5 one
+    ref = np.array([[1.0, 1.0], [1.0, 5.0]])
+    y = ref + np.array([[0.0, 0.5], [0.0, -0.7]])
+    assert O.max_rel_err(y, ref) == pytest.approx(0.7 / math.sqrt(7), rel=1e-12)
+    # all-zero reference: the plain maximum error
+    assert O.max_rel_err([0.0, -0.25], [0.0, 0.0]) == 0.25
+    assert O.max_rel_err(ref, ref) == 0.0
+
+
+def test_expand_block_experts_three_blocks():
+    ex = np.array([[4, 1], [0, 2], [3, 5]], dtype=np.int32)
+    got = O.expand_block_experts(ex, 2)
+    assert got.tolist() == [[4, 1], [4, 1], [0, 2], [0, 2], [3, 5], [3, 5]]
+    assert O.expand_block_experts(ex, 1).tolist() == ex.tolist()
+
+
+def test_hbm_bytes_from_array_sizes():
+    """hbm_bytes counted from the arrays one forward touches: the weights of
+    each unique expert and of the shared expert, the router, x and y."""
+    d = _tiny_layer(E=6, k=2, H=8, I=4, I_s=3, T=6, seed=4)
+    out = O.moe_forward(d, 2, 3, "token")
+    used = sorted(set(out["experts"].reshape(-1).tolist()))
+    touched = sum(d[n][e].nbytes for e in used for n in ("w_gate", "w_up", "w_down"))
+    touched += d["ws_gate"].nbytes + d["ws_up"].nbytes + d["ws_down"].nbytes + d["w_router"].nbytes
+    touched += 2 * d["x"].nbytes
+    assert O.hbm_bytes(len(used), 8, 4, 3, 6, 6, 4) == touched
+    # flops: 2 per multiply-add of the router, three matrices per routed
+    # (token, expert) pair and the shared expert per token
+    macs = 6 * 6 * 8 + 6 * 2 * 3 * 8 * 4 + 6 * 3 * 8 * 3
+    assert O.flops(6, 8, 6, 4, 3, 2) == 2 * macs
