@@ -3,15 +3,20 @@
 block routing vs token routing, on one MI355X.
 
 One step = one whole MoE layer forward (router -> top-k -> unique-expert
-schedule -> expert FFN -> combine) over one batch of tokens.  Steps rotate
-through ``--layers`` layers with distinct weights and hidden states, so that
-the experts a step streams were last touched more than a GiB of traffic
-earlier and cannot be served from the 256 MB Infinity Cache.
+schedule -> expert FFN -> combine) over one batch of tokens, with the layer
+output stored in fp32 (the configuration the parity tests check).  Steps
+rotate through ``--layers`` layers with distinct weights and hidden states,
+so that the experts a step streams were last touched more than a GiB of
+traffic earlier and cannot be served from the 256 MB Infinity Cache.
 
 Prints ONE JSON line.  ``value`` is the block-routed MoE-layer time per decode
-step in microseconds; the token-routed baseline, unique expert counts, HBM
-bandwidth and the expert-FFN roofline are reported beside it, with the CPU
-oracle timed on a bounded sample as ``cpu_baseline``.
+step in microseconds (wall clock around exactly ``--steps`` steps).  Beside it:
+the token-routed baseline and Alg. 1 with the Top-P coreset on the same layers,
+unique expert counts, HBM bandwidth, the expert-FFN roofline, the CPU oracle
+timed on a bounded sample as ``cpu_baseline`` (block and token routing), a
+chained 19-layer decode step (``decode_step_19_layers``) and the larger
+workloads (``workloads``: 16 sequences, the Zipf-biased large layer and 64
+blocks of 64 correlated tokens; block, token and Top-P routing each).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config decode_b1]
     python bench.py --sweep      # paper-shaped sweeps on the decode layer shape
@@ -28,6 +33,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import platform
 import statistics
 import sys
 import time
@@ -39,13 +45,15 @@ if ROOT not in sys.path:
 METRIC = "MoE-layer µs/decode step + achieved HBM GB/s (% peak), block vs token routing"
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E peak (AMD specification)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_traffic.json")
+STEP_LAYERS = 19  # MoE layers of the paper's model (Sec. 4.1)
+WORKLOADS = ("decode_b16", "large_zipf_b8", "corr_b64x64")
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2048, help="timed steps per routing mode")
-    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--steps", type=int, default=1160, help="timed steps per routing mode")
+    ap.add_argument("--warmup", type=int, default=58)
     ap.add_argument("--config", default="decode_b1")
     ap.add_argument("--layers", type=int, default=0, help="distinct layers to rotate through (0: auto)")
     ap.add_argument("--routing", choices=["all", "block", "token", "topp"], default="all",
@@ -54,7 +62,11 @@ def parse():
     ap.add_argument("--sweep", action="store_true", help="run the paper-shaped sweeps instead")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle timing per mode")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the chained decode step and the larger workloads")
+    ap.add_argument("--workloads", default=",".join(WORKLOADS),
+                    help="comma-separated larger workloads reported beside the headline ('' for none)")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0, help="budget of the oracle timing per mode")
     ap.add_argument("--ffn-only", action="store_true",
                     help="only replay the expert FFN (for hardware-counter runs)")
     ap.add_argument("--seed", type=int, default=0)
@@ -71,6 +83,212 @@ def source_hash() -> str:
     from paper_2605_30876_amd.build import ffn_source_hash
 
     return ffn_source_hash()
+
+
+class Runner:
+    """Exactly n calls fn(0), fn(1), ... (layer i % NL), timed.
+
+    With graphs: one HIP graph holds a whole rotation (fn(0..NL-1)) and is
+    replayed n // NL times, then a graph of fn(0..r-1) for the remainder r,
+    so any n is exact.  Returns (wall seconds, GPU-event seconds); the events
+    are recorded on the stream the graphs replay on."""
+
+    def __init__(self, torch, NL: int, fn, use_graph: bool = True):
+        self.torch, self.NL, self.fn, self.use_graph = torch, NL, fn, use_graph
+        self.graphs = {}
+        self.stream = torch.cuda.Stream() if use_graph else None
+
+    def _graph(self, n: int):
+        if n not in self.graphs:
+            torch = self.torch
+            self.stream.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(self.stream):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=self.stream):
+                    for i in range(n):
+                        self.fn(i)
+            torch.cuda.current_stream().wait_stream(self.stream)
+            torch.cuda.synchronize()
+            self.graphs[n] = g
+        return self.graphs[n]
+
+    def enqueue(self, n: int):
+        if not self.use_graph:
+            for i in range(n):
+                self.fn(i % self.NL)
+            return
+        full, rem = divmod(n, self.NL)
+        g_all = self._graph(self.NL) if full else None
+        g_rem = self._graph(rem) if rem else None
+        with self.torch.cuda.stream(self.stream):
+            for _ in range(full):
+                g_all.replay()
+            if rem:
+                g_rem.replay()
+
+    def time(self, n: int):
+        torch = self.torch
+        self.enqueue(min(n, self.NL))  # captures (outside the timed region) and warms both graphs
+        if n % self.NL:
+            self.enqueue(n % self.NL)
+        torch.cuda.synchronize()
+        s = self.stream or torch.cuda.current_stream()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        w0 = time.perf_counter()
+        ev0.record(s)
+        self.enqueue(n)
+        ev1.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        return wall, ev0.elapsed_time(ev1) / 1e3
+
+    def close(self):
+        self.graphs.clear()
+
+
+def auto_layers(torch, cfg, B_e, B_s, min_bytes=1.5 * 2**30, cap=64):
+    """Layers to rotate through: one rotation streams >= min_bytes of distinct
+    selected experts (block routing streams at most k per block), within half
+    the free device memory."""
+    per_step = min(cfg.E, cfg.NB * cfg.k) * B_e + B_s
+    layer_bytes = cfg.E * B_e + B_s
+    free = torch.cuda.mem_get_info()[0]
+    return max(2, min(cap, -(-int(min_bytes) // per_step), int(0.5 * free // layer_bytes)))
+
+
+def build_layers(torch, cfg, NL, seed, dev, top_p, keep_host0=False):
+    from dmoe_synth import make_inputs
+    from paper_2605_30876_amd.layer import MoELayer, pack_weights
+
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    layers, host0 = [], None
+    for l in range(NL):
+        d = make_inputs(cfg, seed=seed, layer=l, device=dev)
+        if l == 0 and keep_host0:
+            host0 = {k: (None if v is None else v.to("cpu")) for k, v in d.items()}
+        w = pack_weights(d)  # the layer keeps only the packed expert weights
+        layers.append((d["x"], w, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
+                                           device=dev, out_dtype=torch.float32, top_p=top_p)))
+        del d
+    torch.cuda.synchronize()
+    return layers, host0
+
+
+def measure_modes(torch, cfg, layers, modes, steps, warmup, use_graph, ffn_only=False):
+    """Per routing mode: whole-layer time over exactly `steps` steps and the
+    expert FFN's time over the same number of launches."""
+    from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes
+
+    NL = len(layers)
+    eb, B_e, B_s = element_bytes(cfg), expert_bytes(cfg), shared_bytes(cfg)
+    results = {}
+    for routing in modes:
+        def step(l, routing=routing):
+            x, w, m = layers[l]
+            m.forward(x, w, routing)
+
+        def ffn(l, routing=routing):
+            _, w, m = layers[l]
+            m.experts_ffn(w, routing)
+
+        for i in range(max(warmup, NL)):
+            step(i % NL)
+        torch.cuda.synchronize()
+        n_unique = [int(m.sched.n_unique[0]) for _, _, m in layers]
+        U = statistics.mean(n_unique)
+        ffn_bytes = U * B_e + B_s
+        r_ffn = Runner(torch, NL, ffn, use_graph)
+        if ffn_only:
+            _, ffn_s = r_ffn.time(steps)
+            results[routing] = {"ffn_us": ffn_s / steps * 1e6, "n_unique": n_unique}
+            log(f"[bench] {cfg.name} {routing}: expert FFN {ffn_s / steps * 1e6:.2f} us/launch")
+            r_ffn.close()
+            continue
+        r_step = Runner(torch, NL, step, use_graph)
+        wall, gpu_s = r_step.time(steps)
+        _, ffn_s = r_ffn.time(steps)
+        r_step.close()
+        r_ffn.close()
+        us = wall / steps * 1e6
+        layer_bytes = ffn_bytes + cfg.E * cfg.H * eb + cfg.T * cfg.H * eb + cfg.T * cfg.H * 4
+        ffn_us = ffn_s / steps * 1e6
+        results[routing] = {
+            "us_per_step": round(us, 3),
+            "gpu_event_us_per_step": round(gpu_s / steps * 1e6, 3),
+            "tokens_per_s": round(cfg.T / (us * 1e-6), 1),
+            "unique_experts_per_forward": round(U, 2),
+            "hbm_bytes_per_step": int(layer_bytes),
+            "hbm_gbps": round(layer_bytes / (us * 1e-6) / 1e9, 1),
+            "frac_peak": round(layer_bytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+            "expert_ffn_us": round(ffn_us, 3),
+            "expert_ffn_gbps": round(ffn_bytes / (ffn_us * 1e-6) / 1e9, 1),
+            "expert_ffn_frac_peak": round(ffn_bytes / (ffn_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+            "expert_ffn_bytes": int(ffn_bytes),
+        }
+        log(f"[bench] {cfg.name} {routing}: {us:.2f} us/step (events {gpu_s / steps * 1e6:.2f}), U={U:.1f}, "
+            f"{results[routing]['hbm_gbps']} GB/s layer; expert FFN {ffn_us:.2f} us = "
+            f"{results[routing]['expert_ffn_gbps']} GB/s")
+    return results
+
+
+def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
+    """A decode step of STEP_LAYERS chained MoE layers (layer l's input plus
+    output is layer l+1's input), timed per mode; the residual adds alone
+    are timed too, so the MoE part of the step is reported without them."""
+    from paper_2605_30876_amd.layer import decode_step
+
+    L = STEP_LAYERS
+    sub = layers[:L]
+    ms = [m for _, _, m in sub]
+    ws = [w for _, w, _ in sub]
+    xs = [sub[0][0]] + [torch.empty_like(sub[0][0]) for _ in range(L - 1)]
+    out = {"layers": L}
+
+    def glue(_i):
+        for l in range(L - 1):
+            torch.add(xs[l], ms[l].y, out=xs[l + 1])
+
+    for routing in modes:
+        decode_step(ms, ws, xs, routing)
+        torch.cuda.synchronize()
+        r = Runner(torch, 1, lambda _i, routing=routing: decode_step(ms, ws, xs, routing), use_graph)
+        wall, gpu_s = r.time(steps)
+        r.close()
+        U = statistics.mean(int(m.sched.n_unique[0]) for m in ms)
+        out[routing] = {"us_per_step": round(wall / steps * 1e6, 2), "gpu_event_us_per_step": round(gpu_s / steps * 1e6, 2),
+                        "unique_experts_per_layer": round(U, 2)}
+    r = Runner(torch, 1, glue, use_graph)
+    wall, _ = r.time(steps)
+    r.close()
+    out["residual_adds_us"] = round(wall / steps * 1e6, 2)
+    for routing in modes:
+        out[routing]["moe_us_per_step"] = round(out[routing]["us_per_step"] - out["residual_adds_us"], 2)
+    log(f"[bench] {L}-layer decode step: " + ", ".join(f"{m} {out[m]['us_per_step']} us" for m in modes)
+        + f" (residual adds {out['residual_adds_us']} us)")
+    return out
+
+
+def workload_figures(torch, name, args, dev, modes):
+    from dmoe_synth import get_config
+    from dmoe_synth.generate import expert_bytes, shared_bytes
+
+    cfg = get_config(name)
+    NL = auto_layers(torch, cfg, expert_bytes(cfg), shared_bytes(cfg), min_bytes=1.0 * 2**30, cap=8)
+    layers, _ = build_layers(torch, cfg, NL, args.seed, dev, args.top_p)
+    steps = max(2 * NL, 16)
+    res = measure_modes(torch, cfg, layers, modes, steps, NL, not args.no_graph)
+    out = {"workload": f"hidden {cfg.H}, {cfg.E} experts of intermediate {cfg.I} + shared {cfg.I_s}, "
+                       f"top-{cfg.k}, {cfg.NB} x {cfg.bs} = {cfg.T} tokens",
+           "layers_rotated": NL, "steps": steps}
+    for m, r in res.items():
+        out[m] = {k: r[k] for k in ("us_per_step", "tokens_per_s", "unique_experts_per_forward", "expert_ffn_us",
+                                    "expert_ffn_gbps", "expert_ffn_frac_peak", "hbm_gbps")}
+    if "block" in res and "token" in res:
+        out["token_over_block_time"] = round(res["token"]["us_per_step"] / res["block"]["us_per_step"], 3)
+    del layers
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -96,129 +314,46 @@ def main():
     if args.sweep:
         return sweep(args, torch)
 
-    from dmoe_synth import get_config, make_inputs
-    from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes
+    from dmoe_synth import get_config
+    from dmoe_synth.generate import expert_bytes, shared_bytes
     from paper_2605_30876_amd import lib
-    from paper_2605_30876_amd.layer import MoELayer, pack_weights
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lib.load()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     cfg = get_config(args.config)
-    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
-    eb = element_bytes(cfg)
     B_e, B_s = expert_bytes(cfg), shared_bytes(cfg)
-
-    # Enough layers that one rotation streams >= 1.5 GiB of distinct selected
-    # experts (block routing streams k experts per block at most).
     if args.layers <= 0:
-        per_step = min(cfg.E, cfg.NB * cfg.k) * B_e + B_s
-        layer_bytes = cfg.E * B_e + B_s
-        free = torch.cuda.mem_get_info()[0]
-        args.layers = max(2, min(64, -(-int(1.5 * 2**30) // per_step), int(0.5 * free // layer_bytes)))
+        args.layers = auto_layers(torch, cfg, B_e, B_s)
     NL = args.layers
-    steps = -(-args.steps // NL) * NL  # whole rotations
+    steps, warmup = max(1, args.steps), max(0, args.warmup)
     log(f"[bench] config {cfg.name}: T={cfg.T} H={cfg.H} E={cfg.E} I={cfg.I} I_s={cfg.I_s} k={cfg.k}; "
         f"{NL} layers ({NL * (cfg.E * B_e + B_s) / 2**30:.1f} GiB of weights), {steps} steps per mode")
 
     t0 = time.time()
-    layers = []
-    for l in range(NL):
-        d = make_inputs(cfg, seed=args.seed, layer=l, device=dev)
-        if l == 0 and not args.no_cpu_baseline:
-            d0_host = {k: (None if v is None else v.to("cpu")) for k, v in d.items()}
-        w = pack_weights(d)  # the layer keeps only the packed expert weights
-        layers.append((d["x"], w, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
-                                           device=dev, out_dtype=dt, top_p=args.top_p)))
-        del d
-    torch.cuda.synchronize()
+    layers, host0 = build_layers(torch, cfg, NL, args.seed, dev, args.top_p, keep_host0=not args.no_cpu_baseline)
     log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
 
     modes = ["block", "token", "topp"] if args.routing == "all" else [args.routing]
-    results = {}
-    for routing in modes:
-        def step(l, routing=routing):
-            x, w, m = layers[l]
-            m.forward(x, w, routing)
-
-        def ffn(l, routing=routing):
-            _, w, m = layers[l]
-            m.experts_ffn(w, routing)
-
-        for i in range(max(args.warmup, NL)):
-            step(i % NL)
-        torch.cuda.synchronize()
-        n_unique = [int(m.sched.n_unique[0]) for _, _, m in layers]
-
-        graph = ffn_graph = None
-        if not args.no_graph:
-            stream = torch.cuda.Stream()
-            stream.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(stream):
-                graph = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(graph, stream=stream):
-                    for l in range(NL):
-                        step(l)
-                ffn_graph = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(ffn_graph, stream=stream):
-                    for l in range(NL):
-                        ffn(l)
-            torch.cuda.current_stream().wait_stream(stream)
-            for _ in range(2):
-                graph.replay()
-                ffn_graph.replay()
-            torch.cuda.synchronize()
-
-        def run(n_steps, fn_graph, fn_eager):
-            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            w0 = time.perf_counter()
-            ev0.record()
-            if fn_graph is not None:
-                for _ in range(n_steps // NL):
-                    fn_graph.replay()
-            else:
-                for i in range(n_steps):
-                    fn_eager(i % NL)
-            ev1.record()
-            torch.cuda.synchronize()
-            wall = time.perf_counter() - w0
-            return wall, ev0.elapsed_time(ev1) / 1e3
-
-        if args.ffn_only:
-            wall, gpu_s = run(steps, ffn_graph, ffn)
-            results[routing] = {"ffn_us": gpu_s / steps * 1e6, "n_unique": n_unique}
-            log(f"[bench] {routing}: expert FFN {gpu_s / steps * 1e6:.2f} us/launch")
-            continue
-
-        wall, gpu_s = run(steps, graph, step)
-        wall_f, ffn_s = run(steps, ffn_graph, ffn)
-        U = statistics.mean(n_unique)
-        us = wall / steps * 1e6
-        layer_bytes = U * B_e + B_s + cfg.E * cfg.H * eb + cfg.T * cfg.H * eb + cfg.T * cfg.H * eb
-        ffn_bytes = U * B_e + B_s
-        ffn_us = ffn_s / steps * 1e6
-        results[routing] = {
-            "us_per_step": round(us, 3),
-            "gpu_event_us_per_step": round(gpu_s / steps * 1e6, 3),
-            "tokens_per_s": round(cfg.T / (us * 1e-6), 1),
-            "unique_experts_per_forward": round(U, 2),
-            "hbm_bytes_per_step": int(layer_bytes),
-            "hbm_gbps": round(layer_bytes / (us * 1e-6) / 1e9, 1),
-            "frac_peak": round(layer_bytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
-            "expert_ffn_us": round(ffn_us, 3),
-            "expert_ffn_gbps": round(ffn_bytes / (ffn_us * 1e-6) / 1e9, 1),
-            "expert_ffn_bytes": int(ffn_bytes),
-        }
-        log(f"[bench] {routing}: {us:.2f} us/step (events {gpu_s / steps * 1e6:.2f}), U={U:.1f}, "
-            f"{results[routing]['hbm_gbps']} GB/s layer; expert FFN {ffn_us:.2f} us = "
-            f"{results[routing]['expert_ffn_gbps']} GB/s")
-        del graph, ffn_graph
-
+    results = measure_modes(torch, cfg, layers, modes, steps, warmup, not args.no_graph, args.ffn_only)
     if args.ffn_only:
         print(json.dumps({"ffn_only": results, "config": cfg.name, "layers": NL, "steps": steps}))
         return 0
+
+    chain = None
+    if not args.no_extras and NL >= STEP_LAYERS:
+        chain = chained_step(torch, cfg, layers, modes, not args.no_graph)
+    del layers
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    workloads = {}
+    if not args.no_extras:
+        for name in [w for w in args.workloads.split(",") if w and w != cfg.name]:
+            t0 = time.time()
+            workloads[name] = workload_figures(torch, name, args, dev, modes)
+            log(f"[bench] workload {name} done in {time.time() - t0:.1f}s")
 
     main_mode = "block" if "block" in results else modes[0]
     r = results[main_mode]
@@ -226,12 +361,12 @@ def main():
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as fh:
             tr = json.load(fh)
-        if tr.get("source_hash") == source_hash() and tr.get("config") == cfg.name:
-            traffic = tr.get("hbm_bytes_per_launch", {}).get(main_mode)
+        if tr.get("source_hash") == source_hash():
+            traffic = tr.get("configs", {}).get(cfg.name, {}).get(main_mode, {}).get("ffn_bytes_per_launch")
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, d0_host, main_mode, args.cpu_seconds)
+        cpu = cpu_baseline(cfg, host0, [m for m in ("block", "token") if m in modes], args.cpu_seconds)
 
     out = {
         "metric": METRIC,
@@ -239,7 +374,7 @@ def main():
         "unit": "us/step",
         "n_gpus": 1,
         "steps": steps,
-        "warmup": max(args.warmup, NL),
+        "warmup": warmup,
         "ms_per_step": round(r["us_per_step"] / 1e3, 6),
         "higher_is_better": False,
         "scaling": "weak",
@@ -248,7 +383,7 @@ def main():
         "data": "synthetic (seeded N(0,1) hidden states, N(0,0.02^2) weights)",
         "config": {"workload": f"{cfg.name}: one MoE layer, hidden {cfg.H}, {cfg.E} routed experts of "
                                f"SwiGLU intermediate {cfg.I} + shared {cfg.I_s}, top-{cfg.k}, "
-                               f"{cfg.NB} sequence(s) x block {cfg.bs} = {cfg.T} tokens per forward",
+                               f"{cfg.NB} sequence(s) x block {cfg.bs} = {cfg.T} tokens per forward, fp32 output",
                    "routing": main_mode, "layers_rotated": NL, "graph": not args.no_graph},
         "roofline": {"bound": "hbm", "kernel": "expert FFN (gate/up+SwiGLU and down launches)",
                      "achieved": r["expert_ffn_gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -260,36 +395,24 @@ def main():
     }
     if "block" in results and "token" in results:
         out["token_over_block_time"] = round(results["token"]["us_per_step"] / results["block"]["us_per_step"], 3)
+    if chain is not None:
+        out["decode_step_19_layers"] = chain
+    if workloads:
+        out["workloads"] = workloads
     print(json.dumps(out))
     return 0
 
 
 def graph_timer(torch, NL: int):
-    """Returns time(fn, steps): captures fn(0..NL-1) in one HIP graph, replays
-    it steps/NL times between two events and returns microseconds per fn call
-    (the events are on the stream the graph replays on)."""
+    """Returns time(fn, steps): microseconds per fn call over a whole number
+    of rotations of fn(0..NL-1) replayed from one HIP graph."""
 
     def time_fn(fn, steps):
-        reps = max(1, -(-steps // NL))
-        stream = torch.cuda.Stream()
-        stream.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(stream):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=stream):
-                for l in range(NL):
-                    fn(l)
-        torch.cuda.current_stream().wait_stream(stream)
-        for _ in range(2):
-            g.replay()
-        torch.cuda.synchronize()
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for _ in range(reps):
-            g.replay()
-        ev1.record()
-        torch.cuda.synchronize()
-        del g
-        return ev0.elapsed_time(ev1) * 1e3 / (reps * NL)
+        r = Runner(torch, NL, fn)
+        n = max(1, -(-steps // NL)) * NL
+        _, gpu_s = r.time(n)
+        r.close()
+        return gpu_s * 1e6 / n
 
     return time_fn
 
@@ -330,7 +453,7 @@ def sweep(args, torch):
     def layer_point(cfg, routings):
         """Whole-layer and expert-FFN time of each routing mode at one shape."""
         xs = [make_hidden_states(cfg, seed=args.seed, layer=l, device=dev) for l in range(NL)]
-        ms = [MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device=dev, out_dtype=torch.bfloat16,
+        ms = [MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device=dev, out_dtype=torch.float32,
                        top_p=args.top_p) for _ in range(NL)]
         res = {}
         for routing in routings:
@@ -355,7 +478,7 @@ def sweep(args, torch):
     # per token, all U experts used), then the token-level schedule.
     cfg = base
     xs = [make_hidden_states(cfg, seed=args.seed, layer=l, device=dev) for l in range(NL)]
-    ms = [MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device=dev, out_dtype=torch.bfloat16)
+    ms = [MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device=dev, out_dtype=torch.float32)
           for _ in range(NL)]
     for l in range(NL):  # the router writes the FFN's chunk-major activations
         ms[l].route(xs[l], weights[l]["w_router"], None, "token")
@@ -386,9 +509,20 @@ def sweep(args, torch):
     return 0
 
 
-def cpu_baseline(cfg, d, routing, budget_s):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(cfg, d, routings, budget_s):
     """The CPU oracle, as it stands, timed on the host on one layer's inputs
-    (host copies of the tensors the GPU runs on)."""
+    (host copies of the tensors the GPU runs on), per routing mode."""
     import numpy as np
 
     import oracle as O
@@ -398,19 +532,28 @@ def cpu_baseline(cfg, d, routing, budget_s):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: numpy BLAS uses the visible cores
         threads = os.cpu_count()
-    times = []
-    t_end = time.perf_counter() + budget_s
-    while time.perf_counter() < t_end or not times:
-        t0 = time.perf_counter()
-        O.moe_forward(d, cfg.k, cfg.bs, routing)
-        times.append(time.perf_counter() - t0)
-        if len(times) >= 50:
-            break
-    us = float(np.median(times)) * 1e6
-    log(f"[bench] cpu oracle ({routing}): {us:.0f} us/step over {len(times)} forwards, {threads} threads")
-    return {"value": round(us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
-            "sample": f"{len(times)} {routing}-routed forwards of one {cfg.name} layer "
-                      f"({cfg.T} tokens), median; inputs already in host memory"}
+    per = {}
+    for routing in routings:
+        times = []
+        t_end = time.perf_counter() + budget_s
+        while time.perf_counter() < t_end or not times:
+            t0 = time.perf_counter()
+            O.moe_forward(d, cfg.k, cfg.bs, routing)
+            times.append(time.perf_counter() - t0)
+            if len(times) >= 50:
+                break
+        us = float(np.median(times)) * 1e6
+        per[routing] = {"value": round(us, 1), "forwards": len(times)}
+        log(f"[bench] cpu oracle ({routing}): {us:.0f} us/step over {len(times)} forwards, {threads} threads")
+    main = routings[0]
+    out = {"value": per[main]["value"], "unit": "us/step", "cores": threads, "kind": "oracle",
+           "sample": f"{per[main]['forwards']} {main}-routed forwards of one {cfg.name} layer "
+                     f"({cfg.T} tokens), median; inputs already in host memory",
+           "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
+    for routing in routings[1:]:
+        out[f"{routing}_routing"] = {"value": per[routing]["value"], "unit": "us/step",
+                                     "sample": f"{per[routing]['forwards']} {routing}-routed forwards, median"}
+    return out
 
 
 if __name__ == "__main__":

@@ -201,3 +201,22 @@ class MoELayer:
         sizes = self.coreset_size.cpu().tolist()
         rows = self.coreset.cpu()
         return [rows[b, :n].tolist() for b, n in enumerate(sizes)]
+
+
+def decode_step(layers: list, weights: list, xs: list, routing: str = "block", stream=None) -> torch.Tensor:
+    """The MoE layers of one decode step, chained: layer l runs on xs[l] and
+    its input plus its output, rounded once to the storage type, is layer
+    l+1's input xs[l+1] (the residual stream of a transformer whose attention
+    and norms are left out; the paper's model has 19 such layers, Sec. 4.1).
+
+    ``layers`` are MoELayer objects of one shape, ``weights`` their packed
+    weights, ``xs`` len(layers) preallocated [T, H] tensors of the storage
+    type with xs[0] the step's input.  Returns the last layer's output y.
+    The residual add is one torch kernel per layer boundary; everything else
+    runs in libdmoe."""
+    y = None
+    for l, (m, w) in enumerate(zip(layers, weights)):
+        y = m.forward(xs[l], w, routing, stream)
+        if l + 1 < len(layers):
+            torch.add(xs[l], y, out=xs[l + 1])
+    return y
