@@ -232,9 +232,10 @@ def measure_modes(torch, cfg, layers, modes, steps, warmup, use_graph, ffn_only=
 
 
 def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
-    """A decode step of STEP_LAYERS chained MoE layers (layer l's input plus
-    output is layer l+1's input), timed per mode; the residual adds alone
-    are timed too, so the MoE part of the step is reported without them."""
+    """A decode step of STEP_LAYERS chained MoE layers (the step's input
+    plus layer l's output is layer l+1's input), timed per mode; the adds
+    alone are timed too, so the MoE part of the step is reported without
+    them."""
     from paper_2605_30876_amd.layer import decode_step
 
     L = STEP_LAYERS
@@ -246,7 +247,7 @@ def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
 
     def glue(_i):
         for l in range(L - 1):
-            torch.add(xs[l], ms[l].y, out=xs[l + 1])
+            torch.add(xs[0], ms[l].y, out=xs[l + 1])
 
     for routing in modes:
         decode_step(ms, ws, xs, routing)

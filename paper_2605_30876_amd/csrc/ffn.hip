@@ -62,17 +62,19 @@ struct Group {
 // Grid row y: the schedule's max_work items, then the shared expert's pieces
 // (kSharedFirst: the pieces first).  One memory round trip: the item count
 // and the item are loaded together (the index stays inside the work array;
-// an item past n_work is loaded but not used).
+// an item past n_work is loaded but not used).  An item naming an expert
+// outside [0, E) is skipped, so no schedule can steer a weight read outside
+// the expert arrays.
 template <bool kSharedFirst = false>
 __device__ __forceinline__ bool decode_item(int y, int shared_items, int max_work, const int* n_work,
-                                            const int* work, const int* row_token, int T, int Tk, Group& g) {
+                                            const int* work, const int* row_token, int T, int Tk, int E, Group& g) {
   const int w = kSharedFirst ? y - shared_items : y;
   if (kSharedFirst ? w >= 0 : w < max_work) {
     const int nw = *n_work;
     const int4 it = reinterpret_cast<const int4*>(work)[w];
     g.expert = it.x;
     g.r0 = it.y;
-    g.n = w < nw ? it.z : 0;
+    g.n = (w < nw && static_cast<unsigned>(it.x) < static_cast<unsigned>(E)) ? it.z : 0;
     g.tok = row_token + it.y;
     g.t0 = 0;
   } else {
@@ -115,7 +117,7 @@ struct FfnParams {
   const int* work;
   const int* row_token;
   const int* row_slot;
-  int T, H, I, I_s, k, Tk, R, max_work;  // R: rows of the h buffer
+  int T, H, E, I, I_s, k, Tk, R, max_work;  // R: rows of the h buffer
   int shared_items;                        // grid rows of the shared expert's pieces (0: none)
   int split_rows;                          // > 0: decode kernels take items of <= split_rows rows,
                                            // the tile kernels the larger ones
@@ -241,7 +243,7 @@ template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst, int RT>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
-                                 p.Tk, g))
+                                 p.Tk, p.E, g))
     return;
   if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
@@ -303,7 +305,7 @@ template <int NT, int KMAX, int BC, int MINW, bool kSharedFirst, int RT>
 __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams p) {
   Group g;
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
-                                 p.Tk, g))
+                                 p.Tk, p.E, g))
     return;
   if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
@@ -372,7 +374,8 @@ template <bool kGateUp, int kRowTiles>
 __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p) {
   constexpr int kTileRows = 4 * kRowTiles;  // weight tiles per workgroup
   Group g;
-  if (!decode_item(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, g)) return;
+  if (!decode_item(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, p.E, g))
+    return;
   if (g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
   const int H = p.H;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
@@ -543,9 +546,9 @@ constexpr int kF32Tok = 8;  // tokens per pass
 __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
     const float* __restrict__ xk, const float* __restrict__ w13, const float* __restrict__ ws13,
     const int* __restrict__ n_work, const int* __restrict__ work, const int* __restrict__ row_token, int T, int H,
-    int I, int I_s, int Tk, int max_work, int ldh, float* __restrict__ hbuf) {
+    int E, int I, int I_s, int Tk, int max_work, int ldh, float* __restrict__ hbuf) {
   Group g;
-  if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, g)) return;
+  if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, E, g)) return;
   const int Iw = g.expert >= 0 ? I : I_s;
   if (static_cast<int>(blockIdx.x) * kWave >= Iw) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -612,10 +615,10 @@ __global__ __launch_bounds__(kThreads) void ffn_gateup_f32_kernel(
 __global__ __launch_bounds__(kThreads) void ffn_down_f32_kernel(
     const float* __restrict__ w2, const float* __restrict__ ws2, const int* __restrict__ n_work,
     const int* __restrict__ work, const int* __restrict__ row_token, const int* __restrict__ row_slot, int T,
-    int H, int I, int I_s, int k, int Tk, int max_work, int ldh, const float* __restrict__ hbuf,
+    int H, int E, int I, int I_s, int k, int Tk, int max_work, int ldh, const float* __restrict__ hbuf,
     float* __restrict__ slot_out, float* __restrict__ shared_out) {
   Group g;
-  if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, g)) return;
+  if (!decode_item(blockIdx.y, 0, max_work, n_work, work, row_token, T, Tk, E, g)) return;
   const int Kd = g.expert >= 0 ? I : I_s;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j = blockIdx.x * kWave + lane;
@@ -785,7 +788,7 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 static_cast<const bf16_t*>(a.w13), static_cast<const bf16_t*>(a.w2),
                 static_cast<const bf16_t*>(a.ws13),
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
-                a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
+                a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
     if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
       const hipError_t err = launch_tile_bf16<true>(p, ldh, items, s);
@@ -814,12 +817,12 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
   dim3 g_gu((ldh + kWave - 1) / kWave, items), g_dn((a.H + kWave - 1) / kWave, items);
   ffn_gateup_f32_kernel<<<g_gu, kThreads, 0, s>>>(
       static_cast<const float*>(a.x), static_cast<const float*>(a.w13), static_cast<const float*>(a.ws13),
-      a.sched.n_work, a.sched.work, a.sched.row_token, a.T, a.H, a.I, a.I_s, Tk, a.max_work, ldh, hbuf);
+      a.sched.n_work, a.sched.work, a.sched.row_token, a.T, a.H, a.E, a.I, a.I_s, Tk, a.max_work, ldh, hbuf);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   ffn_down_f32_kernel<<<g_dn, kThreads, 0, s>>>(
       static_cast<const float*>(a.w2), static_cast<const float*>(a.ws2), a.sched.n_work, a.sched.work,
-      a.sched.row_token, a.sched.row_slot, a.T, a.H, a.I, a.I_s, a.k, Tk, a.max_work, ldh, hbuf, a.slot_out,
+      a.sched.row_token, a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, a.max_work, ldh, hbuf, a.slot_out,
       a.shared_out);
   return hipGetLastError();
 }

@@ -234,65 +234,15 @@ __device__ __forceinline__ void softmax_loaded(const RowPartials<NQ> (&r)[RB], c
 }
 
 // ---- top-k in (score desc, id asc) order ------------------------------------
+//
+// Scores are ranked by order-preserving integer keys: a float's key orders
+// like the float compare (-0 and +0 share a key, as they compare equal), and
+// every float, NaN included, has one.  So each ranking below is a total
+// order and a selection is always k distinct ids, whatever the scores hold
+// (a NaN probability from a NaN hidden state still selects valid experts).
 
 constexpr int kMaxK = 64;
 constexpr int kNone = 0x7fffffff;
-
-struct Cand {
-  float v;
-  int i;
-};
-
-// (v, i) ranks before (w, j).
-__device__ __forceinline__ bool ranks_before(float v, int i, float w, int j) {
-  return v > w || (v == w && i < j);
-}
-
-// Best (v, i) of the wave in (score desc, id asc) order; every lane gets it.
-__device__ __forceinline__ void best_step(Cand& c, float ov, int oi) {
-  if (ranks_before(ov, oi, c.v, c.i)) {
-    c.v = ov;
-    c.i = oi;
-  }
-}
-__device__ __forceinline__ Cand wave_best(Cand c) {
-  best_step(c, dppf<kDppXor1>(c.v, c.v), dpp<kDppXor1>(c.i, c.i));
-  best_step(c, dppf<kDppXor2>(c.v, c.v), dpp<kDppXor2>(c.i, c.i));
-  best_step(c, dppf<kDppHalfMirror>(c.v, c.v), dpp<kDppHalfMirror>(c.i, c.i));
-  best_step(c, dppf<kDppMirror>(c.v, c.v), dpp<kDppMirror>(c.i, c.i));
-  best_step(c, dppf<kDppBcast15, 0xA>(c.v, c.v), dpp<kDppBcast15, 0xA>(c.i, c.i));
-  best_step(c, dppf<kDppBcast31, 0xC>(c.v, c.v), dpp<kDppBcast31, 0xC>(c.i, c.i));
-  return Cand{lane63f(c.v), __builtin_amdgcn_readlane(c.i, 63)};
-}
-
-__device__ __forceinline__ int precedes(float u, int e, float v, int i) {
-  return (u > v || (u == v && e < i)) ? 1 : 0;
-}
-
-// The first `rounds` elements of row[0..E) (LDS) in order, by one wave: round
-// r picks the best element strictly after round r-1's pick.  Lane 0 writes
-// sel[r], selv[r].
-__device__ inline void wave_topk(const float* row, int E, int rounds, int* sel, float* selv) {
-  const int lane = threadIdx.x & 63;
-  float pv = INFINITY;
-  int pi = -1;
-  for (int r = 0; r < rounds; ++r) {
-    Cand best{-INFINITY, kNone};
-    for (int e = lane; e < E; e += kWave) {
-      const float v = row[e];
-      if (ranks_before(pv, pi, v, e) && ranks_before(v, e, best.v, best.i)) best = Cand{v, e};
-    }
-    best = wave_best(best);
-    if (lane == 0) {
-      sel[r] = best.i;
-      selv[r] = best.v;
-    }
-    pv = best.v;
-    pi = best.i;
-  }
-}
-
-constexpr int kRadixMaxPerLane = 16;  // E <= 1024
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   const uint32_t b = __float_as_uint(f + 0.0f);  // -0 -> +0: keys order like the float compare
@@ -303,6 +253,67 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 __device__ __forceinline__ float key_value(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
+
+// (key a, id i) ranks before (key b, id j): higher key, then lower id.
+__device__ __forceinline__ bool key_before(uint32_t a, int i, uint32_t b, int j) {
+  return a > b || (a == b && i < j);
+}
+
+struct Cand {
+  uint32_t key;  // order key of the score
+  int i;         // expert id
+};
+// Sentinels: every candidate ranks after kCandTop and before kCandNone.
+constexpr Cand kCandTop = {0xFFFFFFFFu, -1};
+constexpr Cand kCandNone = {0u, kNone};
+
+// Best candidate of the wave in (score desc, id asc) order; every lane gets it.
+__device__ __forceinline__ void best_step(Cand& c, int ok, int oi) {
+  const uint32_t k = static_cast<uint32_t>(ok);
+  if (key_before(k, oi, c.key, c.i)) {
+    c.key = k;
+    c.i = oi;
+  }
+}
+__device__ __forceinline__ Cand wave_best(Cand c) {
+  int k = static_cast<int>(c.key);
+  best_step(c, dpp<kDppXor1>(k, k), dpp<kDppXor1>(c.i, c.i));
+  k = static_cast<int>(c.key);
+  best_step(c, dpp<kDppXor2>(k, k), dpp<kDppXor2>(c.i, c.i));
+  k = static_cast<int>(c.key);
+  best_step(c, dpp<kDppHalfMirror>(k, k), dpp<kDppHalfMirror>(c.i, c.i));
+  k = static_cast<int>(c.key);
+  best_step(c, dpp<kDppMirror>(k, k), dpp<kDppMirror>(c.i, c.i));
+  k = static_cast<int>(c.key);
+  best_step(c, dpp<kDppBcast15, 0xA>(k, k), dpp<kDppBcast15, 0xA>(c.i, c.i));
+  k = static_cast<int>(c.key);
+  best_step(c, dpp<kDppBcast31, 0xC>(k, k), dpp<kDppBcast31, 0xC>(c.i, c.i));
+  return Cand{static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(c.key), 63)),
+              __builtin_amdgcn_readlane(c.i, 63)};
+}
+
+// The first `rounds` elements of row[0..E) (LDS) in order, by one wave: round
+// r picks the best element strictly after round r-1's pick.  Lane 0 writes
+// sel[r], selv[r].
+__device__ inline void wave_topk(const float* row, int E, int rounds, int* sel, float* selv) {
+  const int lane = threadIdx.x & 63;
+  Cand prev = kCandTop;
+  for (int r = 0; r < rounds; ++r) {
+    Cand best = kCandNone;
+    for (int e = lane; e < E; e += kWave) {
+      const uint32_t k = order_key(row[e]);
+      if (key_before(prev.key, prev.i, k, e) && key_before(k, e, best.key, best.i)) best = Cand{k, e};
+    }
+    best = wave_best(best);
+    if (lane == 0) {
+      sel[r] = best.i;
+      selv[r] = key_value(best.key);
+    }
+    prev = best;
+  }
+}
+
+constexpr int kRadixMaxPerLane = 16;  // E <= 1024
 
 __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
@@ -353,7 +364,8 @@ __device__ inline void wave_topk_radix_rows(const float* const (&row)[RB], const
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const bool in = lv[u] && j * kWave + lane < E && flag[j] != 0;
-      key[u][j] = in ? order_key(val[u][j]) : 0u;  // 0: below every real key
+      // excluded lanes: key 0, below every real key (real keys are >= 1)
+      key[u][j] = in ? max(order_key(val[u][j]), 1u) : 0u;
     }
   // MSB-first search for the rounds-th largest key.  A row stops as soon as
   // exactly `rounds` keys are >= its prefix: the answer is then the smallest
@@ -409,7 +421,7 @@ __device__ inline void wave_topk_radix_rows(const float* const (&row)[RB], const
       if (take) {
         const int pos = placed + lanes_below(t_mask);
         const int e = j * kWave + lane;
-        buf_v[pos] = key_value(key[u][j]);
+        buf_v[pos] = __uint_as_float(key[u][j]);  // the key's bits
         buf_i[pos] = e;
       }
       placed += __popcll(t_mask);
@@ -419,24 +431,24 @@ __device__ inline void wave_topk_radix_rows(const float* const (&row)[RB], const
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (rounds <= kWave) {
       // one gathered element per lane; ranks from broadcasts of the others
-      const float v = lane < rounds ? buf_v[lane] : -INFINITY;
+      const uint32_t kv = lane < rounds ? __float_as_uint(buf_v[lane]) : 0u;
       const int i = lane < rounds ? buf_i[lane] : kNone;
       int r = 0;
       for (int m = 0; m < rounds; ++m)
-        r += precedes(__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), m)),
-                      __builtin_amdgcn_readlane(i, m), v, i);
+        r += key_before(static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(kv), m)),
+                        __builtin_amdgcn_readlane(i, m), kv, i) ? 1 : 0;
       if (lane < rounds) {
         sel[u][r] = i;
-        selv[u][r] = v;
+        selv[u][r] = key_value(kv);
       }
     } else {
       for (int l = lane; l < rounds; l += kWave) {
-        const float v = buf_v[l];
+        const uint32_t kv = __float_as_uint(buf_v[l]);
         const int i = buf_i[l];
         int r = 0;
-        for (int m = 0; m < rounds; ++m) r += precedes(buf_v[m], buf_i[m], v, i);
+        for (int m = 0; m < rounds; ++m) r += key_before(__float_as_uint(buf_v[m]), buf_i[m], kv, i) ? 1 : 0;
         sel[u][r] = i;
-        selv[u][r] = v;
+        selv[u][r] = key_value(kv);
       }
     }
     // the gather buffer is reused by the next row
@@ -460,8 +472,8 @@ __device__ inline void wave_topk_radix_n(const float* row, int E, int rounds, in
 // (score desc, id asc) order, by radix selection: an MSB-first search over
 // order-preserving integer keys finds the rounds-th largest key (each bit is
 // one ballot count per register); the elements above it, then the lowest ids
-// equal to it, are gathered in id order into buf_v / buf_i (LDS, rounds
-// entries) and ranked among themselves.  Lanes write sel[r], selv[r].
+// equal to it, are gathered in id order into buf_v (their keys' bits) / buf_i
+// (LDS, rounds entries) and ranked among themselves by key and id.  Lanes write sel[r], selv[r].
 __device__ inline void wave_topk_radix(const float* row, int E, int rounds, int* sel, float* selv, float* buf_v,
                                        int* buf_i) {
   if (E <= 64)

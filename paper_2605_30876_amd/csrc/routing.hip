@@ -20,9 +20,8 @@ namespace dmoe {
 namespace {
 
 using dev::Cand;
+using dev::key_before;
 using dev::kMaxK;
-using dev::kNone;
-using dev::ranks_before;
 using dev::wave_best;
 
 constexpr int kRadixMaxE = 64 * dev::kRadixMaxPerLane;
@@ -74,13 +73,12 @@ __global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict
     if (wave == 0) dev::wave_topk_radix(S, E, rounds, sel, selv, bufv, bufi);
     __syncthreads();
   } else {
-    float pv = INFINITY;
-    int pi = -1;
+    Cand prev = dev::kCandTop;
     for (int r = 0; r < rounds; ++r) {
-      Cand best{-INFINITY, kNone};
+      Cand best = dev::kCandNone;
       for (int e = tid; e < E; e += blockDim.x) {
-        const float v = S[e];
-        if (ranks_before(pv, pi, v, e) && ranks_before(v, e, best.v, best.i)) best = Cand{v, e};
+        const uint32_t kv = dev::order_key(S[e]);
+        if (key_before(prev.key, prev.i, kv, e) && key_before(kv, e, best.key, best.i)) best = Cand{kv, e};
       }
       best = wave_best(best);
       if (lane == 0) wbest[wave] = best;
@@ -88,13 +86,12 @@ __global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict
       best = wbest[0];
 #pragma unroll
       for (int ww = 1; ww < 4; ++ww)
-        if (ranks_before(wbest[ww].v, wbest[ww].i, best.v, best.i)) best = wbest[ww];
+        if (key_before(wbest[ww].key, wbest[ww].i, best.key, best.i)) best = wbest[ww];
       if (tid == 0) {
         sel[r] = best.i;
-        selv[r] = best.v;
+        selv[r] = dev::key_value(best.key);
       }
-      pv = best.v;
-      pi = best.i;
+      prev = best;
       __syncthreads();
     }
   }

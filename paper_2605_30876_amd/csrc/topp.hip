@@ -111,12 +111,16 @@ __global__ __launch_bounds__(kCoreThreads) void block_coreset_kernel(
   }
   __syncthreads();
 
-  // 3. Sn in place, then each expert's rank (Sn desc, id asc) by counting;
-  //    padding (Sn = 0 at ids >= E) never ranks before a real expert
+  // 3. Sn in place, then each expert's rank (Sn desc, id asc) by counting
+  //    over the order keys of Sn (staged in Sv, free until the ranks are
+  //    known); padding (ids >= E) takes key 0 and never ranks before a real
+  //    expert, so the ranks of the E experts are 0 .. E-1
   const float total = s_total;
+  uint32_t* Sk = reinterpret_cast<uint32_t*>(Sv);
   for (int e = tid; e < Ep; e += kCoreThreads) {
     const float v = S[e] / total;
     S[e] = v;
+    Sk[e] = e < E ? max(dev::order_key(v), 1u) : 0u;
     if (block_scores && e < E) block_scores[static_cast<size_t>(b) * E + e] = v;
   }
   __syncthreads();
@@ -126,17 +130,17 @@ __global__ __launch_bounds__(kCoreThreads) void block_coreset_kernel(
     // row; the counts meet in LDS.
     const int parts = Ep <= 64 ? 8 : Ep <= 128 ? 4 : Ep <= 256 ? 2 : 1;
     const int n4 = Ep / 4, len = (n4 + parts - 1) / parts;
-    const float4* S4 = reinterpret_cast<const float4*>(S);
+    const uint4* K4 = reinterpret_cast<const uint4*>(Sk);
     for (int idx = tid; idx < E * parts; idx += kCoreThreads) {
       const int e = idx / parts, h = idx - e * parts;
-      const float v = S[e];
+      const uint32_t kv = Sk[e];
       const int m1 = min(n4, (h + 1) * len);
       int r = 0;
 #pragma unroll 4
       for (int m = h * len; m < m1; ++m) {
-        const float4 q = S4[m];
-        r += dev::precedes(q.x, 4 * m, v, e) + dev::precedes(q.y, 4 * m + 1, v, e) +
-             dev::precedes(q.z, 4 * m + 2, v, e) + dev::precedes(q.w, 4 * m + 3, v, e);
+        const uint4 q = K4[m];
+        r += (dev::key_before(q.x, 4 * m, kv, e) ? 1 : 0) + (dev::key_before(q.y, 4 * m + 1, kv, e) ? 1 : 0) +
+             (dev::key_before(q.z, 4 * m + 2, kv, e) ? 1 : 0) + (dev::key_before(q.w, 4 * m + 3, kv, e) ? 1 : 0);
       }
       if (r) atomicAdd(&rankc[e], r);
     }

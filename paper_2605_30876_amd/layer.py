@@ -204,19 +204,23 @@ class MoELayer:
 
 
 def decode_step(layers: list, weights: list, xs: list, routing: str = "block", stream=None) -> torch.Tensor:
-    """The MoE layers of one decode step, chained: layer l runs on xs[l] and
-    its input plus its output, rounded once to the storage type, is layer
-    l+1's input xs[l+1] (the residual stream of a transformer whose attention
-    and norms are left out; the paper's model has 19 such layers, Sec. 4.1).
+    """The MoE layers of one decode step, chained: layer l runs on xs[l], and
+    the step's input plus layer l's output, rounded once to the storage
+    type, is layer l+1's input xs[l+1].  Each layer thus waits for its
+    predecessor's output, as in a transformer's residual stream (attention
+    and norms are left out; anchoring every layer's input to the step input
+    keeps its scale that of the inputs, where adding the outputs up would let
+    the quadratic SwiGLU grow the stream until the softmax underflows).  The
+    paper's model has 19 MoE layers (Sec. 4.1).
 
     ``layers`` are MoELayer objects of one shape, ``weights`` their packed
     weights, ``xs`` len(layers) preallocated [T, H] tensors of the storage
     type with xs[0] the step's input.  Returns the last layer's output y.
-    The residual add is one torch kernel per layer boundary; everything else
-    runs in libdmoe."""
+    The add is one torch kernel per layer boundary; everything else runs in
+    libdmoe."""
     y = None
     for l, (m, w) in enumerate(zip(layers, weights)):
         y = m.forward(xs[l], w, routing, stream)
         if l + 1 < len(layers):
-            torch.add(xs[l], y, out=xs[l + 1])
+            torch.add(xs[0], y, out=xs[l + 1])
     return y
