@@ -45,7 +45,8 @@
  *  - Every pointer argument is a DEVICE pointer (memory the caller allocated on
  *    the GPU, e.g. with hipMalloc or a torch CUDA tensor) unless the comment
  *    says otherwise.  The caller owns all memory.  The library allocates
- *    nothing and keeps no state between calls.
+ *    nothing and keeps no state between calls, except the per-GPU device
+ *    array of dmoe_expert_ffn_noalloc.
  *  - All arrays are dense and row-major.  Matrices are indexed [row][col] with
  *    the last index contiguous.
  *  - Tokens are block-major: block b of a forward is rows
@@ -320,7 +321,10 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  *   slot_out[t][j][:] = W_down[e] h
  * and, when the shared expert is present (ws13 != NULL), for every token t:
  *   shared_out[t][:] = Ws_down (silu(Ws_gate x_t) * (Ws_up x_t))
- * Each selected expert's weights are streamed once per call.
+ * Each selected expert's weights are streamed once per work item: an
+ * expert's rows are cut into items of at most DMOE_WORK_ROWS, and an expert
+ * with more rows than that (a popular expert, or the shared expert over more
+ * than DMOE_WORK_ROWS tokens) is streamed once per item.
  * x_chunked: the hidden states x [T][H] in the chunk-major layout above.
  * x: the same hidden states row-major [T][H], optional (NULL: not used).
  * With it, bf16 rows whose tokens are not consecutive (token-level routing)
@@ -330,9 +334,12 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  * ws13, ws2: the shared expert packed the same way (n_experts = 1, I = I_s),
  * both NULL with I_s == 0 or both set with I_s > 0.  All of type dt.
  * sched: written by dmoe_build_expert_schedule for these T and k.
- * max_work: the bound dmoe_schedule_max_work gave for the schedule (the
- * grid is sized for it).  The shared expert's T rows are cut into pieces of
- * DMOE_WORK_ROWS the same way.
+ * max_work: at least dmoe_schedule_max_work(n_groups, group_size, k, E) of
+ * the call that built sched.  The grid has max_work rows for the routed
+ * experts; a work item past max_work is not run and its slot_out rows keep
+ * what they held, so a smaller value gives wrong results without an error.
+ * The shared expert's T rows are cut into pieces of DMOE_WORK_ROWS the same
+ * way.
  * slot_out [T][k][H] float32 (every (t, j) is written); shared_out [T][H]
  * float32 (NULL iff no shared expert).
  * workspace: device scratch of at least dmoe_ffn_workspace_size(...) bytes,
@@ -347,6 +354,27 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w1
                             const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
                             int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
                             float* shared_out, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * dmoe_expert_ffn without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture that may not call
+ * hipMalloc, serving loops and harnesses that forbid allocation).  The
+ * SwiGLU activations go to a device array of DMOE_NOALLOC_SCRATCH_BYTES that
+ * the library holds on each GPU it runs on until the process ends; nothing
+ * is allocated or freed by the call.  Arguments, results and limits are
+ * those of dmoe_expert_ffn (results are bit-identical to it), plus:
+ * dmoe_ffn_workspace_size(T, I, I_s, k, dt) must not exceed
+ * DMOE_NOALLOC_SCRATCH_BYTES, else DMOE_ERR_INVALID_ARG and nothing is
+ * enqueued.  Every call on one GPU shares that GPU's array and leaves its
+ * contents behind (no part of it needs to start at zero): calls that overlap
+ * in time on one GPU (two streams, two threads) race and must be serialised
+ * by the caller.  DMOE_ERR_HIP if the array's device address cannot be found.
+ */
+#define DMOE_NOALLOC_SCRATCH_BYTES (16u << 20)
+dmoe_status dmoe_expert_ffn_noalloc(const void* x_chunked, const void* x, const void* w13, const void* w2,
+                                    const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
+                                    int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
+                                    float* shared_out, void* stream);
 
 /*
  * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn): for every

@@ -40,13 +40,15 @@ constexpr int kMaxScheduleE = 512;
 constexpr int kMaxK = 64;
 constexpr long kIntLimit = 0x7fffffffL;
 
+// Name of the entry point in error messages.
+#define DMOE_FN __func__
 #define REQUIRE(cond, ...)                                  \
   do {                                                      \
-    if (!(cond)) return fail(DMOE_ERR_INVALID_ARG, __func__, __VA_ARGS__); \
+    if (!(cond)) return fail(DMOE_ERR_INVALID_ARG, DMOE_FN, __VA_ARGS__); \
   } while (0)
 #define SUPPORT(cond, ...)                                  \
   do {                                                      \
-    if (!(cond)) return fail(DMOE_ERR_UNSUPPORTED, __func__, __VA_ARGS__); \
+    if (!(cond)) return fail(DMOE_ERR_UNSUPPORTED, DMOE_FN, __VA_ARGS__); \
   } while (0)
 #define ALIGNED(p) REQUIRE(!misaligned(p), #p " is not 16-byte aligned")
 
@@ -391,11 +393,19 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt) {
   return dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
 }
 
-dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w13, const void* w2,
-                            const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
-                            int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
-                            float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
-  REQUIRE(x_chunked && w13 && w2 && slot_out && workspace,
+}  // extern "C"
+
+namespace {
+
+// dmoe_expert_ffn and dmoe_expert_ffn_noalloc: every argument is validated on
+// the host first; then (noalloc) the device scratch replaces the workspace.
+dmoe_status expert_ffn(const char* fn, const void* x_chunked, const void* x, const void* w13, const void* w2,
+                       const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
+                       int max_work, dmoe_schedule sched, float* slot_out, float* shared_out, void* workspace,
+                       size_t ws_bytes, void* stream, bool noalloc) {
+#undef DMOE_FN
+#define DMOE_FN fn  // messages name the entry point
+  REQUIRE(x_chunked && w13 && w2 && slot_out && (workspace || noalloc),
           "x_chunked, w13, w2, slot_out and workspace must not be NULL");
   REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
               sched.work,
@@ -416,7 +426,14 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w1
               static_cast<long>(T) * k * H <= kIntLimit * 4L,
           "T*k*H, T*H or the SwiGLU buffer is too large");
   const size_t need = dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
-  REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
+  if (noalloc) {
+    REQUIRE(need <= DMOE_NOALLOC_SCRATCH_BYTES,
+            "the SwiGLU activations need %zu bytes, more than the %zu-byte device scratch of this entry point "
+            "(call dmoe_expert_ffn with a workspace)",
+            need, static_cast<size_t>(DMOE_NOALLOC_SCRATCH_BYTES));
+  } else {
+    REQUIRE(ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
+  }
   ALIGNED(x_chunked);
   ALIGNED(x);
   ALIGNED(w13);
@@ -435,9 +452,35 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w1
     SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
             "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
   }
+  if (noalloc) {
+    const hipError_t err = dmoe::noalloc_scratch(&workspace);
+    if (err != hipSuccess) return fail(DMOE_ERR_HIP, fn, "device scratch lookup failed: %s", hipGetErrorString(err));
+  }
   dmoe::FfnArgs a{x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
                   sched, slot_out, shared_out, workspace};
-  return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
+  return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), fn);
+}
+#undef DMOE_FN
+#define DMOE_FN __func__
+
+}  // namespace
+
+extern "C" {
+
+dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w13, const void* w2,
+                            const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
+                            int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
+                            float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
+  return expert_ffn(__func__, x_chunked, x, w13, w2, ws13, ws2, dt, T, H, E, I, I_s, k, max_work, sched, slot_out,
+                    shared_out, workspace, ws_bytes, stream, false);
+}
+
+dmoe_status dmoe_expert_ffn_noalloc(const void* x_chunked, const void* x, const void* w13, const void* w2,
+                                    const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
+                                    int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
+                                    float* shared_out, void* stream) {
+  return expert_ffn(__func__, x_chunked, x, w13, w2, ws13, ws2, dt, T, H, E, I, I_s, k, max_work, sched, slot_out,
+                    shared_out, nullptr, 0, stream, true);
 }
 
 size_t dmoe_shared_ffn_workspace_size(int T, int I_s, dmoe_dtype dt) {

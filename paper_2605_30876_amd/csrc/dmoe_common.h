@@ -134,6 +134,9 @@ struct FfnArgs {
   void* workspace;  // SwiGLU activations of T*k (+ T) rows, max(I, I_s) wide, storage type
 };
 hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s);
+// Device address of this device's DMOE_NOALLOC_SCRATCH_BYTES scratch array
+// (looked up on the first call per device, then cached).
+hipError_t noalloc_scratch(void** ptr);
 size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
 long schedule_max_work(long n_groups, long group_size, long k, long E);
 size_t schedule_scratch_ints(long n_groups, long k, long E);

@@ -32,7 +32,7 @@ EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggre
            "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work",
            "dmoe_schedule_scratch_ints", "dmoe_route_block",
            "dmoe_route_token", "dmoe_route_topp", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
-           "dmoe_expert_ffn", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
+           "dmoe_expert_ffn", "dmoe_expert_ffn_noalloc", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
            "dmoe_last_error", "dmoe_version")
 
 
@@ -73,6 +73,7 @@ _SIGS = {
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
     "dmoe_expert_ffn": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
+    "dmoe_expert_ffn_noalloc": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _P], _I),
     "dmoe_shared_ffn_workspace_size": ([_I, _I, _I], _S),
     "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
@@ -263,6 +264,17 @@ def dmoe_expert_ffn(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_wo
                                   dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
                                   ptr(slot_out), ptr(shared_out), ptr(workspace),
                                   workspace.numel() * workspace.element_size(), stream_handle(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # DMOE_NOALLOC_SCRATCH_BYTES
+
+
+def dmoe_expert_ffn_noalloc(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work, sched: Schedule,
+                            slot_out, shared_out, stream=None):
+    """dmoe_expert_ffn with the library's device scratch instead of a workspace."""
+    _check(load().dmoe_expert_ffn_noalloc(ptr(x_chunked), ptr(x), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
+                                          dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
+                                          ptr(slot_out), ptr(shared_out), stream_handle(stream)))
 
 
 def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):

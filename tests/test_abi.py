@@ -339,3 +339,30 @@ def test_schedule_scratch_ints():
     assert lib.dmoe_schedule_scratch_ints(1, 1, 16) == 2 * 16
     assert lib.dmoe_schedule_scratch_ints(0, 8, 256) == 0
     assert lib.dmoe_schedule_scratch_ints(8, 8, 0) == 0
+
+
+def _ffn_noalloc(L, p, **kw):
+    a = dict(x=p, xr=None, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512,
+             k=8, max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, shared=p)
+    a.update(kw)
+    return status(L, "dmoe_expert_ffn_noalloc", a["x"], a["xr"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"],
+                  a["T"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"],
+                  a["shared"], None)
+
+
+def test_ffn_noalloc_validation(L, buf):
+    """Every argument is checked on the host before the device scratch is
+    looked up: these calls fail without touching a GPU."""
+    _, p = buf
+    INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    # activations of T*k + T rows x max(I, I_s) bf16 beyond the 16 MiB scratch
+    need = lib.dmoe_ffn_workspace_size(4096, 512, 512, 8, lib.DMOE_BF16)
+    assert need > lib.NOALLOC_SCRATCH_BYTES
+    st, msg = _ffn_noalloc(L, p, T=4096, max_work=1024)
+    assert st == INV and "scratch" in msg and "dmoe_expert_ffn_noalloc" in msg
+    assert lib.dmoe_ffn_workspace_size(512, 512, 512, 8, lib.DMOE_BF16) <= lib.NOALLOC_SCRATCH_BYTES
+    assert _ffn_noalloc(L, p, x=None)[0] == INV
+    assert _ffn_noalloc(L, p, slot=p + 4)[0] == INV
+    assert _ffn_noalloc(L, p, max_work=0)[0] == INV
+    assert _ffn_noalloc(L, p, ws2=None)[0] == INV
+    assert _ffn_noalloc(L, p, H=2000)[0] == UNS

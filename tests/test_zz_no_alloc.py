@@ -1,0 +1,56 @@
+"""dmoe_expert_ffn_noalloc (the library's device scratch in place of a
+workspace) against dmoe_expert_ffn on the same schedule: slot and shared
+outputs must be bitwise equal, on two calls in a row, the second with a
+smaller input (its scratch then still holds the first call's activations).
+Marked ``gpu``."""
+import pytest
+import torch
+
+from dmoe_synth import get_config, make_inputs
+from paper_2605_30876_amd import lib
+from paper_2605_30876_amd.layer import MoELayer, pack_weights
+
+pytestmark = pytest.mark.gpu
+
+
+def _routed_layer(name, routing, seed):
+    cfg = get_config(name)
+    d = make_inputs(cfg, seed=seed, device="cuda")
+    w = pack_weights(d)
+    m = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device="cuda")
+    m.route(d["x"], w["w_router"], w.get("bias"), routing)
+    return cfg, d, w, m
+
+
+def _both(cfg, d, w, m, routing):
+    args = (m.x_chunked, d["x"], w["w13"], w["w2"], w.get("ws13"), w.get("ws2"), cfg.T, cfg.H, cfg.E, cfg.I,
+            cfg.I_s, cfg.k, m.max_work(routing), m.sched)
+    slot_ref = torch.full_like(m.slot_out, float("nan"))
+    sh_ref = torch.full_like(m.shared_out, float("nan"))
+    lib.dmoe_expert_ffn(*args, slot_ref, sh_ref, m.workspace)
+    slot = torch.full_like(m.slot_out, float("nan"))
+    sh = torch.full_like(m.shared_out, float("nan"))
+    lib.dmoe_expert_ffn_noalloc(*args, slot, sh)
+    torch.cuda.synchronize()
+    assert torch.isfinite(slot_ref).all() and torch.isfinite(sh_ref).all()
+    assert torch.equal(slot, slot_ref), "slot outputs differ"
+    assert torch.equal(sh, sh_ref), "shared-expert outputs differ"
+
+
+def test_noalloc_ffn_equals_workspace_ffn(gpu_lib):
+    # 512 tokens (4.7 MB of activations), then 32 tokens: the second call runs
+    # on scratch the first one filled
+    for name, routing in (("decode_b16", "block"), ("decode_b1", "token")):
+        print("case", name, routing, flush=True)
+        cfg, d, w, m = _routed_layer(name, routing, seed=8)
+        assert lib.dmoe_ffn_workspace_size(cfg.T, cfg.I, cfg.I_s, cfg.k, lib.DMOE_BF16) <= lib.NOALLOC_SCRATCH_BYTES
+        _both(cfg, d, w, m, routing)
+
+
+def test_noalloc_ffn_rejects_oversized(gpu_lib):
+    cfg, d, w, m = _routed_layer("corr_b64x64", "block", seed=0)
+    with pytest.raises(lib.DmoeError) as ei:
+        lib.dmoe_expert_ffn_noalloc(m.x_chunked, d["x"], w["w13"], w["w2"], w["ws13"], w["ws2"], cfg.T, cfg.H,
+                                    cfg.E, cfg.I, cfg.I_s, cfg.k, m.max_work("block"), m.sched, m.slot_out,
+                                    m.shared_out)
+    assert ei.value.status == lib.DMOE_ERR_INVALID_ARG
