@@ -32,7 +32,7 @@ def ffn_source_hash() -> str:
     import re
 
     h = hashlib.sha256()
-    for f in ("ffn.hip", "pack.hip"):
+    for f in ("ffn.hip", "ffn_dev.h", "pack.hip"):
         with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
             for line in fh:
                 code = re.sub(r"//.*", "", line).rstrip()
