@@ -409,6 +409,75 @@ dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, cons
 dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const float* shared_out,
                          dmoe_dtype dt, int T, int H, int k, void* y, void* stream);
 
+/*
+ * The whole MoE layer forward in one call: routing (dmoe_routing), the
+ * expert FFN and the combine,
+ *   y[t] = sum_j w[t][j] * FFN_{e_tj}(x_t) + FFN_shared(x_t)          (Sec. 3)
+ * with the routing of Sec. 4.2 (block: Alg. 1 with a coreset of size k;
+ * token: the baseline; topp: Alg. 1 with the Top-P coreset p, min_coreset).
+ *
+ * A block-routed forward of a single bf16 block (n_blocks == 1, block_size
+ * <= 64, E <= 512, k + (I_s > 0) <= 12, T*E small enough for on-chip
+ * probabilities) runs as three kernels: the router with the shared expert's
+ * gate/up beside it; the routing, recomputed by every workgroup of the routed
+ * gate/up (the combine weight applied to the SwiGLU activations); and one
+ * down projection over all selected experts and the shared expert that
+ * writes y (no slot outputs, no combine kernel).  Its routing outputs equal
+ * dmoe_route_block's up to the float32 rounding of the logits (one
+ * reduction over the whole hidden dimension instead of slices), and y
+ * differs from the chained path's by the bf16 rounding of the weighted
+ * activations.  Every other forward chains dmoe_route_block / _token /
+ * _topp, dmoe_expert_ffn and dmoe_combine, with results bit-identical to
+ * those calls.
+ *
+ * Inputs: x [T][H] (T = n_blocks*block_size); w_router [E][H]; bias [E] or
+ * NULL; w13, w2 routed and ws13, ws2 shared experts packed by
+ * dmoe_pack_expert_weights (ws13 = ws2 = NULL iff I_s == 0); all of type dt.
+ * buf: a HOST pointer to the device buffers below, all as documented for the
+ * entry points the layer chains (experts is block_experts [n_blocks][k] for
+ * block routing and token_experts [T][k] otherwise; gap is [n_blocks] or
+ * [T]; coreset and coreset_size are used by topp only, else may be NULL;
+ * slot_out [T][k][H] and shared_out [T][H] are scratch of the chained path
+ * and are left untouched by the three-kernel path, shared_out NULL iff
+ * I_s == 0).  y [T][H] of type y_dt.  workspace: at least
+ * dmoe_moe_forward_workspace_size bytes (contents on entry do not matter;
+ * calls sharing one must not overlap in time).
+ * Limits: those of the chained entry points (E <= 512; bf16: H, I, I_s
+ * multiples of 128).
+ */
+typedef enum dmoe_routing {
+  DMOE_ROUTE_BLOCK = 0,
+  DMOE_ROUTE_TOKEN = 1,
+  DMOE_ROUTE_TOPP = 2
+} dmoe_routing;
+
+typedef struct dmoe_layer_buffers {
+  float* logits;        /* [T][E] or NULL */
+  float* probs;         /* [T][E] */
+  void* x_chunked;      /* T*H elements of dt */
+  float* block_scores;  /* [n_blocks][E] or NULL */
+  int32_t* experts;
+  float* combine_w;     /* [T][k] */
+  float* gap;           /* or NULL */
+  int32_t* coreset;     /* topp: [n_blocks][E] */
+  int32_t* coreset_size;/* topp: [n_blocks] */
+  dmoe_schedule sched;
+  float* slot_out;
+  float* shared_out;
+  void* workspace;
+  size_t ws_bytes;
+} dmoe_layer_buffers;
+
+/* Bytes of dmoe_layer_buffers.workspace for these sizes (0 on invalid sizes). */
+size_t dmoe_moe_forward_workspace_size(int n_blocks, int block_size, int H, int E, int I, int I_s, int k,
+                                       dmoe_dtype dt);
+
+dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* bias, const void* w13,
+                             const void* w2, const void* ws13, const void* ws2, dmoe_dtype dt, int n_blocks,
+                             int block_size, int H, int E, int I, int I_s, int k, dmoe_routing routing, float top_p,
+                             int min_coreset, const dmoe_layer_buffers* buf, void* y, dmoe_dtype y_dt,
+                             void* stream);
+
 /* Message describing the last non-OK status returned on this thread ("" if none). */
 const char* dmoe_last_error(void);
 

@@ -21,7 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdmoe.so")
 SOURCES = ["dmoe_api.cpp", "router.hip", "routing.hip", "topp.hip", "schedule.hip", "route.hip", "pack.hip",
-           "ffn.hip", "combine.hip", "noalloc.hip"]
+           "ffn.hip", "combine.hip", "noalloc.hip", "layer.hip"]
 ARCH = os.environ.get("DMOE_OFFLOAD_ARCH", "gfx950")
 
 

@@ -531,4 +531,140 @@ dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const fl
                     __func__);
 }
 
+namespace {
+
+size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
+
+// Workspace of the layer: the chained path's router partials and FFN
+// activations, or the three-kernel path's logits and weighted activations.
+size_t layer_workspace_bytes(int n_blocks, int bs, int H, int E, int I, int I_s, int k, dmoe_dtype dt) {
+  const int T = n_blocks * bs;
+  const size_t chain = align256(dmoe::router_workspace_bytes(T, H, E, dt)) + dmoe::ffn_workspace_bytes(T, I, I_s, k, dt);
+  const size_t fused = dmoe::layer_fused_fits(dt, n_blocks, T, H, E, I, I_s, k)
+                           ? dmoe::layer_fused_workspace_bytes(T, E, I, I_s, k)
+                           : 0;
+  return chain > fused ? chain : fused;
+}
+
+}  // namespace
+
+size_t dmoe_moe_forward_workspace_size(int n_blocks, int block_size, int H, int E, int I, int I_s, int k,
+                                       dmoe_dtype dt) {
+  if (n_blocks < 1 || block_size < 1 || H < 1 || E < 1 || E > kMaxScheduleE || I < 1 || I_s < 0 || k < 1 || k > E ||
+      !valid_dtype(dt))
+    return 0;
+  return layer_workspace_bytes(n_blocks, block_size, H, E, I, I_s, k, dt);
+}
+
+dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* bias, const void* w13,
+                             const void* w2, const void* ws13, const void* ws2, dmoe_dtype dt, int n_blocks,
+                             int block_size, int H, int E, int I, int I_s, int k, dmoe_routing routing, float top_p,
+                             int min_coreset, const dmoe_layer_buffers* buf, void* y, dmoe_dtype y_dt,
+                             void* stream) {
+  // Everything the chained entry points check is checked here first, so a
+  // bad argument enqueues nothing.
+  REQUIRE(buf, "buf must not be NULL");
+  REQUIRE(x && w_router && w13 && w2 && y && buf->probs && buf->x_chunked && buf->experts && buf->combine_w &&
+              buf->slot_out && buf->workspace,
+          "x, w_router, w13, w2, y and buf's probs, x_chunked, experts, combine_w, slot_out and workspace must "
+          "not be NULL");
+  const dmoe_schedule& sched = buf->sched;
+  REQUIRE(sched.n_unique && sched.unique && sched.offsets && sched.row_token && sched.row_slot && sched.n_work &&
+              sched.work,
+          "every schedule array must be set");
+  REQUIRE(valid_dtype(dt) && valid_dtype(y_dt), "unknown dtype %d / %d", static_cast<int>(dt), static_cast<int>(y_dt));
+  REQUIRE(routing == DMOE_ROUTE_BLOCK || routing == DMOE_ROUTE_TOKEN || routing == DMOE_ROUTE_TOPP,
+          "unknown routing %d", static_cast<int>(routing));
+  REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
+  REQUIRE(block_size >= 1 && block_size <= 4096, "block_size=%d must be in [1, 4096]", block_size);
+  REQUIRE(H >= 1 && I >= 1 && I_s >= 0, "H=%d, I=%d must be >= 1 and I_s=%d >= 0", H, I, I_s);
+  REQUIRE(E >= 1 && E <= kMaxE, "E=%d must be in [1, %d]", E, kMaxE);
+  REQUIRE(k >= 1 && k <= E && k <= kMaxK, "k=%d must be in [1, min(E, %d)]", k, kMaxK);
+  const long T = static_cast<long>(n_blocks) * block_size;
+  REQUIRE(T * E <= kIntLimit && T * H <= kIntLimit && T * k < kIntLimit, "T*E, T*H and T*k must fit in int32");
+  const bool shared = I_s > 0;
+  REQUIRE(shared == (ws13 != nullptr) && shared == (ws2 != nullptr) && shared == (buf->shared_out != nullptr),
+          "ws13, ws2 and shared_out must all be set iff I_s > 0");
+  const long rows = T * k + (shared ? T : 0);
+  REQUIRE(rows < kIntLimit && rows * (I > I_s ? I : I_s) <= kIntLimit && T * k * H <= kIntLimit * 4L,
+          "T*k*H or the SwiGLU buffer is too large");
+  REQUIRE(H % dmoe::chunk_elems(dt) == 0, "H=%d must be a multiple of %d", H, dmoe::chunk_elems(dt));
+  REQUIRE(H % 4 == 0, "H=%d must be a multiple of 4", H);
+  if (routing == DMOE_ROUTE_TOPP) {
+    REQUIRE(buf->coreset && buf->coreset_size, "Top-P routing needs coreset and coreset_size");
+    REQUIRE(min_coreset >= k && min_coreset <= E, "min_coreset=%d must be in [k, E]", min_coreset);
+    REQUIRE(top_p > 0.f && top_p <= 1.f, "p=%g must be in (0, 1]", static_cast<double>(top_p));
+  }
+  const size_t need = layer_workspace_bytes(n_blocks, block_size, H, E, I, I_s, k, dt);
+  REQUIRE(buf->ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", buf->ws_bytes, need);
+  ALIGNED(x);
+  ALIGNED(w_router);
+  ALIGNED(bias);
+  ALIGNED(w13);
+  ALIGNED(w2);
+  ALIGNED(ws13);
+  ALIGNED(ws2);
+  ALIGNED(y);
+  ALIGNED(buf->logits);
+  ALIGNED(buf->probs);
+  ALIGNED(buf->x_chunked);
+  ALIGNED(buf->block_scores);
+  ALIGNED(buf->experts);
+  ALIGNED(buf->combine_w);
+  ALIGNED(buf->gap);
+  ALIGNED(buf->coreset);
+  ALIGNED(buf->coreset_size);
+  ALIGNED(buf->slot_out);
+  ALIGNED(buf->shared_out);
+  ALIGNED(buf->workspace);
+  ALIGNED(sched.n_unique);
+  ALIGNED(sched.unique);
+  ALIGNED(sched.offsets);
+  ALIGNED(sched.scratch);
+  ALIGNED(sched.row_token);
+  ALIGNED(sched.row_slot);
+  ALIGNED(sched.n_work);
+  ALIGNED(sched.work);
+  SUPPORT(E <= kMaxScheduleE, "the schedule supports E <= %d (E=%d)", kMaxScheduleE, E);
+  if (dt == DMOE_BF16) {
+    SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
+            "bf16 layers need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
+  }
+  if (routing == DMOE_ROUTE_TOPP) {
+    SUPPORT(dmoe::topp_supported(block_size, E, k), "the Top-P kernels do not support block_size=%d, E=%d, k=%d",
+            block_size, E, k);
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int Ti = static_cast<int>(T);
+  if (routing == DMOE_ROUTE_BLOCK && dmoe::layer_fused_fits(dt, n_blocks, Ti, H, E, I, I_s, k)) {
+    dmoe::LayerArgs a{x, w_router, bias, w13, w2, ws13, ws2, Ti, H, E, I, I_s, k, buf->logits, buf->probs,
+                      buf->x_chunked, buf->block_scores, buf->experts, buf->combine_w, buf->gap, sched,
+                      buf->workspace, y, y_dt};
+    return hip_status(dmoe::launch_layer_fused(a, s), __func__);
+  }
+  const size_t rbytes = dmoe::router_workspace_bytes(Ti, H, E, dt);
+  void* ffn_ws = static_cast<char*>(buf->workspace) + align256(rbytes);
+  dmoe::RouteArgs ra{x, w_router, bias, Ti, H, E, k, routing == DMOE_ROUTE_TOKEN ? 1 : block_size,
+                     routing == DMOE_ROUTE_BLOCK, buf->logits, buf->probs, buf->x_chunked,
+                     routing == DMOE_ROUTE_TOKEN ? nullptr : buf->block_scores, buf->experts, buf->combine_w,
+                     buf->gap, sched, rbytes ? buf->workspace : nullptr, rbytes};
+  if (routing == DMOE_ROUTE_TOPP) {
+    ra.topp = true;
+    ra.top_p = top_p;
+    ra.min_coreset = min_coreset;
+    ra.coreset = buf->coreset;
+    ra.coreset_size = buf->coreset_size;
+  }
+  hipError_t err = dmoe::launch_route(ra, dt, s);
+  if (err != hipSuccess) return hip_status(err, __func__);
+  const long mw = routing == DMOE_ROUTE_BLOCK ? dmoe::schedule_max_work(n_blocks, block_size, k, E)
+                                              : dmoe::schedule_max_work(T, 1, k, E);
+  dmoe::FfnArgs fa{buf->x_chunked, x, w13, w2, ws13, ws2, Ti, H, E, I, I_s, k, static_cast<int>(mw), sched,
+                   buf->slot_out, buf->shared_out, ffn_ws};
+  err = dmoe::launch_ffn(fa, dt, s);
+  if (err != hipSuccess) return hip_status(err, __func__);
+  return hip_status(dmoe::launch_combine(buf->slot_out, buf->combine_w, buf->shared_out, y_dt, Ti, H, k, y, s),
+                    __func__);
+}
+
 }  // extern "C"

@@ -141,6 +141,33 @@ size_t ffn_workspace_bytes(int T, int I, int I_s, int k, dmoe_dtype dt);
 long schedule_max_work(long n_groups, long group_size, long k, long E);
 size_t schedule_scratch_ints(long n_groups, long k, long E);
 
+// The whole block-routed layer of one block in three launches (layer.hip):
+// router + shared gate/up, routing + routed gate/up, down + combine.
+struct LayerArgs {
+  const void* x;
+  const void* w_router;
+  const float* bias;
+  const void* w13;
+  const void* w2;
+  const void* ws13;  // nullptr: no shared expert
+  const void* ws2;
+  int T, H, E, I, I_s, k;
+  float* logits;  // or nullptr
+  float* probs;
+  void* x_chunked;
+  float* block_scores;  // or nullptr
+  int32_t* experts;
+  float* combine_w;
+  float* gap;  // or nullptr
+  dmoe_schedule sched;
+  void* workspace;  // layer_fused_workspace_bytes
+  void* y;
+  dmoe_dtype y_dt;
+};
+bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, int I_s, int k);
+size_t layer_fused_workspace_bytes(int T, int E, int I, int I_s, int k);
+hipError_t launch_layer_fused(const LayerArgs& a, hipStream_t s);
+
 hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
                           dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);
 

@@ -1,0 +1,393 @@
+// The whole block-routed MoE layer forward of ONE block (a decode step of one
+// sequence) in three launches.
+//
+// A decode step's layer is a chain of small dependent phases -- router,
+// routing, gate/up, down, combine -- and on gfx950 each kernel boundary costs
+// a launch plus a memory round trip to data another XCD wrote, while a
+// cross-XCD barrier inside a kernel costs more (cache write-back and
+// invalidation).  So the phases are merged where the merge needs no
+// synchronisation at all:
+//
+//  1. router + shared gate/up.  Router tiles of 16 tokens x 16 experts over
+//     the whole hidden dimension write the logits; the workgroups of the
+//     first expert tile also write x in the chunk-major layout.  The shared
+//     expert needs only x, so its gate/up tiles run in the same launch on
+//     otherwise idle CUs (reading the row-major x).
+//  2. routing + routed gate/up.  Every workgroup recomputes the block's
+//     routing from the logits -- softmax of each token row, the block mean
+//     in token order, the top-(k+1) by radix selection, the weights -- with
+//     the device routines of the routing kernels, so every workgroup reaches
+//     the same bits (workgroup (0, 0) writes the routing outputs and the
+//     closed-form schedule).  Workgroup (it, j) then streams packed tile it of
+//     the j-th selected expert's gate/up weights over all tokens of the block
+//     and stores the SwiGLU activations already multiplied by the token's
+//     combine weight, w[t][j] * silu(g) * u, as bf16.
+//  3. down + combine.  With every token using the same k experts, the
+//     weighted sum over experts of the down projections is ONE product with a
+//     reduction over k*I + I_s: y[t] = [Wd_1 .. Wd_k Wsd] [w_1 h_1; ..; w_k
+//     h_k; h_s](t).  A workgroup owns 16 output features; wave j reduces over
+//     the j-th expert's intermediate units (the last wave over the shared
+//     expert's), and the waves' partial tiles are added in wave order, so y
+//     is deterministic and there is no per-slot output and no combine launch.
+//
+// Activations between the launches are chunk-major over the concatenated
+// reduction index: hk[(kk/8)*T + t][kk%8], kk = j*I + i for routed slot j and
+// unit i, kk = k*I + i for the shared expert.
+#include "ffn_dev.h"
+#include "route_dev.h"
+
+namespace dmoe {
+namespace {
+
+using fdev::kFrag;
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kTok = 16;  // tokens per MFMA tile
+
+struct LayerParams {
+  const bf16_t* x;     // [T][H] row-major
+  const bf16_t* wr;    // router [E][H]
+  const float* bias;   // [E] or nullptr
+  const bf16_t* w13;   // routed gate/up, packed
+  const bf16_t* w2;    // routed down, packed
+  const bf16_t* ws13;  // shared gate/up, packed (nullptr: no shared expert)
+  const bf16_t* ws2;   // shared down, packed
+  int T, H, E, I, I_s, k;
+  float* z;            // [T][E] logits without the bias (workspace)
+  bf16_t* xk;          // x chunk-major [H/8][T][8] (output)
+  bf16_t* hk;          // activations chunk-major [(k*I + I_s)/8][T][8] (workspace)
+  float* logits;       // [T][E] or nullptr
+  float* probs;        // [T][E]
+  float* block_scores; // [E] or nullptr
+  int32_t* experts;    // [k]
+  float* cw;           // [T][k]
+  float* gap;          // [1] or nullptr
+  dmoe_schedule sched;
+  void* y;             // [T][H], float32 or bf16
+};
+
+// ---- launch 1: router tiles and the shared expert's gate/up -----------------
+
+constexpr int kRouterBurst = 16;  // K-steps of 32 loaded at once per wave
+
+// Logits of 16 tokens x 16 experts over the whole hidden dimension (the four
+// waves each reduce a quarter, summed in wave order).  A = x rows (tokens),
+// B = router rows (experts): lane (q, c) ends with tokens 4q..4q+3 of expert
+// column c.
+__device__ void router_tile(const LayerParams& p, int tile, f32x4 (*red)[kWave]) {
+  const int T = p.T, H = p.H, E = p.E;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
+  const int ntt = (T + kTok - 1) / kTok;
+  const int tt = tile % ntt, et = tile / ntt;
+  const int kq = H / 4, k0 = wave * kq, steps = kq / 32;
+  const int t = min(tt * kTok + c, T - 1), e = min(et * kTok + c, E - 1);
+  const bf16_t* pa = p.x + static_cast<size_t>(t) * H + k0 + q * 8;
+  const bf16_t* pb = p.wr + static_cast<size_t>(e) * H + k0 + q * 8;
+  const bool write_x = et == 0 && tt * kTok + c < T;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < steps; s0 += kRouterBurst) {
+    const int ns = min(kRouterBurst, steps - s0);
+    bf16x8 a[kRouterBurst], b[kRouterBurst];
+#pragma unroll
+    for (int s = 0; s < kRouterBurst; ++s)
+      if (s < ns) {
+        a[s] = ld_bf16x8(pa + (s0 + s) * 32);
+        b[s] = ld_bf16x8(pb + (s0 + s) * 32);
+      }
+#pragma unroll
+    for (int s = 0; s < kRouterBurst; ++s)
+      if (s < ns) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b[s], acc, 0, 0, 0);
+    if (write_x) {
+#pragma unroll
+      for (int s = 0; s < kRouterBurst; ++s)
+        if (s < ns) {
+          const int j = ((k0 + (s0 + s) * 32) >> 3) + q;  // chunk of 8 features
+          *reinterpret_cast<bf16x8*>(p.xk + (static_cast<size_t>(j) * T + tt * kTok + c) * 8) = a[s];
+        }
+    }
+  }
+  if (wave > 0) red[wave - 1][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 0; w < kWaves - 1; ++w) acc += red[w][lane];
+  const int ec = et * kTok + c;
+  if (ec >= E) return;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int tr = tt * kTok + 4 * q + r;
+    if (tr < T) p.z[static_cast<size_t>(tr) * E + ec] = acc[r];
+  }
+}
+
+// SwiGLU of one lane's accumulators (g_i, g_i+1, u_i, u_i+1), scaled by w,
+// stored as the two bf16 activations of units i, i+1 of token `col`.
+__device__ __forceinline__ void store_h(bf16_t* hk, int T, int chunk, int col, int q, const f32x4& v, float w) {
+  const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2] * w);
+  const uint32_t h1 = f32_to_bf16(silu_f32(v[1]) * v[3] * w);
+  *reinterpret_cast<uint32_t*>(hk + (static_cast<size_t>(chunk) * T + col) * 8 + 2 * q) = h0 | (h1 << 16);
+}
+
+// Gate/up of packed tile `it` (8 intermediate units) of the shared expert
+// over all T tokens, read from the row-major x.
+template <int NT>
+__device__ void shared_gateup_tile(const LayerParams& p, int it, f32x4 (*red)[1][NT][kWave]) {
+  const int T = p.T, H = p.H;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
+  const int ksteps = H >> 5, steps = ksteps >> 2;
+  const bf16_t* pa = p.ws13 + (static_cast<size_t>(it) * ksteps + wave * steps) * kFrag + lane * 8;
+  const bf16_t* pb[NT];
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int tok = min(ct * kTok + c, T - 1);
+    pb[ct] = p.x + static_cast<size_t>(tok) * H + wave * (H / 4) + q * 8;
+  }
+  f32x4 acc[1][NT];
+  fdev::zero(acc);
+  fdev::WaveOps<NT, 16, 4, 1> w;
+  fdev::wave_dot(w, pa, 0, pb, 32, steps, acc, false);
+  fdev::reduce_waves(acc, red, wave, lane);
+  if (wave != 0) return;
+  const int chunk = (p.k * p.I) / 8 + it;
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int col = ct * kTok + c;
+    if (col < T) store_h(p.hk, T, chunk, col, q, acc[0][ct], 1.f);
+  }
+}
+
+template <int NT>
+__global__ __launch_bounds__(kThreads) void layer_router_shared_kernel(LayerParams p, int n_router) {
+  __shared__ f32x4 rred[kWaves - 1][kWave];
+  __shared__ f32x4 sred[kWaves - 1][1][NT][kWave];
+  if (static_cast<int>(blockIdx.x) < n_router)
+    router_tile(p, blockIdx.x, rred);
+  else
+    shared_gateup_tile<NT>(p, blockIdx.x - n_router, sred);
+}
+
+// ---- launch 2: the block's routing, then the routed gate/up ------------------
+
+constexpr int kRoundsMax = dev::kMaxK + 1;
+
+// LDS of the routing prologue (4-byte words): P [T][Es] probabilities, then
+// S [Es] block means.  Es = E rounded up to a multiple of 4.
+__host__ __device__ inline size_t prologue_words(int T, int E) {
+  const size_t Es = static_cast<size_t>(dev::pad4(E));
+  return (static_cast<size_t>(T) + 1) * Es;
+}
+
+template <int NQ, int NT>
+__global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerParams p) {
+  extern __shared__ float lds[];
+  __shared__ int sel[kRoundsMax];
+  __shared__ float selv[kRoundsMax];
+  __shared__ float bufv[kRoundsMax];
+  __shared__ int bufi[kRoundsMax];
+  __shared__ float wslot[NT * kTok];
+  __shared__ int slds[kWave];
+  __shared__ f32x4 red[kWaves - 1][1][NT][kWave];
+  const int T = p.T, E = p.E, k = p.k;
+  const int Es = dev::pad4(E);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int it = blockIdx.x, j = blockIdx.y;
+  const bool first = it == 0 && j == 0;  // writes the routing outputs
+  float* P = lds;
+  float* S = lds + static_cast<size_t>(T) * Es;
+
+  // 1. softmax of each token row (RB rows per wave in flight together)
+  {
+    constexpr int RB = 4 / NQ;
+    for (int t0 = wave; t0 < T; t0 += kWaves * RB) {
+      dev::RowPartials<NQ> r[RB];
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int t = t0 + u * kWaves;
+        if (t < T) dev::load_row<NQ>(p.z, static_cast<size_t>(T) * E, 1, p.bias, E, t, r[u]);
+      }
+      bool live[RB];
+      float* out[RB];
+      float* prow[RB];
+      float* lo[RB];
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int t = min(t0 + u * kWaves, T - 1);
+        live[u] = t0 + u * kWaves < T;
+        prow[u] = P + static_cast<size_t>(t) * Es;
+        out[u] = first ? p.probs + static_cast<size_t>(t) * E : prow[u];
+        lo[u] = first && p.logits ? p.logits + static_cast<size_t>(t) * E : nullptr;
+      }
+      dev::softmax_loaded<NQ, RB>(r, live, 1, p.bias != nullptr, E, out, prow, lo);
+    }
+  }
+  __syncthreads();
+
+  // 2. block means in token order, 3. top-(k+1) by one wave
+  const float n_tok = static_cast<float>(T);
+  for (int e = tid; e < E; e += kThreads) {
+    const float* pe = P + e;
+    float acc = 0.f;
+#pragma unroll 8
+    for (int t = 0; t < T; ++t) acc += pe[static_cast<size_t>(t) * Es];  // token order
+    const float v = acc / n_tok;
+    S[e] = v;
+    if (first && p.block_scores) p.block_scores[e] = v;
+  }
+  __syncthreads();
+  const int rounds = k < E ? k + 1 : k;
+  if (wave == 0) dev::wave_topk_radix_n<4 * NQ>(S, E, rounds, sel, selv, bufv, bufi);
+  __syncthreads();
+
+  // 4. combine weights: each token's probabilities on the selection,
+  //    renormalised (the denominator summed in slot order)
+  for (int t = tid; t < T; t += kThreads) {
+    const float* prow = P + static_cast<size_t>(t) * Es;
+    float denom = 0.f;
+    for (int jj = 0; jj < k; ++jj) denom += prow[sel[jj]];
+    wslot[t] = prow[sel[j]] / denom;
+    if (first)
+      for (int jj = 0; jj < k; ++jj) p.cw[static_cast<size_t>(t) * k + jj] = prow[sel[jj]] / denom;
+  }
+  if (first) {
+    for (int jj = tid; jj < k; jj += kThreads) p.experts[jj] = sel[jj];
+    if (p.gap && tid == 0) p.gap[0] = k < E ? selv[k - 1] - selv[k] : INFINITY;
+    dev::schedule_one_group(sel, T, k, slds, p.sched);  // all threads; synchronises
+  }
+  __syncthreads();
+
+  // 5. packed tile `it` of expert sel[j]'s gate/up over all tokens
+  const int H = p.H, q = lane >> 4, c = lane & 15;
+  const int ksteps = H >> 5, steps = ksteps >> 2;
+  const bf16_t* W = p.w13 + static_cast<size_t>(sel[j]) * 2 * p.I * H;
+  const bf16_t* pa = W + (static_cast<size_t>(it) * ksteps + wave * steps) * kFrag + lane * 8;
+  const int chunk0 = wave * steps * 4 + q;
+  const bf16_t* pb[NT];
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int tok = min(ct * kTok + c, T - 1);
+    pb[ct] = p.xk + (static_cast<size_t>(chunk0) * T + tok) * 8;
+  }
+  f32x4 acc[1][NT];
+  fdev::zero(acc);
+  fdev::WaveOps<NT, 16, 4, 1> w;
+  fdev::wave_dot(w, pa, 0, pb, 32 * T, steps, acc, false);
+  fdev::reduce_waves(acc, red, wave, lane);
+  if (wave != 0) return;
+  const int chunk = (j * p.I) / 8 + it;
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int col = ct * kTok + c;
+    if (col < T) store_h(p.hk, T, chunk, col, q, acc[0][ct], wslot[col]);
+  }
+}
+
+// ---- launch 3: down projection of every expert and the combine ---------------
+
+// Waves of the down kernel: k routed experts + the shared expert, at most 12
+// (three waves per SIMD leave each wave room for a 16-step weight burst).
+constexpr int kMaxSegments = 12;
+
+__device__ __forceinline__ void store_y(float* y, const f32x4& v) { *reinterpret_cast<f32x4*>(y) = v; }
+__device__ __forceinline__ void store_y(bf16_t* y, const f32x4& v) {
+  const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+  const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+  *reinterpret_cast<uint2*>(y) = make_uint2(lo, hi);
+}
+
+// Workgroup = one packed down tile jt (16 output features) x all T tokens;
+// wave j < k reduces over slot j's expert, wave k (when present) over the
+// shared expert.
+template <int NT, typename OutT>
+__global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kernel(LayerParams p) {
+  __shared__ f32x4 red[kMaxSegments - 1][NT][kWave];
+  const int T = p.T, H = p.H, k = p.k;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
+  const int nw = blockDim.x >> 6;
+  const int jt = blockIdx.x;
+  const bool shared = wave == k;
+  const int Kd = shared ? p.I_s : p.I;
+  const int ksteps = Kd >> 5;
+  // token operand first (it does not depend on the routing), then the expert
+  const int chunk0 = (wave * p.I) / 8 + q;  // wave == k: the shared block starts at k*I
+  const bf16_t* pb[NT];
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int tok = min(ct * kTok + c, T - 1);
+    pb[ct] = p.hk + (static_cast<size_t>(chunk0) * T + tok) * 8;
+  }
+  const bf16_t* W = shared ? p.ws2 : p.w2 + static_cast<size_t>(p.experts[wave]) * H * p.I;
+  const bf16_t* pa = W + static_cast<size_t>(jt) * ksteps * kFrag + lane * 8;
+  f32x4 acc[1][NT];
+  fdev::zero(acc);
+  fdev::WaveOps<NT, 16, 4, 1> w;
+  fdev::wave_dot(w, pa, 0, pb, 32 * T, ksteps, acc, false);
+  if (wave > 0) {
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) red[wave - 1][ct][lane] = acc[0][ct];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  for (int ww = 0; ww < nw - 1; ++ww)
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) acc[0][ct] += red[ww][ct][lane];  // wave order
+  OutT* y = static_cast<OutT*>(p.y);
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int col = ct * kTok + c;
+    if (col < T) store_y(y + static_cast<size_t>(col) * H + jt * 16 + 4 * q, acc[0][ct]);
+  }
+}
+
+template <int NT>
+hipError_t launch_nt(const LayerParams& p, dmoe_dtype y_dt, hipStream_t s) {
+  const int n_router = ((p.T + kTok - 1) / kTok) * ((p.E + kTok - 1) / kTok);
+  const int n_shared = p.ws13 ? p.I_s / 8 : 0;
+  layer_router_shared_kernel<NT><<<n_router + n_shared, kThreads, 0, s>>>(p, n_router);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const size_t lds = prologue_words(p.T, p.E) * sizeof(float);
+  if (p.E <= 256)
+    layer_route_gateup_kernel<1, NT><<<dim3(p.I / 8, p.k), kThreads, lds, s>>>(p);
+  else
+    layer_route_gateup_kernel<2, NT><<<dim3(p.I / 8, p.k), kThreads, lds, s>>>(p);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int waves = p.k + (p.ws13 ? 1 : 0);
+  if (y_dt == DMOE_F32)
+    layer_down_combine_kernel<NT, float><<<p.H / 16, waves * kWave, 0, s>>>(p);
+  else
+    layer_down_combine_kernel<NT, bf16_t><<<p.H / 16, waves * kWave, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, int I_s, int k) {
+  if (dt != DMOE_BF16 || n_blocks != 1) return false;
+  if (T < 1 || T > 4 * kTok || E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
+  if (k + (I_s > 0 ? 1 : 0) > kMaxSegments) return false;
+  if (H % 128 || I % 128 || I_s % 128) return false;
+  return prologue_words(T, E) * sizeof(float) <= 48 * 1024;
+}
+
+size_t layer_fused_workspace_bytes(int T, int E, int I, int I_s, int k) {
+  const size_t z = (static_cast<size_t>(T) * E * sizeof(float) + 255) & ~static_cast<size_t>(255);
+  return z + (static_cast<size_t>(k) * I + I_s) * T * sizeof(bf16_t);
+}
+
+hipError_t launch_layer_fused(const LayerArgs& a, hipStream_t s) {
+  const size_t zb = (static_cast<size_t>(a.T) * a.E * sizeof(float) + 255) & ~static_cast<size_t>(255);
+  LayerParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w_router), a.bias,
+                static_cast<const bf16_t*>(a.w13), static_cast<const bf16_t*>(a.w2),
+                static_cast<const bf16_t*>(a.ws13), static_cast<const bf16_t*>(a.ws2), a.T, a.H, a.E, a.I, a.I_s,
+                a.k, static_cast<float*>(a.workspace),
+                static_cast<bf16_t*>(a.x_chunked),
+                reinterpret_cast<bf16_t*>(static_cast<char*>(a.workspace) + zb), a.logits, a.probs, a.block_scores,
+                a.experts, a.combine_w, a.gap, a.sched, a.y};
+  if (a.T <= kTok) return launch_nt<1>(p, a.y_dt, s);
+  if (a.T <= 2 * kTok) return launch_nt<2>(p, a.y_dt, s);
+  return launch_nt<4>(p, a.y_dt, s);
+}
+
+}  // namespace dmoe

@@ -99,6 +99,8 @@ class MoELayer:
             self._side = torch.cuda.Stream(device=device)
         # The layer output is accumulated in fp32; it is stored as out_dtype.
         self.y = torch.empty((T, H), dtype=out_dtype, device=device)
+        lbytes = lib.dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt)
+        self.layer_ws = torch.empty((max(lbytes, 16),), dtype=torch.uint8, device=device)
 
     def max_work(self, routing: str) -> int:
         """Work items the expert FFN's grid is sized for (dmoe_schedule_max_work)."""
@@ -173,9 +175,24 @@ class MoELayer:
         lib.dmoe_combine(self.slot_out, self.combine_w, self.shared_out, self.T, self.H, self.k, self.y,
                          stream)
 
-    def forward(self, x, w: dict, routing: str = "block", stream=None, fused_routing: bool = True) -> torch.Tensor:
+    def forward(self, x, w: dict, routing: str = "block", stream=None, fused_routing: bool = True,
+                chained: bool = False) -> torch.Tensor:
         """Whole layer on hidden states x[T, H] with weights from
-        :func:`pack_weights`; returns (a view of) y[T, H]."""
+        :func:`pack_weights`; returns (a view of) y[T, H].
+
+        By default one dmoe_moe_forward call (three kernels for a block-routed
+        single block, else the chain below inside the library).  chained=True
+        (or overlap_shared) enqueues the routing, expert FFN and combine entry
+        points one by one instead."""
+        if not chained and not self.overlap_shared and fused_routing:
+            self._x = x
+            lib.dmoe_moe_forward(x, w["w_router"], w.get("bias"), w["w13"], w["w2"], w.get("ws13"), w.get("ws2"),
+                                 self.NB, self.bs, self.H, self.E, self.I, self.I_s, self.k, routing, self.top_p,
+                                 self.min_coreset, self.logits, self.probs, self.x_chunked,
+                                 self.block_scores, self.experts(routing), self.combine_w, self.gaps(routing),
+                                 self.coreset, self.coreset_size, self.sched, self.slot_out, self.shared_out,
+                                 self.layer_ws, self.y, stream)
+            return self.y
         main = stream if stream is not None else torch.cuda.current_stream()
         if self.overlap_shared:
             # the shared expert needs no routing: pack x for it and run it

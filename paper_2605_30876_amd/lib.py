@@ -33,7 +33,7 @@ EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggre
            "dmoe_schedule_scratch_ints", "dmoe_route_block",
            "dmoe_route_token", "dmoe_route_topp", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
            "dmoe_expert_ffn", "dmoe_expert_ffn_noalloc", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
-           "dmoe_last_error", "dmoe_version")
+           "dmoe_moe_forward_workspace_size", "dmoe_moe_forward", "dmoe_last_error", "dmoe_version")
 
 
 class DmoeError(RuntimeError):
@@ -50,6 +50,18 @@ class dmoe_schedule(ctypes.Structure):
                 ("offsets", ctypes.c_void_p), ("row_token", ctypes.c_void_p),
                 ("row_slot", ctypes.c_void_p), ("n_work", ctypes.c_void_p), ("work", ctypes.c_void_p),
                 ("scratch", ctypes.c_void_p)]
+
+
+DMOE_ROUTE_BLOCK, DMOE_ROUTE_TOKEN, DMOE_ROUTE_TOPP = 0, 1, 2
+ROUTING = {"block": DMOE_ROUTE_BLOCK, "token": DMOE_ROUTE_TOKEN, "topp": DMOE_ROUTE_TOPP}
+
+
+class dmoe_layer_buffers(ctypes.Structure):
+    _fields_ = [("logits", ctypes.c_void_p), ("probs", ctypes.c_void_p), ("x_chunked", ctypes.c_void_p),
+                ("block_scores", ctypes.c_void_p), ("experts", ctypes.c_void_p), ("combine_w", ctypes.c_void_p),
+                ("gap", ctypes.c_void_p), ("coreset", ctypes.c_void_p), ("coreset_size", ctypes.c_void_p),
+                ("sched", dmoe_schedule), ("slot_out", ctypes.c_void_p), ("shared_out", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t)]
 
 
 _P = ctypes.c_void_p
@@ -77,6 +89,9 @@ _SIGS = {
     "dmoe_shared_ffn_workspace_size": ([_I, _I, _I], _S),
     "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
+    "dmoe_moe_forward_workspace_size": ([_I] * 7 + [_I], _S),
+    "dmoe_moe_forward": ([_P] * 7 + [_I] * 8 + [_I, ctypes.c_float, _I, ctypes.POINTER(dmoe_layer_buffers), _P, _I, _P],
+                         _I),
     "dmoe_last_error": ([], ctypes.c_char_p),
     "dmoe_version": ([], ctypes.c_char_p),
 }
@@ -280,6 +295,24 @@ def dmoe_expert_ffn_noalloc(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k
 def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):
     _check(load().dmoe_combine(ptr(slot_out), ptr(combine_w), ptr(shared_out), dtype_code(y), T, H,
                                k, ptr(y), stream_handle(stream)))
+
+
+def dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt) -> int:
+    return int(load().dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt))
+
+
+def dmoe_moe_forward(x, w_router, bias, w13, w2, ws13, ws2, n_blocks, block_size, H, E, I, I_s, k, routing: str,
+                     top_p, min_coreset, logits, probs, x_chunked, block_scores, experts, combine_w, gap, coreset,
+                     coreset_size, sched: Schedule, slot_out, shared_out, workspace, y, stream=None):
+    """One MoE layer forward; ``routing`` is "block", "token" or "topp"; the
+    buffers are gathered into a dmoe_layer_buffers (a host struct)."""
+    buf = dmoe_layer_buffers(ptr(logits), ptr(probs), ptr(x_chunked), ptr(block_scores), ptr(experts),
+                             ptr(combine_w), ptr(gap), ptr(coreset), ptr(coreset_size), sched.as_c(), ptr(slot_out),
+                             ptr(shared_out), ptr(workspace), _nbytes(workspace))
+    _check(load().dmoe_moe_forward(ptr(x), ptr(w_router), ptr(bias), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
+                                   dtype_code(x), n_blocks, block_size, H, E, I, I_s, k, ROUTING[routing],
+                                   float(top_p), min_coreset, ctypes.byref(buf), ptr(y), dtype_code(y),
+                                   stream_handle(stream)))
 
 
 def dmoe_version() -> str:

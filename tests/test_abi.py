@@ -366,3 +366,37 @@ def test_ffn_noalloc_validation(L, buf):
     assert _ffn_noalloc(L, p, max_work=0)[0] == INV
     assert _ffn_noalloc(L, p, ws2=None)[0] == INV
     assert _ffn_noalloc(L, p, H=2000)[0] == UNS
+
+
+def _moe(L, p, ws_bytes=1 << 30, **kw):
+    a = dict(x=p, wr=p, bias=None, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, NB=1, bs=32, H=2048, E=256, I=512,
+             I_s=512, k=8, routing=lib.DMOE_ROUTE_BLOCK, top_p=0.6, min_c=8, y=p, y_dt=lib.DMOE_F32)
+    bufkw = {f: kw.pop(f) for f in list(kw) if f in ("probs", "coreset", "shared_out", "workspace")}
+    a.update(kw)
+    sched = lib.dmoe_schedule(p, p, p, p, p, p, p, None)
+    buf = lib.dmoe_layer_buffers(None, bufkw.get("probs", p), p, None, p, p, None, bufkw.get("coreset", None), None,
+                                 sched, p, bufkw.get("shared_out", p), bufkw.get("workspace", p), ws_bytes)
+    return status(L, "dmoe_moe_forward", a["x"], a["wr"], a["bias"], a["w13"], a["w2"], a["ws13"], a["ws2"],
+                  a["dt"], a["NB"], a["bs"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["routing"], a["top_p"],
+                  a["min_c"], ctypes.byref(buf), a["y"], a["y_dt"], None)
+
+
+def test_moe_forward_validation(L, buf):
+    _, p = buf
+    INV, UNS = lib.DMOE_ERR_INVALID_ARG, lib.DMOE_ERR_UNSUPPORTED
+    need = lib.dmoe_moe_forward_workspace_size(1, 32, 2048, 256, 512, 512, 8, lib.DMOE_BF16)
+    assert need > 0
+    st, msg = _moe(L, p, ws_bytes=need - 1)
+    assert st == INV and "workspace" in msg
+    assert _moe(L, p, probs=None)[0] == INV
+    assert _moe(L, p, routing=7)[0] == INV
+    assert _moe(L, p, routing=lib.DMOE_ROUTE_TOPP)[0] == INV  # no coreset buffers
+    assert _moe(L, p, shared_out=None)[0] == INV              # shared pointers inconsistent
+    assert _moe(L, p, y=p + 4)[0] == INV
+    assert _moe(L, p, k=0)[0] == INV
+    assert _moe(L, p, I=500)[0] == UNS
+    assert _moe(L, p, E=600)[0] == UNS
+    st = L.dmoe_moe_forward(p, p, None, p, p, p, p, lib.DMOE_BF16, 1, 32, 2048, 256, 512, 512, 8, 0, 0.6, 8, None, p,
+                            lib.DMOE_F32, None)
+    assert st == INV  # buf is NULL
+    assert lib.dmoe_moe_forward_workspace_size(1, 32, 2048, 600, 512, 512, 8, lib.DMOE_BF16) == 0

@@ -1,0 +1,91 @@
+"""dmoe_moe_forward, the one-call layer.  A block-routed single bf16 block
+runs as three kernels (router + shared gate/up, routing + routed gate/up,
+down + combine); these tests check that path on single blocks of several
+shapes against the oracle and against the chained entry points' routing.
+Marked ``gpu``."""
+import numpy as np
+import pytest
+import torch
+
+from dmoe_synth import get_config, make_inputs
+from paper_2605_30876_amd import lib
+from paper_2605_30876_amd.layer import MoELayer, pack_weights
+from parity import PROB_TOL, run_and_check
+
+pytestmark = pytest.mark.gpu
+
+# (base config, overrides): one block each, spanning 1, 2 and 4 token tiles,
+# E above 256 (two register quarters per softmax lane), no shared expert, a
+# Zipf-biased router, and k = 11 (twelve waves in the down kernel).
+SINGLE = {
+    "t24": ("small_bf16", dict(NB=1, bs=24)),
+    "t5_noshared_zipf": ("small_bf16_zipf", dict(NB=1, bs=5)),
+    "t40_corr": ("small_bf16_corr", dict(NB=1, bs=40)),
+    "t17_e300_k11": ("small_bf16", dict(NB=1, bs=17, E=300, k=11)),
+    "t64_e128": ("small_bf16", dict(NB=1, bs=64, E=128)),
+    "t1": ("small_bf16", dict(NB=1, bs=1)),
+}
+
+
+def _layer(cfg, out_dtype=torch.float32):
+    return MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device="cuda", out_dtype=out_dtype)
+
+
+@pytest.mark.parametrize("name", list(SINGLE))
+def test_single_block_layer(gpu_lib, name):
+    base, kw = SINGLE[name]
+    cfg = get_config(base).with_(name=f"one_block_{name}", **kw)
+    print("case", cfg.name, flush=True)
+    d = {k: (None if v is None else v.cuda()) for k, v in make_inputs(cfg, seed=11).items()}
+    w = pack_weights(d)
+    layer = _layer(cfg)
+    layer.slot_out.fill_(float("nan"))
+    rep = run_and_check(cfg, d, "block", layer, packed=w)
+    torch.cuda.synchronize()
+    # the three-kernel path ran: the chained path's slot outputs were not written
+    assert torch.isnan(layer.slot_out).all()
+    print("  ", {k: v for k, v in rep.items() if k != "near_ties"}, flush=True)
+
+    # its routing agrees with dmoe_route_block's (same routines; logits
+    # reduced in one pass instead of slices)
+    ref = _layer(cfg)
+    ref.route(d["x"], w["w_router"], w.get("bias"), "block")
+    torch.cuda.synchronize()
+    assert float((ref.probs - layer.probs).abs().max()) <= PROB_TOL
+    assert float((ref.block_scores - layer.block_scores).abs().max()) <= PROB_TOL
+    if float(ref.block_gap[0]) >= 1e-6:
+        assert torch.equal(ref.block_experts, layer.block_experts)
+        assert float((ref.combine_w - layer.combine_w).abs().max()) <= PROB_TOL
+        assert torch.equal(ref.sched.work[:cfg.k], layer.sched.work[:cfg.k])
+        assert int(ref.sched.n_work[0]) == int(layer.sched.n_work[0])
+
+
+def test_single_block_bf16_output_and_chain(gpu_lib):
+    """bf16 y is the RNE rounding of the fp32 y; the chained path (the same
+    routing, per-slot outputs and a combine) agrees within the tolerance."""
+    cfg = get_config("decode_b1")
+    d = make_inputs(cfg, seed=12, device="cuda")
+    w = pack_weights(d)
+    l32, l16 = _layer(cfg), _layer(cfg, torch.bfloat16)
+    y32 = l32.forward(d["x"], w, "block").clone()
+    y16 = l16.forward(d["x"], w, "block").clone()
+    yc = l32.forward(d["x"], w, "block", chained=True).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+    rms = float(y32.double().pow(2).mean().sqrt())
+    assert float((y32 - yc).abs().max()) <= 2e-2 * rms
+
+
+def test_layer_workspace_too_small(gpu_lib):
+    cfg = get_config("decode_b1")
+    layer = _layer(cfg)
+    d = make_inputs(cfg, seed=0, device="cuda")
+    w = pack_weights(d)
+    small = torch.empty((64,), dtype=torch.uint8, device="cuda")
+    with pytest.raises(lib.DmoeError) as ei:
+        lib.dmoe_moe_forward(d["x"], w["w_router"], None, w["w13"], w["w2"], w["ws13"], w["ws2"], cfg.NB, cfg.bs,
+                             cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, "block", 0.6, cfg.k, None, layer.probs,
+                             layer.x_chunked, None, layer.block_experts, layer.combine_w, None, None, None,
+                             layer.sched, layer.slot_out, layer.shared_out, small, layer.y)
+    assert ei.value.status == lib.DMOE_ERR_INVALID_ARG
+    assert np.isfinite(lib.dmoe_moe_forward_workspace_size(1, 32, 2048, 256, 512, 512, 8, lib.DMOE_BF16))
