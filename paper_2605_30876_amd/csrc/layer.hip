@@ -171,11 +171,168 @@ __global__ __launch_bounds__(kThreads) void layer_router_shared_kernel(LayerPara
 
 constexpr int kRoundsMax = dev::kMaxK + 1;
 
+// The first `rounds` of S[0..E) (LDS; E <= kThreads, rounds <= 16) in (score
+// desc, id asc) order, by all threads of the workgroup; the same selection
+// as dev::wave_topk_radix.  Thread e holds expert e's order key.  A lower
+// bound of the rounds-th largest key: the rounds-th largest of the maxima of
+// the 16-lane groups (each of those groups holds an element at least that
+// large).  Only keys at or above it are candidates, and each candidate's rank
+// among them, by (key, id), is its rank in the row.  Called by all threads.
+constexpr int kCandMax = kThreads;
+__device__ void block_topk_small(const float* S, int E, int rounds, int* sel, float* selv, uint32_t* gmax,
+                                 uint32_t* ckey, int* cid, int* wcount) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // excluded threads (e >= E) take key 0, below every real key (real keys >= 1)
+  const uint32_t key = tid < E ? max(dev::order_key(S[tid]), 1u) : 0u;
+  uint32_t g = key;  // max over the 16 lanes of the row: rotations by 1, 2, 4, 8
+  g = max(g, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(g), 0x121, 0xF, 0xF, false)));
+  g = max(g, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(g), 0x122, 0xF, 0xF, false)));
+  g = max(g, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(g), 0x124, 0xF, 0xF, false)));
+  g = max(g, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(g), 0x128, 0xF, 0xF, false)));
+  if ((lane & 15) == 0) gmax[tid >> 4] = g;
+  __syncthreads();
+  if (tid < 16) {  // rank of group tid's maximum among the 16 (ties by group index)
+    const uint32_t mine = gmax[tid];
+    int r = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) r += dev::key_before(gmax[i], i, mine, tid) ? 1 : 0;
+    if (r == rounds - 1) gmax[16] = mine;
+  }
+  __syncthreads();
+  const uint32_t bound = gmax[16];
+  const bool cand = key >= bound && tid < E;
+  const uint64_t m = __ballot(cand);
+  if (lane == 0) wcount[wave] = __popcll(m);
+  __syncthreads();
+  int base = 0, ncand = 0;
+#pragma unroll
+  for (int w = 0; w < kThreads / kWave; ++w) {
+    base += w < wave ? wcount[w] : 0;
+    ncand += wcount[w];
+  }
+  if (cand) {
+    const int pos = base + dev::lanes_below(m);
+    ckey[pos] = key;
+    cid[pos] = tid;
+  }
+  if (tid < 3) {  // pad to a multiple of 4 with entries that rank after everything
+    ckey[ncand + tid] = 0u;
+    cid[ncand + tid] = dev::kNone;
+  }
+  __syncthreads();
+  if (cand) {
+    int r = 0;
+    const uint4* k4 = reinterpret_cast<const uint4*>(ckey);
+    const int4* i4 = reinterpret_cast<const int4*>(cid);
+    for (int i = 0; i < (ncand + 3) / 4; ++i) {
+      const uint4 kk = k4[i];
+      const int4 ii = i4[i];
+      r += (dev::key_before(kk.x, ii.x, key, tid) ? 1 : 0) + (dev::key_before(kk.y, ii.y, key, tid) ? 1 : 0) +
+           (dev::key_before(kk.z, ii.z, key, tid) ? 1 : 0) + (dev::key_before(kk.w, ii.w, key, tid) ? 1 : 0);
+    }
+    if (r < rounds) {
+      sel[r] = tid;
+      selv[r] = dev::key_value(key);
+    }
+  }
+}
+
 // LDS of the routing prologue (4-byte words): P [T][Es] probabilities, then
 // S [Es] block means.  Es = E rounded up to a multiple of 4.
 __host__ __device__ inline size_t prologue_words(int T, int E) {
   const size_t Es = static_cast<size_t>(dev::pad4(E));
   return (static_cast<size_t>(T) + 1) * Es;
+}
+
+// Softmax of the T logit rows (p.z, plus the bias), max-subtracted, with the
+// hardware exp2 on z*log2(e) - m*log2(e) and one reciprocal per row.  Eight
+// lanes share a row: lane l of wave w takes row 8*(w + 4*pass) + l/8 and the
+// experts 4*(s + 8*i) + c (s = l%8, i < 8*NQ, c < 4), so each of its float4
+// loads is one 16-byte piece of a 128-byte run the row's 8 lanes read
+// together, and a row's max and sum take three lane exchanges (within the 8
+// lanes) instead of six.  A wave handles 8 rows in one pass, all of their
+// loads in flight together.  Probabilities go to P (LDS, row stride Es) and,
+// for the first workgroup, to probs (and the logits to logits when requested).
+template <int NQ, int NPASS>
+__device__ void rows_softmax(const LayerParams& p, float* P, int Es, bool first) {
+  // E % 4 == 0 (checked by layer_fused_fits): a lane's pieces lie wholly in
+  // or past the row, and pieces past it are masked, not branched around, so
+  // all loads of a pass are issued before the first wait.
+  constexpr int NV = 8 * NQ;  // float4 pieces per lane
+  const int T = p.T, E = p.E;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int sl = lane & 7;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 b[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) b[i] = zero4;
+  if (p.bias) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int e0 = 4 * (sl + 8 * i);
+      const f32x4 v = *reinterpret_cast<const f32x4*>(p.bias + min(e0, E - 4));
+      b[i] = e0 < E ? v : zero4;
+    }
+  }
+#pragma unroll
+  for (int pass = 0; pass < NPASS; ++pass) {
+    const int t = 8 * (wave + kWaves * pass) + (lane >> 3);
+    const float* src = p.z + static_cast<size_t>(min(t, T - 1)) * E;
+    f32x4 z[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) z[i] = *reinterpret_cast<const f32x4*>(src + min(4 * (sl + 8 * i), E - 4));
+    float* lo = first && p.logits && t < T ? p.logits + static_cast<size_t>(t) * E : nullptr;
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const bool in = 4 * (sl + 8 * i) < E;
+      z[i] += b[i];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) m = fmaxf(m, in ? z[i][c] : -INFINITY);
+    }
+    if (lo) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int e0 = 4 * (sl + 8 * i);
+        if (e0 < E) *reinterpret_cast<f32x4*>(lo + e0) = z[i];
+      }
+    }
+    // max over the row's 8 lanes: xor 1, xor 2, then mirror within the 8
+    m = fmaxf(m, dev::dppf<dev::kDppXor1>(m, m));
+    m = fmaxf(m, dev::dppf<dev::kDppXor2>(m, m));
+    m = fmaxf(m, dev::dppf<dev::kDppHalfMirror>(m, m));
+    const float ml = m * dev::kLog2e;
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const bool in = 4 * (sl + 8 * i) < E;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        z[i][c] = dev::exp2_hw(fmaf(z[i][c], dev::kLog2e, -ml));
+        sum += in ? z[i][c] : 0.f;
+      }
+    }
+    sum += dev::dppf<dev::kDppXor1>(sum, sum);
+    sum += dev::dppf<dev::kDppXor2>(sum, sum);
+    sum += dev::dppf<dev::kDppHalfMirror>(sum, sum);
+    const float rs = __builtin_amdgcn_rcpf(sum);
+    if (t < T) {
+      float* prow = P + static_cast<size_t>(t) * Es;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int e0 = 4 * (sl + 8 * i);
+        if (e0 < E) *reinterpret_cast<f32x4*>(prow + e0) = z[i] * rs;
+      }
+      if (first) {
+        float* out = p.probs + static_cast<size_t>(t) * E;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+          const int e0 = 4 * (sl + 8 * i);
+          if (e0 < E) *reinterpret_cast<f32x4*>(out + e0) = z[i] * rs;
+        }
+      }
+    }
+  }
 }
 
 template <int NQ, int NT>
@@ -185,9 +342,13 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   __shared__ float selv[kRoundsMax];
   __shared__ float bufv[kRoundsMax];
   __shared__ int bufi[kRoundsMax];
-  __shared__ float wslot[NT * kTok];
   __shared__ int slds[kWave];
+  __shared__ float wslot[NT * kTok];
   __shared__ f32x4 red[kWaves - 1][1][NT][kWave];
+  __shared__ uint32_t gmax[17];
+  __shared__ __align__(16) uint32_t ckey[kCandMax + 4];
+  __shared__ __align__(16) int cid[kCandMax + 4];
+  __shared__ int wcount[kWaves];
   const int T = p.T, E = p.E, k = p.k;
   const int Es = dev::pad4(E);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -196,31 +357,9 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   float* P = lds;
   float* S = lds + static_cast<size_t>(T) * Es;
 
-  // 1. softmax of each token row (RB rows per wave in flight together)
-  {
-    constexpr int RB = 4 / NQ;
-    for (int t0 = wave; t0 < T; t0 += kWaves * RB) {
-      dev::RowPartials<NQ> r[RB];
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int t = t0 + u * kWaves;
-        if (t < T) dev::load_row<NQ>(p.z, static_cast<size_t>(T) * E, 1, p.bias, E, t, r[u]);
-      }
-      bool live[RB];
-      float* out[RB];
-      float* prow[RB];
-      float* lo[RB];
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        const int t = min(t0 + u * kWaves, T - 1);
-        live[u] = t0 + u * kWaves < T;
-        prow[u] = P + static_cast<size_t>(t) * Es;
-        out[u] = first ? p.probs + static_cast<size_t>(t) * E : prow[u];
-        lo[u] = first && p.logits ? p.logits + static_cast<size_t>(t) * E : nullptr;
-      }
-      dev::softmax_loaded<NQ, RB>(r, live, 1, p.bias != nullptr, E, out, prow, lo);
-    }
-  }
+  // 1. softmax of each token row: wave w owns rows w, w + 4, ..., all of
+  //    whose loads are issued at once (one memory round trip)
+  rows_softmax<NQ, (NT * kTok + 8 * kWaves - 1) / (8 * kWaves)>(p, P, Es, first);
   __syncthreads();
 
   // 2. block means in token order, 3. top-(k+1) by one wave
@@ -236,23 +375,10 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   }
   __syncthreads();
   const int rounds = k < E ? k + 1 : k;
-  if (wave == 0) dev::wave_topk_radix_n<4 * NQ>(S, E, rounds, sel, selv, bufv, bufi);
-  __syncthreads();
-
-  // 4. combine weights: each token's probabilities on the selection,
-  //    renormalised (the denominator summed in slot order)
-  for (int t = tid; t < T; t += kThreads) {
-    const float* prow = P + static_cast<size_t>(t) * Es;
-    float denom = 0.f;
-    for (int jj = 0; jj < k; ++jj) denom += prow[sel[jj]];
-    wslot[t] = prow[sel[j]] / denom;
-    if (first)
-      for (int jj = 0; jj < k; ++jj) p.cw[static_cast<size_t>(t) * k + jj] = prow[sel[jj]] / denom;
-  }
-  if (first) {
-    for (int jj = tid; jj < k; jj += kThreads) p.experts[jj] = sel[jj];
-    if (p.gap && tid == 0) p.gap[0] = k < E ? selv[k - 1] - selv[k] : INFINITY;
-    dev::schedule_one_group(sel, T, k, slds, p.sched);  // all threads; synchronises
+  if (E <= kThreads && rounds <= 16) {
+    block_topk_small(S, E, rounds, sel, selv, gmax, ckey, cid, wcount);
+  } else if (wave == 0) {
+    dev::wave_topk_radix_n<4 * NQ>(S, E, rounds, sel, selv, bufv, bufi);
   }
   __syncthreads();
 
@@ -272,8 +398,39 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   fdev::zero(acc);
   fdev::WaveOps<NT, 16, 4, 1> w;
   fdev::wave_dot(w, pa, 0, pb, 32 * T, steps, acc, false);
+
+  // 6. the routing outputs (workgroup (0, 0), while the other workgroups
+  //    stream): the selection, gap, every token's combine weights (its
+  //    probabilities on the selection, renormalised, summed in slot order) and
+  //    the closed-form schedule
+  if (first) {
+    for (int i = tid; i < T * k; i += kThreads) {
+      const int t = i / k, jj = i - t * k;
+      const float* prow = P + static_cast<size_t>(t) * Es;
+      float denom = 0.f;
+      for (int j2 = 0; j2 < k; ++j2) denom += prow[sel[j2]];
+      p.cw[i] = prow[sel[jj]] / denom;
+    }
+    for (int jj = tid; jj < k; jj += kThreads) p.experts[jj] = sel[jj];
+    if (p.gap && tid == 0) p.gap[0] = k < E ? selv[k - 1] - selv[k] : INFINITY;
+    dev::schedule_one_group(sel, T, k, slds, p.sched);  // all threads; synchronises
+  }
+  // 7. slot j's combine weight of every token, a quarter of the tokens per
+  //    wave (read by wave 0 after the barrier of the reduction)
+  {
+    constexpr int kPer = NT * kTok / kWaves;  // tokens per wave
+    const int t = wave * kPer + lane;
+    if (lane < kPer && t < T) {
+      const float* prow = P + static_cast<size_t>(t) * Es;
+      float denom = 0.f;
+#pragma unroll 8
+      for (int j2 = 0; j2 < k; ++j2) denom += prow[sel[j2]];  // slot order
+      wslot[t] = prow[sel[j]] / denom;
+    }
+  }
   fdev::reduce_waves(acc, red, wave, lane);
   if (wave != 0) return;
+  // 8. SwiGLU scaled by the weights
   const int chunk = (j * p.I) / 8 + it;
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
@@ -295,16 +452,19 @@ __device__ __forceinline__ void store_y(bf16_t* y, const f32x4& v) {
   *reinterpret_cast<uint2*>(y) = make_uint2(lo, hi);
 }
 
-// Workgroup = one packed down tile jt (16 output features) x all T tokens;
-// wave j < k reduces over slot j's expert, wave k (when present) over the
-// shared expert.
-template <int NT, typename OutT>
+// Workgroup = one packed down tile jt (16 output features) x one tile of 16
+// tokens; wave j < k reduces over slot j's expert, wave k (when present) over
+// the shared expert.  Grid index tt * (H/16) + jt: the token tiles of one
+// feature tile are dispatched to the same XCD (H/16 is a multiple of the 8
+// XCDs), so their second read of the tile's weights is served by its L2.
+template <typename OutT>
 __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kernel(LayerParams p) {
+  constexpr int NT = 1;
   __shared__ f32x4 red[kMaxSegments - 1][NT][kWave];
   const int T = p.T, H = p.H, k = p.k;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
   const int nw = blockDim.x >> 6;
-  const int jt = blockIdx.x;
+  const int jt = blockIdx.x % (H / 16), tt = blockIdx.x / (H / 16);
   const bool shared = wave == k;
   const int Kd = shared ? p.I_s : p.I;
   const int ksteps = Kd >> 5;
@@ -313,7 +473,7 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
   const bf16_t* pb[NT];
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
-    const int tok = min(ct * kTok + c, T - 1);
+    const int tok = min((tt + ct) * kTok + c, T - 1);
     pb[ct] = p.hk + (static_cast<size_t>(chunk0) * T + tok) * 8;
   }
   const bf16_t* W = shared ? p.ws2 : p.w2 + static_cast<size_t>(p.experts[wave]) * H * p.I;
@@ -334,7 +494,7 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
   OutT* y = static_cast<OutT*>(p.y);
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
-    const int col = ct * kTok + c;
+    const int col = (tt + ct) * kTok + c;
     if (col < T) store_y(y + static_cast<size_t>(col) * H + jt * 16 + 4 * q, acc[0][ct]);
   }
 }
@@ -354,10 +514,11 @@ hipError_t launch_nt(const LayerParams& p, dmoe_dtype y_dt, hipStream_t s) {
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int waves = p.k + (p.ws13 ? 1 : 0);
+  const unsigned down_grid = (p.H / 16) * ((p.T + kTok - 1) / kTok);
   if (y_dt == DMOE_F32)
-    layer_down_combine_kernel<NT, float><<<p.H / 16, waves * kWave, 0, s>>>(p);
+    layer_down_combine_kernel<float><<<down_grid, waves * kWave, 0, s>>>(p);
   else
-    layer_down_combine_kernel<NT, bf16_t><<<p.H / 16, waves * kWave, 0, s>>>(p);
+    layer_down_combine_kernel<bf16_t><<<down_grid, waves * kWave, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -367,7 +528,7 @@ bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, i
   if (dt != DMOE_BF16 || n_blocks != 1) return false;
   if (T < 1 || T > 4 * kTok || E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
   if (k + (I_s > 0 ? 1 : 0) > kMaxSegments) return false;
-  if (H % 128 || I % 128 || I_s % 128) return false;
+  if (H % 128 || I % 128 || I_s % 128 || E % 4) return false;
   return prologue_words(T, E) * sizeof(float) <= 48 * 1024;
 }
 
