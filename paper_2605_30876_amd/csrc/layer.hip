@@ -8,17 +8,16 @@
 // invalidation).  So the phases are merged where the merge needs no
 // synchronisation at all:
 //
-//  1. router + shared gate/up.  Router tiles of 16 tokens x 16 experts over
-//     the whole hidden dimension write the logits; the workgroups of the
-//     first expert tile also write x in the chunk-major layout.  The shared
-//     expert needs only x, so its gate/up tiles run in the same launch on
-//     otherwise idle CUs (reading the row-major x).
-//  2. routing + routed gate/up.  Every workgroup recomputes the block's
+//  1. router.  Router tiles of 16 tokens x 16 experts over the whole hidden
+//     dimension write the logits; the workgroups of the first expert tile
+//     also write x in the chunk-major layout.
+//  2. routing + gate/up.  The shared expert needs only x: its workgroups
+//     stream its gate/up tiles at once.  Every other workgroup recomputes the block's
 //     routing from the logits -- softmax of each token row, the block mean
 //     in token order, the top-(k+1) by radix selection, the weights -- with
 //     the device routines of the routing kernels, so every workgroup reaches
 //     the same bits (workgroup (0, 0) writes the routing outputs and the
-//     closed-form schedule).  Workgroup (it, j) then streams packed tile it of
+//     closed-form schedule).  Workgroup (x, j) then streams two packed tiles of
 //     the j-th selected expert's gate/up weights over all tokens of the block
 //     and stores the SwiGLU activations already multiplied by the token's
 //     combine weight, w[t][j] * silu(g) * u, as bf16.
@@ -33,6 +32,8 @@
 // Activations between the launches are chunk-major over the concatenated
 // reduction index: hk[(kk/8)*T + t][kk%8], kk = j*I + i for routed slot j and
 // unit i, kk = k*I + i for the shared expert.
+#include <algorithm>
+
 #include "ffn_dev.h"
 #include "route_dev.h"
 
@@ -44,6 +45,11 @@ using fdev::kFrag;
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kTok = 16;  // tokens per MFMA tile
+// K-steps of token fragments loaded per chunk: with one or two token tiles
+// all 16 steps go out with the weight burst (one memory round trip per
+// product); four tiles would not fit in registers, so they take chunks of 4.
+template <int NT>
+constexpr int kTokChunk = NT <= 2 ? 16 : 4;
 
 struct LayerParams {
   const bf16_t* x;     // [T][H] row-major
@@ -129,42 +135,9 @@ __device__ __forceinline__ void store_h(bf16_t* hk, int T, int chunk, int col, i
   *reinterpret_cast<uint32_t*>(hk + (static_cast<size_t>(chunk) * T + col) * 8 + 2 * q) = h0 | (h1 << 16);
 }
 
-// Gate/up of packed tile `it` (8 intermediate units) of the shared expert
-// over all T tokens, read from the row-major x.
-template <int NT>
-__device__ void shared_gateup_tile(const LayerParams& p, int it, f32x4 (*red)[1][NT][kWave]) {
-  const int T = p.T, H = p.H;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
-  const int ksteps = H >> 5, steps = ksteps >> 2;
-  const bf16_t* pa = p.ws13 + (static_cast<size_t>(it) * ksteps + wave * steps) * kFrag + lane * 8;
-  const bf16_t* pb[NT];
-#pragma unroll
-  for (int ct = 0; ct < NT; ++ct) {
-    const int tok = min(ct * kTok + c, T - 1);
-    pb[ct] = p.x + static_cast<size_t>(tok) * H + wave * (H / 4) + q * 8;
-  }
-  f32x4 acc[1][NT];
-  fdev::zero(acc);
-  fdev::WaveOps<NT, 16, 4, 1> w;
-  fdev::wave_dot(w, pa, 0, pb, 32, steps, acc, false);
-  fdev::reduce_waves(acc, red, wave, lane);
-  if (wave != 0) return;
-  const int chunk = (p.k * p.I) / 8 + it;
-#pragma unroll
-  for (int ct = 0; ct < NT; ++ct) {
-    const int col = ct * kTok + c;
-    if (col < T) store_h(p.hk, T, chunk, col, q, acc[0][ct], 1.f);
-  }
-}
-
-template <int NT>
-__global__ __launch_bounds__(kThreads) void layer_router_shared_kernel(LayerParams p, int n_router) {
-  __shared__ f32x4 rred[kWaves - 1][kWave];
-  __shared__ f32x4 sred[kWaves - 1][1][NT][kWave];
-  if (static_cast<int>(blockIdx.x) < n_router)
-    router_tile(p, blockIdx.x, rred);
-  else
-    shared_gateup_tile<NT>(p, blockIdx.x - n_router, sred);
+__global__ __launch_bounds__(kThreads) void layer_router_kernel(LayerParams p) {
+  __shared__ f32x4 red[kWaves - 1][kWave];
+  router_tile(p, blockIdx.x, red);
 }
 
 // ---- launch 2: the block's routing, then the routed gate/up ------------------
@@ -335,6 +308,45 @@ __device__ void rows_softmax(const LayerParams& p, float* P, int Es, bool first)
   }
 }
 
+// Workgroups (x, j): slot j < k streams packed tiles kRT*x .. kRT*x+kRT-1 of
+// the j-th selected expert; slot j == k (when there is a shared expert)
+// streams the shared expert's tiles and needs no routing.
+// 16-row weight tiles per wave: two (half the workgroups, so each CU reads
+// the token operand once per two tiles) unless four token tiles would not
+// fit in registers.
+template <int NT>
+constexpr int kRTof = NT <= 2 ? 2 : 1;
+
+// The shared expert's gate/up tiles over all T tokens (chunk-major x).
+template <int NT>
+__device__ void shared_gateup_tiles(const LayerParams& p, int it0, f32x4 (*red)[kRTof<NT>][NT][kWave]) {
+  constexpr int kRT = kRTof<NT>;
+  const int T = p.T, H = p.H;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
+  const int ksteps = H >> 5, steps = ksteps >> 2;
+  const bf16_t* pa = p.ws13 + (static_cast<size_t>(it0) * ksteps + wave * steps) * kFrag + lane * 8;
+  const int chunk0 = wave * steps * 4 + q;
+  const bf16_t* pb[NT];
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    const int tok = min(ct * kTok + c, T - 1);
+    pb[ct] = p.xk + (static_cast<size_t>(chunk0) * T + tok) * 8;
+  }
+  f32x4 acc[kRT][NT];
+  fdev::zero(acc);
+  fdev::WaveOps<NT, 16, 4, kRT> w;
+  fdev::wave_dot(w, pa, static_cast<size_t>(ksteps) * kFrag, pb, 32 * T, steps, acc, false);
+  fdev::reduce_waves(acc, red, wave, lane);
+  if (wave != 0) return;
+#pragma unroll
+  for (int r = 0; r < kRT; ++r)
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const int col = ct * kTok + c;
+      if (col < T) store_h(p.hk, T, (p.k * p.I) / 8 + it0 + r, col, q, acc[r][ct], 1.f);
+    }
+}
+
 template <int NQ, int NT>
 __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerParams p) {
   extern __shared__ float lds[];
@@ -344,15 +356,21 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   __shared__ int bufi[kRoundsMax];
   __shared__ int slds[kWave];
   __shared__ float wslot[NT * kTok];
-  __shared__ f32x4 red[kWaves - 1][1][NT][kWave];
+  __shared__ f32x4 red[kWaves - 1][kRTof<NT>][NT][kWave];
   __shared__ uint32_t gmax[17];
   __shared__ __align__(16) uint32_t ckey[kCandMax + 4];
   __shared__ __align__(16) int cid[kCandMax + 4];
   __shared__ int wcount[kWaves];
+  constexpr int kRT = kRTof<NT>;
   const int T = p.T, E = p.E, k = p.k;
   const int Es = dev::pad4(E);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int it = blockIdx.x, j = blockIdx.y;
+  const int it = blockIdx.x * kRT, j = blockIdx.y;
+  if (j == k) {  // the shared expert: no routing needed
+    if (it * 8 < p.I_s) shared_gateup_tiles<NT>(p, it, red);
+    return;
+  }
+  if (it * 8 >= p.I) return;  // past this expert's tiles (I < I_s)
   const bool first = it == 0 && j == 0;  // writes the routing outputs
   float* P = lds;
   float* S = lds + static_cast<size_t>(T) * Es;
@@ -394,10 +412,10 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
     const int tok = min(ct * kTok + c, T - 1);
     pb[ct] = p.xk + (static_cast<size_t>(chunk0) * T + tok) * 8;
   }
-  f32x4 acc[1][NT];
+  f32x4 acc[kRT][NT];
   fdev::zero(acc);
-  fdev::WaveOps<NT, 16, 4, 1> w;
-  fdev::wave_dot(w, pa, 0, pb, 32 * T, steps, acc, false);
+  fdev::WaveOps<NT, 16, 4, kRT> w;
+  fdev::wave_dot(w, pa, static_cast<size_t>(ksteps) * kFrag, pb, 32 * T, steps, acc, false);
 
   // 6. the routing outputs (workgroup (0, 0), while the other workgroups
   //    stream): the selection, gap, every token's combine weights (its
@@ -431,12 +449,13 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   fdev::reduce_waves(acc, red, wave, lane);
   if (wave != 0) return;
   // 8. SwiGLU scaled by the weights
-  const int chunk = (j * p.I) / 8 + it;
 #pragma unroll
-  for (int ct = 0; ct < NT; ++ct) {
-    const int col = ct * kTok + c;
-    if (col < T) store_h(p.hk, T, chunk, col, q, acc[0][ct], wslot[col]);
-  }
+  for (int r = 0; r < kRT; ++r)
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const int col = ct * kTok + c;
+      if (col < T) store_h(p.hk, T, (j * p.I) / 8 + it + r, col, q, acc[r][ct], wslot[col]);
+    }
 }
 
 // ---- launch 3: down projection of every expert and the combine ---------------
@@ -480,7 +499,7 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
   const bf16_t* pa = W + static_cast<size_t>(jt) * ksteps * kFrag + lane * 8;
   f32x4 acc[1][NT];
   fdev::zero(acc);
-  fdev::WaveOps<NT, 16, 4, 1> w;
+  fdev::WaveOps<NT, 16, kTokChunk<NT>, 1> w;
   fdev::wave_dot(w, pa, 0, pb, 32 * T, ksteps, acc, false);
   if (wave > 0) {
 #pragma unroll
@@ -502,15 +521,15 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
 template <int NT>
 hipError_t launch_nt(const LayerParams& p, dmoe_dtype y_dt, hipStream_t s) {
   const int n_router = ((p.T + kTok - 1) / kTok) * ((p.E + kTok - 1) / kTok);
-  const int n_shared = p.ws13 ? p.I_s / 8 : 0;
-  layer_router_shared_kernel<NT><<<n_router + n_shared, kThreads, 0, s>>>(p, n_router);
+  layer_router_kernel<<<n_router, kThreads, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t lds = prologue_words(p.T, p.E) * sizeof(float);
+  const dim3 gu_grid(std::max(p.I, p.ws13 ? p.I_s : 0) / (8 * kRTof<NT>), p.k + (p.ws13 ? 1 : 0));
   if (p.E <= 256)
-    layer_route_gateup_kernel<1, NT><<<dim3(p.I / 8, p.k), kThreads, lds, s>>>(p);
+    layer_route_gateup_kernel<1, NT><<<gu_grid, kThreads, lds, s>>>(p);
   else
-    layer_route_gateup_kernel<2, NT><<<dim3(p.I / 8, p.k), kThreads, lds, s>>>(p);
+    layer_route_gateup_kernel<2, NT><<<gu_grid, kThreads, lds, s>>>(p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int waves = p.k + (p.ws13 ? 1 : 0);
