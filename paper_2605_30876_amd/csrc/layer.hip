@@ -81,12 +81,13 @@ constexpr int kRouterBurst = 16;  // K-steps of 32 loaded at once per wave
 // waves each reduce a quarter, summed in wave order).  A = x rows (tokens),
 // B = router rows (experts): lane (q, c) ends with tokens 4q..4q+3 of expert
 // column c.
+template <int NW>
 __device__ void router_tile(const LayerParams& p, int tile, f32x4 (*red)[kWave]) {
   const int T = p.T, H = p.H, E = p.E;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
   const int ntt = (T + kTok - 1) / kTok;
   const int tt = tile % ntt, et = tile / ntt;
-  const int kq = H / 4, k0 = wave * kq, steps = kq / 32;
+  const int kq = H / NW, k0 = wave * kq, steps = kq / 32;
   const int t = min(tt * kTok + c, T - 1), e = min(et * kTok + c, E - 1);
   const bf16_t* pa = p.x + static_cast<size_t>(t) * H + k0 + q * 8;
   const bf16_t* pb = p.wr + static_cast<size_t>(e) * H + k0 + q * 8;
@@ -117,7 +118,7 @@ __device__ void router_tile(const LayerParams& p, int tile, f32x4 (*red)[kWave])
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
-  for (int w = 0; w < kWaves - 1; ++w) acc += red[w][lane];
+  for (int w = 0; w < NW - 1; ++w) acc += red[w][lane];
   const int ec = et * kTok + c;
   if (ec >= E) return;
 #pragma unroll
@@ -135,9 +136,11 @@ __device__ __forceinline__ void store_h(bf16_t* hk, int T, int chunk, int col, i
   *reinterpret_cast<uint32_t*>(hk + (static_cast<size_t>(chunk) * T + col) * 8 + 2 * q) = h0 | (h1 << 16);
 }
 
-__global__ __launch_bounds__(kThreads) void layer_router_kernel(LayerParams p) {
-  __shared__ f32x4 red[kWaves - 1][kWave];
-  router_tile(p, blockIdx.x, red);
+// Eight waves split the hidden dimension (eight K-steps each for H = 2048).
+constexpr int kRouterWaves = 8;
+__global__ __launch_bounds__(kRouterWaves * kWave) void layer_router_kernel(LayerParams p) {
+  __shared__ f32x4 red[kRouterWaves - 1][kWave];
+  router_tile<kRouterWaves>(p, blockIdx.x, red);
 }
 
 // ---- launch 2: the block's routing, then the routed gate/up ------------------
@@ -521,7 +524,7 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
 template <int NT>
 hipError_t launch_nt(const LayerParams& p, dmoe_dtype y_dt, hipStream_t s) {
   const int n_router = ((p.T + kTok - 1) / kTok) * ((p.E + kTok - 1) / kTok);
-  layer_router_kernel<<<n_router, kThreads, 0, s>>>(p);
+  layer_router_kernel<<<n_router, kRouterWaves * kWave, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t lds = prologue_words(p.T, p.E) * sizeof(float);
@@ -547,7 +550,7 @@ bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, i
   if (dt != DMOE_BF16 || n_blocks != 1) return false;
   if (T < 1 || T > 4 * kTok || E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
   if (k + (I_s > 0 ? 1 : 0) > kMaxSegments) return false;
-  if (H % 128 || I % 128 || I_s % 128 || E % 4) return false;
+  if (H % 256 || I % 128 || I_s % 128 || E % 4) return false;
   return prologue_words(T, E) * sizeof(float) <= 48 * 1024;
 }
 
