@@ -103,9 +103,10 @@ typedef enum dmoe_dtype {
  *   row_token[n_rows]   token of each row (n_rows = n_groups*group_size*k)
  *   row_slot [n_rows]   slot j in 0..k-1 of the token's expert list
  *   n_work   [1]        number of work items
- *   work     [4*max_work] work items {expert id, first row, row count, 0}:
+ *   work     [4*max_work] work items {expert id, first row, row count, piece}:
  *                       each unique expert's rows cut, in order, into pieces
- *                       of at most DMOE_WORK_ROWS rows; items are ordered by
+ *                       of at most DMOE_WORK_ROWS rows (piece = 0, 1, ... its
+ *                       index within the expert); items are ordered by
  *                       expert id, then row.  max_work: dmoe_schedule_max_work.
  * Within one expert, rows are ordered by token.
  *   scratch  optional (NULL: not used); with group_size 1 and at least

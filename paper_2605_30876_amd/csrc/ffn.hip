@@ -12,9 +12,9 @@
 // exit at once are dispatched last; the others put them last (measured
 // faster for block-routed decode steps).  A decode workgroup owns one or two
 // 16-row weight tiles of one item, streams them from HBM and applies them to
-// the item's rows (tokens); a tile workgroup owns 128 rows and up to 128
-// tokens.  Each selected expert's weights are read once per forward per piece
-// of its rows.
+// the item's rows (tokens); a tile workgroup owns 64 or 128 weight rows and
+// up to 128 tokens.  Each selected expert's weights are read once per forward
+// per piece of its rows.
 //
 // bf16 path (matrix cores, v_mfma_f32_16x16x32_bf16, fp32 accumulation):
 //  * A operand = weight rows, B operand = token rows, C = [weight row][token].
@@ -58,6 +58,7 @@ struct Group {
   int expert;      // routed expert id, or -1 for the shared expert
   const int* tok;  // token of each row (routed), or nullptr: row c is token t0 + c
   int t0;
+  int piece;       // index of the item among its expert's items (0, 1, ...)
 };
 
 // Grid row y: the schedule's max_work items, then the shared expert's pieces
@@ -78,9 +79,11 @@ __device__ __forceinline__ bool decode_item(int y, int shared_items, int max_wor
     g.n = (w < nw && static_cast<unsigned>(it.x) < static_cast<unsigned>(E)) ? it.z : 0;
     g.tok = row_token + it.y;
     g.t0 = 0;
+    g.piece = it.w;
   } else {
     const int c = kSharedFirst ? y : y - max_work;
     g.expert = -1;
+    g.piece = c;
     g.t0 = c * DMOE_WORK_ROWS;
     g.r0 = Tk + g.t0;
     g.n = min(DMOE_WORK_ROWS, T - g.t0);
@@ -142,7 +145,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
                                  p.Tk, p.E, g))
     return;
-  if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
+  if (p.split_rows > 0 && (g.n > p.split_rows || g.piece > 0)) return;  // a tile-kernel item
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int it = blockIdx.x * RT;  // first of the RT packed tiles (Iw / 8 is a multiple of 16)
   if (it * 8 >= Iw) return;
@@ -204,7 +207,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
                                  p.Tk, p.E, g))
     return;
-  if (p.split_rows > 0 && g.n > p.split_rows) return;  // a tile-kernel item
+  if (p.split_rows > 0 && (g.n > p.split_rows || g.piece > 0)) return;  // a tile-kernel item
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
   const int jt = blockIdx.x * RT;  // first of the RT packed tiles (H / 16 is a multiple of 8)
@@ -251,6 +254,30 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   }
 }
 
+// Workgroups are dispatched to the 8 XCDs round-robin by linear id, and each
+// XCD has its own L2.  The 1-D grid of gx * items8 workgroups (gx row blocks
+// per item, items8: the grid rows rounded up to a multiple of 8) is mapped
+// onto the schedule's live items (the first n_work, then the shared
+// expert's) so that each item's row blocks run on S XCDs: its token rows
+// enter S L2 caches.  Schedules of many live items (>= 256: thousands of
+// tokens, whose token rows per XCD copy cost about as much traffic as the
+// weights) take S = 1; the others S = 8 (every XCD shares every item's
+// work, the most even load; measured faster for 16 blocks of 32 tokens and
+// for the Zipf-biased large layer).  XCD x of group x / S runs row blocks
+// x % S, x % S + S, ... of the group's items, one item after the other.
+__device__ __forceinline__ bool map_item(const FfnParams& p, int gx, int& item, int& rb) {
+  const int nw = min(*p.n_work, p.max_work);
+  const int live = nw + p.shared_items;
+  const int S = min(live >= 256 ? 1 : 8, gx & -gx);  // a power of two dividing gx
+  const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int per = gx / S;  // row blocks of an item on each of its XCDs
+  const int j = (slot / per) * (8 / S) + x / S;
+  rb = x % S + S * (slot % per);
+  if (j >= live) return false;
+  item = j < nw ? j : p.max_work + (j - nw);
+  return true;
+}
+
 // ---- tile kernels: many tokens per work item --------------------------------
 //
 // A workgroup covers 4 * kRowTiles (one or two) 16-row weight tiles (wave w: packed tiles
@@ -268,20 +295,21 @@ constexpr int kStageSteps = 2;    // K-steps per LDS stage (two: 32 KB of LDS, t
 static_assert(kTileTok * 16 == DMOE_WORK_ROWS, "a tile workgroup covers one work item's rows");
 
 template <bool kGateUp, int kRowTiles>
-__global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p) {
+__global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p, int gx) {
   constexpr int kTileRows = 4 * kRowTiles;  // weight tiles per workgroup
+  int item, bx;
+  if (!map_item(p, gx, item, bx)) return;
   Group g;
-  if (!decode_item(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, p.E, g))
-    return;
-  if (g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
+  if (!decode_item(item, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, p.E, g)) return;
+  if (g.piece == 0 && g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
   const int H = p.H;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int Kd = kGateUp ? H : Iw;                    // reduction length
   const int tiles = kGateUp ? Iw / 8 : H / 16;        // packed 16-row tiles of the matrix
-  if (static_cast<int>(blockIdx.x) * kTileRows >= tiles) return;  // uniform: past the matrix
+  if (bx * kTileRows >= tiles) return;  // uniform: past the matrix
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   // tiles % kTileRows == 0 (H, I, I_s multiples of 128)
-  const int tile0 = (blockIdx.x * 4 + wave) * kRowTiles;
+  const int tile0 = (bx * 4 + wave) * kRowTiles;
   const int ksteps = Kd >> 5;                         // multiple of kStageSteps
   const bf16_t* W;
   if (kGateUp)
@@ -626,20 +654,21 @@ hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile kernels.  Two weight tiles per wave halve the LDS reads per weight
-// byte; one tile per wave doubles the workgroups.  A gate/up grid of fewer than
-// two rounds of the chip (three resident workgroups on each of 256 CUs) ends
-// in a long partial round, which the finer split shortens; both halves of the
-// FFN take the gate/up choice.
+// Tile kernels, one item per workgroup: two weight tiles per wave
+// halve the LDS reads per weight byte; one tile per wave doubles the
+// workgroups.  A gate/up grid of fewer than two rounds of the chip (three
+// resident workgroups on each of 256 CUs) ends in a long partial round, which
+// the finer split shortens; both halves of the FFN take the gate/up choice.
 constexpr long kTileRound = 3L * 256;
 template <bool kGateUp>
 hipError_t launch_tile_bf16(const FfnParams& p, int ldh, int items, hipStream_t s) {
   const bool fine = static_cast<long>(ldh / 64) * items < 2 * kTileRound;
-  const int rows = kGateUp ? ldh / 8 : p.H / 16;  // packed 16-row tiles
+  const int tiles = kGateUp ? ldh / 8 : p.H / 16;  // packed 16-row tiles
+  const int items8 = (items + 7) / 8 * 8;
   if (fine)
-    ffn_tile_bf16_kernel<kGateUp, 1><<<dim3(rows / 4, items), kThreads, 0, s>>>(p);
+    ffn_tile_bf16_kernel<kGateUp, 1><<<dim3(tiles / 4 * items8), kThreads, 0, s>>>(p, tiles / 4);
   else
-    ffn_tile_bf16_kernel<kGateUp, 2><<<dim3(rows / 8, items), kThreads, 0, s>>>(p);
+    ffn_tile_bf16_kernel<kGateUp, 2><<<dim3(tiles / 8 * items8), kThreads, 0, s>>>(p, tiles / 8);
   return hipGetLastError();
 }
 

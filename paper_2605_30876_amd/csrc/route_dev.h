@@ -555,7 +555,7 @@ __device__ inline void schedule_totals(int c, int gs, int E, const dmoe_schedule
     }
     int4* work = reinterpret_cast<int4*>(sched.work) + c_excl;
     for (int q = 0; q < chunks; ++q)
-      work[q] = make_int4(tid, r_excl + q * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, rows - q * DMOE_WORK_ROWS), 0);
+      work[q] = make_int4(tid, r_excl + q * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, rows - q * DMOE_WORK_ROWS), q);
   }
   if (tid == kSchedThreads - 1) {
     sched.offsets[u_excl + pres] = r_excl + rows;
@@ -681,7 +681,7 @@ __device__ inline void schedule_one_group(const int32_t* experts, int gs, int k,
       sched.offsets[r] = r * gs;
       int4* work = reinterpret_cast<int4*>(sched.work) + r * chunks;
       for (int c = 0; c < chunks; ++c)
-        work[c] = make_int4(e, r * gs + c * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, gs - c * DMOE_WORK_ROWS), 0);
+        work[c] = make_int4(e, r * gs + c * DMOE_WORK_ROWS, min(DMOE_WORK_ROWS, gs - c * DMOE_WORK_ROWS), c);
     }
     if (tid == 0) {
       sched.offsets[k] = k * gs;

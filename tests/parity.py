@@ -53,14 +53,15 @@ def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: lis
 
 
 def expected_work(uniq, rows: dict, work_rows: int = 128):
-    """Work items {expert, first row, rows} from the oracle's per-expert rows:
-    each unique expert's rows, in ascending id order, cut into pieces of at
-    most work_rows (the schedule's documented layout)."""
+    """Work items {expert, first row, rows, piece} from the oracle's per-expert
+    rows: each unique expert's rows, in ascending id order, cut into pieces
+    of at most work_rows, numbered 0, 1, ... within the expert (the
+    schedule's documented layout)."""
     items, r0 = [], 0
     for e in uniq.tolist():
         n = len(rows[e])
         for c in range(0, n, work_rows):
-            items.append([e, r0 + c, min(work_rows, n - c), 0])
+            items.append([e, r0 + c, min(work_rows, n - c), c // work_rows])
         r0 += n
     return items
 

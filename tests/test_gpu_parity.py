@@ -41,14 +41,15 @@ def test_small_layer_parity(gpu_lib, name, routing, seed):
 
 
 # Shapes whose expert FFN takes the tile kernels (work items of >= 32 rows on
-# average, >= 512 tile workgroups) while the oracle still checks every token:
-# 8 blocks of 32 tokens over 32 experts, and 4 blocks of 64 with top-8 (grids
-# of under 1536 two-tile workgroups: one weight tile per wave), and 16 blocks
-# of 32 over 128 experts with I = 1024 (2112 workgroups under block routing:
-# two weight tiles per wave).
+# average, >= 512 grid rows x 32-row units) while the oracle still checks every
+# token: 8 blocks of 32 tokens over 32 experts; 4 blocks of 64 with top-8;
+# 16 blocks of 32 over 128 experts with I = 1024; and 5 blocks of 64 over 8
+# experts, where an expert collects up to 320 rows (three items: a pair and a
+# lone third piece) and the shared expert's 320 tokens end in a lone piece.
 TILE = {"tile_b8x32": dict(H=512, E=32, I=512, I_s=512, k=4, NB=8, bs=32),
         "tile_b4x64": dict(H=256, E=16, I=1024, I_s=512, k=8, NB=4, bs=64),
-        "tile_b16x32_wide": dict(H=256, E=128, I=1024, I_s=256, k=8, NB=16, bs=32)}
+        "tile_b16x32_wide": dict(H=256, E=128, I=1024, I_s=256, k=8, NB=16, bs=32),
+        "tile_b5x64_e8": dict(H=256, E=8, I=1024, I_s=512, k=4, NB=5, bs=64)}
 
 
 @pytest.mark.parametrize("routing", ["block", "token"])
