@@ -316,8 +316,9 @@ dmoe_status dmoe_pack_expert_weights(const void* w_gate, const void* w_up, const
 size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
 
 /*
- * Expert execution: for every unique expert e = sched.unique[u] and each of
- * its rows (t, j):
+ * Expert execution (Sec. 3: the MoE layer is routing plus expert execution;
+ * each token's selected experts and the shared expert are SwiGLU FFNs): for
+ * every unique expert e = sched.unique[u] and each of its rows (t, j):
  *   h = silu(W_gate[e] x_t) * (W_up[e] x_t)          (SwiGLU, silu(a) = a/(1+e^-a))
  *   slot_out[t][j][:] = W_down[e] h
  * and, when the shared expert is present (ws13 != NULL), for every token t:
@@ -378,8 +379,8 @@ dmoe_status dmoe_expert_ffn_noalloc(const void* x_chunked, const void* x, const 
                                     float* shared_out, void* stream);
 
 /*
- * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn): for every
- * token t,
+ * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn; expert
+ * execution, Sec. 3, for the always-on shared expert): for every token t,
  *   shared_out[t][:] = Ws_down (silu(Ws_gate x_t) * (Ws_up x_t))
  * It needs no routing, so a caller can run it on a second stream while the
  * routing of the same forward runs, then call dmoe_expert_ffn with the
@@ -400,9 +401,14 @@ dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, cons
                                    void* stream);
 
 /*
- * Weighted combine:
+ * Weighted combine (Sec. 3, the layer output as the weighted sum of the
+ * selected experts' outputs plus the shared expert's):
  *   y[t][h] = sum_{j=0..k-1} combine_w[t][j] * slot_out[t][j][h]  (+ shared_out[t][h])
- * summed in slot order in float32, stored as dt.
+ * summed in slot order in float32, stored as dt.  The weights are those the
+ * routing entry points write: the token's own router probabilities on its
+ * selected experts renormalised to sum to 1, with no further scaling (the
+ * paper leaves the weighting open; this is the reading taken), and the
+ * shared expert enters with weight 1.
  * slot_out [T][k][H] float32; combine_w [T][k] float32; shared_out [T][H]
  * float32 or NULL; y [T][H] of type dt.
  * Limits: T >= 1; 1 <= k <= 64; H >= 1; H % 4 == 0.
@@ -418,12 +424,14 @@ dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const fl
  * token: the baseline; topp: Alg. 1 with the Top-P coreset p, min_coreset).
  *
  * A block-routed forward of a single bf16 block (n_blocks == 1, block_size
- * <= 64, E <= 512, k + (I_s > 0) <= 12, T*E small enough for on-chip
- * probabilities) runs as three kernels: the router with the shared expert's
- * gate/up beside it; the routing, recomputed by every workgroup of the routed
- * gate/up (the combine weight applied to the SwiGLU activations); and one
- * down projection over all selected experts and the shared expert that
- * writes y (no slot outputs, no combine kernel).  Its routing outputs equal
+ * <= 64, E <= 512 and E % 4 == 0, k + (I_s > 0) <= 12, H % 256 == 0, T*E
+ * small enough for on-chip probabilities; dmoe_moe_forward_fused says
+ * whether a call qualifies) runs as three kernels: the router (logits, and x
+ * in the chunk-major layout); the routing, recomputed by every workgroup of
+ * the routed gate/up (the combine weight applied to the SwiGLU
+ * activations), with the shared expert's gate/up as further workgroups of
+ * the same launch; and one down projection over all selected experts and
+ * the shared expert that writes y (no slot outputs, no combine kernel).  Its routing outputs equal
  * dmoe_route_block's up to the float32 rounding of the logits (one
  * reduction over the whole hidden dimension instead of slices), and y
  * differs from the chained path's by the bf16 rounding of the weighted
@@ -472,6 +480,14 @@ typedef struct dmoe_layer_buffers {
 /* Bytes of dmoe_layer_buffers.workspace for these sizes (0 on invalid sizes). */
 size_t dmoe_moe_forward_workspace_size(int n_blocks, int block_size, int H, int E, int I, int I_s, int k,
                                        dmoe_dtype dt);
+
+/*
+ * 1 if dmoe_moe_forward with these arguments runs the three-kernel path of a
+ * single block (see above), 0 if it chains the entry points (also for sizes
+ * dmoe_moe_forward would reject).  Host only; enqueues nothing.
+ */
+int dmoe_moe_forward_fused(dmoe_dtype dt, int n_blocks, int block_size, int H, int E, int I, int I_s, int k,
+                           dmoe_routing routing);
 
 dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* bias, const void* w13,
                              const void* w2, const void* ws13, const void* ws2, dmoe_dtype dt, int n_blocks,

@@ -25,14 +25,16 @@ SOURCES = ["dmoe_api.cpp", "router.hip", "routing.hip", "topp.hip", "schedule.hi
 ARCH = os.environ.get("DMOE_OFFLOAD_ARCH", "gfx950")
 
 
-def ffn_source_hash() -> str:
-    """Hash of the code of the expert-FFN kernels (line comments and blank
+def kernel_source_hash() -> str:
+    """Hash of the code of every kernel source (line comments and blank
     lines left out): hardware-counter figures taken on other code are stale."""
     import hashlib
     import re
 
     h = hashlib.sha256()
-    for f in ("ffn.hip", "ffn_dev.h", "pack.hip"):
+    for f in sorted(os.listdir(CSRC)):
+        if not f.endswith((".hip", ".h")):
+            continue
         with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
             for line in fh:
                 code = re.sub(r"//.*", "", line).rstrip()

@@ -556,6 +556,14 @@ size_t dmoe_moe_forward_workspace_size(int n_blocks, int block_size, int H, int 
   return layer_workspace_bytes(n_blocks, block_size, H, E, I, I_s, k, dt);
 }
 
+int dmoe_moe_forward_fused(dmoe_dtype dt, int n_blocks, int block_size, int H, int E, int I, int I_s, int k,
+                           dmoe_routing routing) {
+  if (routing != DMOE_ROUTE_BLOCK || !valid_dtype(dt) || n_blocks < 1 || block_size < 1 || block_size > 4096 ||
+      H < 1 || H % 4 || I < 1 || I_s < 0 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK)
+    return 0;
+  return dmoe::layer_fused_fits(dt, n_blocks, n_blocks * block_size, H, E, I, I_s, k) ? 1 : 0;
+}
+
 dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* bias, const void* w13,
                              const void* w2, const void* ws13, const void* ws2, dmoe_dtype dt, int n_blocks,
                              int block_size, int H, int E, int I, int I_s, int k, dmoe_routing routing, float top_p,

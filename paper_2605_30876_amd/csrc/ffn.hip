@@ -263,16 +263,29 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 // tokens, whose token rows per XCD copy cost about as much traffic as the
 // weights) take S = 1; the others S = 8 (every XCD shares every item's
 // work, the most even load; measured faster for 16 blocks of 32 tokens and
-// for the Zipf-biased large layer).  XCD x of group x / S runs row blocks
-// x % S, x % S + S, ... of the group's items, one item after the other.
+// for the Zipf-biased large layer).  With S = 1, XCD x runs a contiguous
+// run of ceil(live / 8) items, one item (all its row blocks) after the
+// other: the items of one expert are adjacent in the schedule, so its pieces
+// run back to back on one XCD and share that L2's copy of its weights.  With
+// S > 1, XCD x of group x / S runs row blocks x % S, x % S + S, ... of the
+// group's items (an expert's pieces again meet on the XCDs of each row
+// block).
 __device__ __forceinline__ bool map_item(const FfnParams& p, int gx, int& item, int& rb) {
   const int nw = min(*p.n_work, p.max_work);
   const int live = nw + p.shared_items;
   const int S = min(live >= 256 ? 1 : 8, gx & -gx);  // a power of two dividing gx
   const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int per = gx / S;  // row blocks of an item on each of its XCDs
-  const int j = (slot / per) * (8 / S) + x / S;
-  rb = x % S + S * (slot % per);
+  int j;
+  if (S == 1) {
+    const int q = (live + 7) >> 3, i = slot / gx;  // q items per XCD
+    rb = slot % gx;
+    if (i >= q) return false;
+    j = x * q + i;
+  } else {
+    const int per = gx / S;  // row blocks of an item on each of its XCDs
+    j = (slot / per) * (8 / S) + x / S;
+    rb = x % S + S * (slot % per);
+  }
   if (j >= live) return false;
   item = j < nw ? j : p.max_work + (j - nw);
   return true;

@@ -102,6 +102,12 @@ class MoELayer:
         lbytes = lib.dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt)
         self.layer_ws = torch.empty((max(lbytes, 16),), dtype=torch.uint8, device=device)
 
+    def fused(self, routing: str) -> bool:
+        """Whether :meth:`forward` (one dmoe_moe_forward call) runs the
+        three-kernel one-block path for this routing."""
+        dt = lib.DMOE_F32 if self.dtype == torch.float32 else lib.DMOE_BF16
+        return lib.dmoe_moe_forward_fused(dt, self.NB, self.bs, self.H, self.E, self.I, self.I_s, self.k, routing)
+
     def max_work(self, routing: str) -> int:
         """Work items the expert FFN's grid is sized for (dmoe_schedule_max_work)."""
         return self._max_work[routing]

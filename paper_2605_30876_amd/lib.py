@@ -33,7 +33,8 @@ EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggre
            "dmoe_schedule_scratch_ints", "dmoe_route_block",
            "dmoe_route_token", "dmoe_route_topp", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
            "dmoe_expert_ffn", "dmoe_expert_ffn_noalloc", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
-           "dmoe_moe_forward_workspace_size", "dmoe_moe_forward", "dmoe_last_error", "dmoe_version")
+           "dmoe_moe_forward_workspace_size", "dmoe_moe_forward_fused", "dmoe_moe_forward", "dmoe_last_error",
+           "dmoe_version")
 
 
 class DmoeError(RuntimeError):
@@ -90,6 +91,7 @@ _SIGS = {
     "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
     "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
     "dmoe_moe_forward_workspace_size": ([_I] * 7 + [_I], _S),
+    "dmoe_moe_forward_fused": ([_I] * 9, _I),
     "dmoe_moe_forward": ([_P] * 7 + [_I] * 8 + [_I, ctypes.c_float, _I, ctypes.POINTER(dmoe_layer_buffers), _P, _I, _P],
                          _I),
     "dmoe_last_error": ([], ctypes.c_char_p),
@@ -299,6 +301,11 @@ def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):
 
 def dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt) -> int:
     return int(load().dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt))
+
+
+def dmoe_moe_forward_fused(dt, n_blocks, block_size, H, E, I, I_s, k, routing: str) -> bool:
+    """Whether dmoe_moe_forward runs the three-kernel one-block path here."""
+    return bool(load().dmoe_moe_forward_fused(dt, n_blocks, block_size, H, E, I, I_s, k, ROUTING[routing]))
 
 
 def dmoe_moe_forward(x, w_router, bias, w13, w2, ws13, ws2, n_blocks, block_size, H, E, I, I_s, k, routing: str,

@@ -5,13 +5,15 @@
         (``rocprofv3 --kernel-trace --stats``), as markdown.
 
     python -m paper_2605_30876_amd.prof_summary traffic --config NAME \\
-            --fetch MODE=CSV ... --write MODE=CSV ... \\
+            --fetch MODE=CSV ... --write MODE=CSV ... --unique MODE=U ... \\
             --copy-fetch CSV --copy-write CSV --copy-bytes N [--json OUT] [--cmd C]
-        HBM traffic per expert-FFN launch (the gate/up + down kernels) from
-        ``rocprofv3 --pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE`` counter runs
-        (KiB per dispatch), each scaled by what the same counter reads for a
-        plain copy kernel of N bytes.  Writes markdown to stdout and, with
-        --json, the figures bench.py reports as ``roofline.traffic``.
+        HBM traffic per MoE-layer forward by kernel group (expert FFN,
+        combine, one-block layer kernels, routing) from ``rocprofv3 --pmc
+        FETCH_SIZE`` and ``--pmc WRITE_SIZE`` counter runs (KiB per
+        dispatch), each scaled by what the same counter reads for a plain copy
+        kernel of N bytes, against the algorithmic bytes for U unique experts.
+        Writes markdown to stdout and, with --json, merges the configuration's
+        figures into OUT (bench.py reports them as ``roofline.traffic``).
 
     python -m paper_2605_30876_amd.prof_summary mfma --csv CSV --kernel PATTERN ... [--avg-us US ...]
         bf16 MFMA work per dispatch (SQ_INSTS_VALU_MFMA_MOPS_BF16 of a
@@ -36,10 +38,6 @@ import re
 import sqlite3
 import statistics
 import sys
-
-FFN_KERNELS = ("ffn_gateup_bf16_kernel", "ffn_down_bf16_kernel", "ffn_tile_bf16_kernel", "ffn_gateup_f32_kernel",
-               "ffn_down_f32_kernel")
-
 
 def short(name: str) -> str:
     n = name.replace("(anonymous namespace)::", "").replace("void ", "")
@@ -78,6 +76,33 @@ def mean_per_dispatch(rows, pattern: str):
     return (statistics.mean(vals), len(vals)) if vals else (None, 0)
 
 
+# Kernel groups of one MoE layer forward (substrings of the full kernel names).
+GROUPS = (
+    ("ffn", ("::ffn_gateup_bf16_kernel", "::ffn_down_bf16_kernel", "::ffn_tile_bf16_kernel", "::ffn_gateup_f32_kernel",
+             "::ffn_down_f32_kernel")),
+    ("combine", ("::combine_kernel<",)),
+    ("layer", ("::layer_router_kernel", "::layer_route_gateup_kernel", "::layer_down_combine_kernel")),
+)
+
+
+def group_of(name: str):
+    if "dmoe::" not in name:
+        return None
+    for g, pats in GROUPS:
+        if any(p in name for p in pats):
+            return g
+    return "route" if "pack_" not in name else None
+
+
+def per_kernel(rows):
+    """{kernel name: (dispatches, mean value per dispatch)} of the library's kernels."""
+    by = {}
+    for _, n, v in rows:
+        if group_of(n):
+            by.setdefault(n, []).append(v)
+    return {n: (len(v), statistics.mean(v)) for n, v in by.items()}
+
+
 def copy_kib(rows):
     """Median KiB of the largest plain-copy dispatches (torch's elementwise copy kernel)."""
     vals = [v for _, n, v in rows if "copy" in n.lower() and "dmoe" not in n]
@@ -85,41 +110,81 @@ def copy_kib(rows):
     return statistics.median([v for v in vals if v > 0.5 * big])
 
 
+def algorithmic_bytes(config: str, U: float):
+    """(expert weights once: U routed experts + the shared expert, the whole
+    forward: those + router weights + x in + fp32 y out) in bytes."""
+    from dmoe_synth import get_config
+    from dmoe_synth.generate import element_bytes, expert_bytes, shared_bytes
+
+    cfg = get_config(config)
+    eb = element_bytes(cfg)
+    ffn = U * expert_bytes(cfg) + shared_bytes(cfg)
+    return ffn, ffn + cfg.E * cfg.H * eb + cfg.T * cfg.H * eb + cfg.T * cfg.H * 4
+
+
 def cmd_traffic(a):
-    from paper_2605_30876_amd.build import ffn_source_hash
+    from paper_2605_30876_amd.build import kernel_source_hash
 
     fetch = dict(x.split("=", 1) for x in a.fetch)
     write = dict(x.split("=", 1) for x in a.write)
+    unique = {m: float(u) for m, u in (x.split("=", 1) for x in a.unique)}
     copy_read = copy_kib(read_counters(a.copy_fetch, "FETCH_SIZE")) * 1024
     copy_write = copy_kib(read_counters(a.copy_write, "WRITE_SIZE")) * 1024
     f_scale = a.copy_bytes / copy_read
     w_scale = a.copy_bytes / copy_write
-    print(f"# Expert-FFN HBM traffic, {a.config}\n")
+    print(f"# HBM traffic per MoE-layer forward, {a.config}\n")
     if a.cmd:
         print(f"Commands (from the repository root on the GPU box):\n\n```\n{a.cmd}\n```\n")
-    print(f"Calibration: a plain copy of {a.copy_bytes} bytes reads {copy_read:.0f} B by FETCH_SIZE "
-          f"(scale {f_scale:.4f}) and writes {copy_write:.0f} B by WRITE_SIZE (scale {w_scale:.4f}).\n")
-    print("| routing | kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled read MB | scaled write MB |")
-    print("|---|---|---|---|---|---|---|")
-    per_launch = {}
+    print(f"FETCH_SIZE and WRITE_SIZE (KiB per dispatch, two runs) are scaled by what they read for a plain copy "
+          f"of {a.copy_bytes} bytes: reads x{f_scale:.4f}, writes x{w_scale:.4f}. A group's bytes per launch are "
+          "the sum over its kernels of the mean per dispatch. Algorithmic bytes: the selected experts' and the "
+          "shared expert's weights once (FFN); plus the router weights, x in and the fp32 y out (forward).\n")
+    print("| routing | group | kernel | dispatches | read MB | write MB |\n|---|---|---|---|---|---|")
+    figures = {}
     for mode in fetch:
-        fr, wr = read_counters(fetch[mode], "FETCH_SIZE"), read_counters(write[mode], "WRITE_SIZE")
-        total = 0.0
-        for k in FFN_KERNELS:
-            fk, nf = mean_per_dispatch(fr, k)
-            wk, nw = mean_per_dispatch(wr, k)
-            if fk is None:
-                continue
-            rb, wb = fk * 1024 * f_scale, (wk or 0) * 1024 * w_scale
-            total += rb + wb
-            print(f"| {mode} | `{k}` | {nf} | {fk:.0f} | {wk or 0:.0f} | {rb / 1e6:.2f} | {wb / 1e6:.2f} |")
-        per_launch[mode] = int(total)
-    print("\nPer expert-FFN launch (gate/up + down), read + write, scaled: " +
-          ", ".join(f"{m} {v / 1e6:.2f} MB" for m, v in per_launch.items()))
+        fk = per_kernel(read_counters(fetch[mode], "FETCH_SIZE"))
+        wk = per_kernel(read_counters(write[mode], "WRITE_SIZE"))
+        tot = {}
+        for n in sorted(set(fk) | set(wk), key=lambda n: (group_of(n), n)):
+            g = group_of(n)
+            rb = fk.get(n, (0, 0.0))[1] * 1024 * f_scale
+            wb = wk.get(n, (0, 0.0))[1] * 1024 * w_scale
+            tot[g] = tot.get(g, 0.0) + rb + wb
+            print(f"| {mode} | {g} | `{short(n)}` | {fk.get(n, (0, 0))[0]} | {rb / 1e6:.2f} | {wb / 1e6:.2f} |")
+        alg_ffn, alg_fwd = algorithmic_bytes(a.config, unique[mode])
+        fused = tot.get("layer", 0.0) > 0
+        fwd = tot["layer"] if fused else tot.get("route", 0.0) + tot.get("ffn", 0.0) + tot.get("combine", 0.0)
+        figures[mode] = {"unique_experts": unique[mode], "fused_layer": fused,
+                         "ffn_bytes_per_launch": int(tot.get("ffn", 0.0)),
+                         "combine_bytes_per_launch": int(tot.get("combine", 0.0)),
+                         "route_bytes_per_launch": int(tot.get("route", 0.0)),
+                         "layer_bytes_per_launch": int(tot.get("layer", 0.0)),
+                         "forward_bytes": int(fwd),
+                         "algorithmic_ffn_bytes": int(alg_ffn), "algorithmic_forward_bytes": int(alg_fwd)}
+    print("\n| routing | unique experts | FFN MB (x algorithmic) | combine MB | routing MB | forward MB "
+          "(x algorithmic) |\n|---|---|---|---|---|---|")
+    for mode, f in figures.items():
+        ffn = f"{f['ffn_bytes_per_launch'] / 1e6:.1f} ({f['ffn_bytes_per_launch'] / f['algorithmic_ffn_bytes']:.2f})"
+        if f["fused_layer"]:
+            ffn = "(one-block path: in the forward)"
+        print(f"| {mode} | {f['unique_experts']:.1f} | {ffn} | {f['combine_bytes_per_launch'] / 1e6:.1f} "
+              f"| {f['route_bytes_per_launch'] / 1e6:.1f} | {f['forward_bytes'] / 1e6:.1f} "
+              f"({f['forward_bytes'] / f['algorithmic_forward_bytes']:.2f}) |")
     if a.json:
+        h = kernel_source_hash()
+        data = {}
+        try:
+            with open(a.json) as fh:
+                data = json.load(fh)
+        except (OSError, ValueError):
+            pass
+        if data.get("source_hash") != h:
+            data = {"source_hash": h, "configs": {}, "commands": {}}
+        data["fetch_scale"], data["write_scale"] = f_scale, w_scale
+        data.setdefault("configs", {})[a.config] = figures
+        data.setdefault("commands", {})[a.config] = a.cmd
         with open(a.json, "w") as fh:
-            json.dump({"config": a.config, "source_hash": ffn_source_hash(), "hbm_bytes_per_launch": per_launch,
-                       "fetch_scale": f_scale, "write_scale": w_scale, "command": a.cmd}, fh, indent=1)
+            json.dump(data, fh, indent=1, sort_keys=True)
 
 
 def cmd_mfma(a):
@@ -206,6 +271,7 @@ def main(argv=None):
     r.add_argument("--copy-fetch", required=True)
     r.add_argument("--copy-write", required=True)
     r.add_argument("--copy-bytes", type=int, required=True)
+    r.add_argument("--unique", nargs="+", required=True, help="MODE=mean unique experts per forward (bench log)")
     r.add_argument("--json")
     r.add_argument("--cmd", default="")
     r.set_defaults(fn=cmd_traffic)

@@ -400,3 +400,22 @@ def test_moe_forward_validation(L, buf):
                             lib.DMOE_F32, None)
     assert st == INV  # buf is NULL
     assert lib.dmoe_moe_forward_workspace_size(1, 32, 2048, 600, 512, 512, 8, lib.DMOE_BF16) == 0
+
+
+def test_moe_forward_fused_query(L):
+    """The host-side answer to which path dmoe_moe_forward takes (no GPU)."""
+    bf, f32 = lib.DMOE_BF16, lib.DMOE_F32
+    fused = lib.dmoe_moe_forward_fused
+    assert fused(bf, 1, 32, 2048, 256, 512, 512, 8, "block")          # one decode block
+    assert fused(bf, 1, 64, 2048, 128, 512, 0, 8, "block")            # no shared expert, 64 tokens
+    assert not fused(bf, 1, 64, 2048, 256, 512, 0, 8, "block")        # 64 x 256 probabilities exceed on-chip space
+    assert not fused(bf, 1, 32, 2048, 256, 512, 512, 8, "token")      # token routing chains the entry points
+    assert not fused(bf, 1, 32, 2048, 256, 512, 512, 8, "topp")
+    assert not fused(bf, 2, 32, 2048, 256, 512, 512, 8, "block")      # several blocks
+    assert not fused(bf, 1, 65, 2048, 256, 512, 512, 8, "block")      # more than 64 tokens
+    assert not fused(f32, 1, 32, 256, 16, 128, 0, 2, "block")         # fp32 layers
+    assert not fused(bf, 1, 32, 2176, 256, 512, 512, 8, "block")      # H not a multiple of 256
+    assert not fused(bf, 1, 32, 2048, 254, 512, 512, 8, "block")      # E not a multiple of 4
+    assert not fused(bf, 1, 32, 2048, 256, 512, 512, 12, "block")     # k + shared > 12
+    assert not fused(bf, 1, 32, 2048, 600, 512, 512, 8, "block")      # E beyond the limit
+    assert not fused(bf, 0, 32, 2048, 256, 512, 512, 8, "block")      # invalid sizes
