@@ -426,14 +426,15 @@ dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const fl
  * A block-routed forward of a single bf16 block (n_blocks == 1, block_size
  * <= 64, E <= 512 and E % 4 == 0, k + (I_s > 0) <= 12, H % 256 == 0, T*E
  * small enough for on-chip probabilities; dmoe_moe_forward_fused says
- * whether a call qualifies) runs as three kernels: the router (logits, and x
- * in the chunk-major layout); the routing, recomputed by every workgroup of
+ * whether a call qualifies) runs as three kernels: the router (partial
+ * logits over up to four slices of the hidden dimension, and x in the
+ * chunk-major layout); the routing, recomputed by every workgroup of
  * the routed gate/up (the combine weight applied to the SwiGLU
  * activations), with the shared expert's gate/up as further workgroups of
  * the same launch; and one down projection over all selected experts and
  * the shared expert that writes y (no slot outputs, no combine kernel).  Its routing outputs equal
- * dmoe_route_block's up to the float32 rounding of the logits (one
- * reduction over the whole hidden dimension instead of slices), and y
+ * dmoe_route_block's up to the float32 rounding of the logits (the two
+ * routers may split the hidden dimension differently), and y
  * differs from the chained path's by the bf16 rounding of the weighted
  * activations.  Every other forward chains dmoe_route_block / _token /
  * _topp, dmoe_expert_ffn and dmoe_combine, with results bit-identical to

@@ -8,12 +8,15 @@
 // invalidation).  So the phases are merged where the merge needs no
 // synchronisation at all:
 //
-//  1. router.  Router tiles of 16 tokens x 16 experts over the whole hidden
-//     dimension write the logits; the workgroups of the first expert tile
-//     also write x in the chunk-major layout.
+//  1. router.  Router tiles of 16 tokens x 16 experts over one of up to four
+//     slices of the hidden dimension write partial logits (a decode step's
+//     router is bound by what each CU can load, so the slices spread it over
+//     more CUs); the workgroups of the first expert tile also write x in the
+//     chunk-major layout.
 //  2. routing + gate/up.  The shared expert needs only x: its workgroups
 //     stream its gate/up tiles at once.  Every other workgroup recomputes the block's
-//     routing from the logits -- softmax of each token row, the block mean
+//     routing from the logits -- the slices' partial logits added in slice
+//     order, softmax of each token row, the block mean
 //     in token order, the top-(k+1) by radix selection, the weights -- with
 //     the device routines of the routing kernels, so every workgroup reaches
 //     the same bits (workgroup (0, 0) writes the routing outputs and the
@@ -60,7 +63,8 @@ struct LayerParams {
   const bf16_t* ws13;  // shared gate/up, packed (nullptr: no shared expert)
   const bf16_t* ws2;   // shared down, packed
   int T, H, E, I, I_s, k;
-  float* z;            // [T][E] logits without the bias (workspace)
+  float* z;            // [nz][T][E] partial logits without the bias (workspace)
+  int nz;              // slices of the hidden dimension in the router (1, 2 or 4)
   bf16_t* xk;          // x chunk-major [H/8][T][8] (output)
   bf16_t* hk;          // activations chunk-major [(k*I + I_s)/8][T][8] (workspace)
   float* logits;       // [T][E] or nullptr
@@ -76,18 +80,29 @@ struct LayerParams {
 // ---- launch 1: router tiles and the shared expert's gate/up -----------------
 
 constexpr int kRouterBurst = 16;  // K-steps of 32 loaded at once per wave
+// Slices of the hidden dimension (when H is a multiple of 512): the router's
+// workgroups each read half of the bytes of a whole-dimension tile, over
+// twice the CUs (a decode step's router is bound by the loads each CU can
+// take); the softmax adds the slices' partial logits in slice order.
+constexpr int kRouterSlices = 4;
+template <int NQ>
+constexpr int kSlicesOf = NQ == 1 ? 4 : 2;  // partial rows a softmax lane can hold (E <= 256: 4)
+constexpr int router_slices(int H, int E) {  // 8: the router's waves
+  const int most = E <= 256 ? 4 : 2;
+  return most >= 4 && H % (32 * 8 * 4) == 0 ? 4 : (H % (32 * 8 * 2) == 0 ? 2 : 1);
+}
 
 // Logits of 16 tokens x 16 experts over the whole hidden dimension (the four
 // waves each reduce a quarter, summed in wave order).  A = x rows (tokens),
 // B = router rows (experts): lane (q, c) ends with tokens 4q..4q+3 of expert
 // column c.
 template <int NW>
-__device__ void router_tile(const LayerParams& p, int tile, f32x4 (*red)[kWave]) {
+__device__ void router_tile(const LayerParams& p, int tile, int slice, f32x4 (*red)[kWave]) {
   const int T = p.T, H = p.H, E = p.E;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
   const int ntt = (T + kTok - 1) / kTok;
   const int tt = tile % ntt, et = tile / ntt;
-  const int kq = H / NW, k0 = wave * kq, steps = kq / 32;
+  const int kq = H / (p.nz * NW), k0 = (slice * NW + wave) * kq, steps = kq / 32;
   const int t = min(tt * kTok + c, T - 1), e = min(et * kTok + c, E - 1);
   const bf16_t* pa = p.x + static_cast<size_t>(t) * H + k0 + q * 8;
   const bf16_t* pb = p.wr + static_cast<size_t>(e) * H + k0 + q * 8;
@@ -124,7 +139,7 @@ __device__ void router_tile(const LayerParams& p, int tile, f32x4 (*red)[kWave])
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int tr = tt * kTok + 4 * q + r;
-    if (tr < T) p.z[static_cast<size_t>(tr) * E + ec] = acc[r];
+    if (tr < T) p.z[(static_cast<size_t>(slice) * T + tr) * E + ec] = acc[r];
   }
 }
 
@@ -136,11 +151,12 @@ __device__ __forceinline__ void store_h(bf16_t* hk, int T, int chunk, int col, i
   *reinterpret_cast<uint32_t*>(hk + (static_cast<size_t>(chunk) * T + col) * 8 + 2 * q) = h0 | (h1 << 16);
 }
 
-// Eight waves split the hidden dimension (eight K-steps each for H = 2048).
+// Eight waves split one of the nz slices of the hidden dimension
+// (two K-steps each for H = 2048 in four slices).
 constexpr int kRouterWaves = 8;
 __global__ __launch_bounds__(kRouterWaves * kWave) void layer_router_kernel(LayerParams p) {
   __shared__ f32x4 red[kRouterWaves - 1][kWave];
-  router_tile<kRouterWaves>(p, blockIdx.x, red);
+  router_tile<kRouterWaves>(p, blockIdx.x, blockIdx.y, red);
 }
 
 // ---- launch 2: the block's routing, then the routed gate/up ------------------
@@ -254,9 +270,22 @@ __device__ void rows_softmax(const LayerParams& p, float* P, int Es, bool first)
   for (int pass = 0; pass < NPASS; ++pass) {
     const int t = 8 * (wave + kWaves * pass) + (lane >> 3);
     const float* src = p.z + static_cast<size_t>(min(t, T - 1)) * E;
-    f32x4 z[NV];
+    // the second slice (slice 0 again, not added, with one slice): every
+    // load is issued before the first wait
+    constexpr int NS = kSlicesOf<NQ>;
+    f32x4 z[NV], zs[NS - 1][NV];
 #pragma unroll
     for (int i = 0; i < NV; ++i) z[i] = *reinterpret_cast<const f32x4*>(src + min(4 * (sl + 8 * i), E - 4));
+#pragma unroll
+    for (int h = 1; h < NS; ++h) {
+      const float* sh = src + static_cast<size_t>(min(h, p.nz - 1)) * T * E;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) zs[h - 1][i] = *reinterpret_cast<const f32x4*>(sh + min(4 * (sl + 8 * i), E - 4));
+    }
+#pragma unroll
+    for (int h = 1; h < NS; ++h)  // slice order
+#pragma unroll
+      for (int i = 0; i < NV; ++i) z[i] += h < p.nz ? zs[h - 1][i] : zero4;
     float* lo = first && p.logits && t < T ? p.logits + static_cast<size_t>(t) * E : nullptr;
     float m = -INFINITY;
 #pragma unroll
@@ -524,7 +553,7 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
 template <int NT>
 hipError_t launch_nt(const LayerParams& p, dmoe_dtype y_dt, hipStream_t s) {
   const int n_router = ((p.T + kTok - 1) / kTok) * ((p.E + kTok - 1) / kTok);
-  layer_router_kernel<<<n_router, kRouterWaves * kWave, 0, s>>>(p);
+  layer_router_kernel<<<dim3(n_router, p.nz), kRouterWaves * kWave, 0, s>>>(p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t lds = prologue_words(p.T, p.E) * sizeof(float);
@@ -550,21 +579,21 @@ bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, i
   if (dt != DMOE_BF16 || n_blocks != 1) return false;
   if (T < 1 || T > 4 * kTok || E > dev::kRegSoftmaxMaxE || k > dev::kMaxK) return false;
   if (k + (I_s > 0 ? 1 : 0) > kMaxSegments) return false;
-  if (H % 256 || I % 128 || I_s % 128 || E % 4) return false;
+  if (H % (32 * kRouterWaves) || I % 128 || I_s % 128 || E % 4) return false;
   return prologue_words(T, E) * sizeof(float) <= 48 * 1024;
 }
 
 size_t layer_fused_workspace_bytes(int T, int E, int I, int I_s, int k) {
-  const size_t z = (static_cast<size_t>(T) * E * sizeof(float) + 255) & ~static_cast<size_t>(255);
+  const size_t z = (static_cast<size_t>(kRouterSlices) * T * E * sizeof(float) + 255) & ~static_cast<size_t>(255);
   return z + (static_cast<size_t>(k) * I + I_s) * T * sizeof(bf16_t);
 }
 
 hipError_t launch_layer_fused(const LayerArgs& a, hipStream_t s) {
-  const size_t zb = (static_cast<size_t>(a.T) * a.E * sizeof(float) + 255) & ~static_cast<size_t>(255);
+  const size_t zb = (static_cast<size_t>(kRouterSlices) * a.T * a.E * sizeof(float) + 255) & ~static_cast<size_t>(255);
   LayerParams p{static_cast<const bf16_t*>(a.x), static_cast<const bf16_t*>(a.w_router), a.bias,
                 static_cast<const bf16_t*>(a.w13), static_cast<const bf16_t*>(a.w2),
                 static_cast<const bf16_t*>(a.ws13), static_cast<const bf16_t*>(a.ws2), a.T, a.H, a.E, a.I, a.I_s,
-                a.k, static_cast<float*>(a.workspace),
+                a.k, static_cast<float*>(a.workspace), router_slices(a.H, a.E),
                 static_cast<bf16_t*>(a.x_chunked),
                 reinterpret_cast<bf16_t*>(static_cast<char*>(a.workspace) + zb), a.logits, a.probs, a.block_scores,
                 a.experts, a.combine_w, a.gap, a.sched, a.y};
