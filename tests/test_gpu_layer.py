@@ -89,3 +89,33 @@ def test_layer_workspace_too_small(gpu_lib):
                              layer.sched, layer.slot_out, layer.shared_out, small, layer.y)
     assert ei.value.status == lib.DMOE_ERR_INVALID_ARG
     assert np.isfinite(lib.dmoe_moe_forward_workspace_size(1, 32, 2048, 256, 512, 512, 8, lib.DMOE_BF16))
+
+
+# Forwards that do not take the one-block path: several blocks, token and
+# Top-P routing, a block above 64 tokens.
+CHAINED = {"small_bf16": ("small_bf16", {}), "small_bf16_zipf": ("small_bf16_zipf", {}),
+           "b2_bs72": ("small_bf16", dict(NB=2, bs=72)), "decode_b16": ("decode_b16", {})}
+
+
+@pytest.mark.parametrize("routing", ["block", "token", "topp"])
+@pytest.mark.parametrize("name", list(CHAINED))
+def test_moe_forward_equals_chained_calls(gpu_lib, name, routing):
+    """dmoe_moe_forward, where it chains the entry points inside the library,
+    gives bitwise what the same entry points give called one by one."""
+    base, kw = CHAINED[name]
+    cfg = get_config(base).with_(name=name, **kw)
+    print("case", name, routing, flush=True)
+    d = make_inputs(cfg, seed=21, device="cuda")
+    w = pack_weights(d)
+    one, ch = _layer(cfg), _layer(cfg)
+    assert not one.fused(routing)
+    y1 = one.forward(d["x"], w, routing).clone()
+    y2 = ch.forward(d["x"], w, routing, chained=True).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    assert torch.equal(one.probs, ch.probs)
+    assert torch.equal(one.experts(routing), ch.experts(routing))
+    assert torch.equal(one.combine_w, ch.combine_w)
+    n_work = int(one.sched.n_work[0])
+    assert n_work == int(ch.sched.n_work[0])
+    assert torch.equal(one.sched.work[:n_work], ch.sched.work[:n_work])
