@@ -119,3 +119,25 @@ def test_moe_forward_equals_chained_calls(gpu_lib, name, routing):
     n_work = int(one.sched.n_work[0])
     assert n_work == int(ch.sched.n_work[0])
     assert torch.equal(one.sched.work[:n_work], ch.sched.work[:n_work])
+
+
+@pytest.mark.parametrize("base,kw", [("decode_b1", {}), ("small_bf16", dict(NB=1, bs=24)),
+                                     ("small_bf16_zipf", dict(NB=1, bs=5))])
+def test_single_block_logits_output(gpu_lib, base, kw):
+    """The one-block path's optional logits output (the router's slices
+    summed in slice order, plus the bias) against the oracle's logits: four,
+    two and one hidden-dimension slices (H = 2048, 512, 768)."""
+    import oracle as O
+
+    cfg = get_config(base).with_(name=base + "_logits", **kw)
+    d = make_inputs(cfg, seed=5, device="cuda")
+    w = pack_weights(d)
+    layer = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, device="cuda", keep_logits=True)
+    assert layer.fused("block")
+    layer.forward(d["x"], w, "block")
+    torch.cuda.synchronize()
+    ref = O.router_logits(d["x"].cpu(), d["w_router"].cpu(), None if d.get("bias") is None else d["bias"].cpu())
+    got = layer.logits.cpu().numpy()
+    err = float(np.abs(got - ref).max())
+    print("  logits max|err|", err, "max|z|", float(np.abs(ref).max()), flush=True)
+    assert err <= 1e-4 * max(1.0, float(np.abs(ref).max()))
