@@ -177,7 +177,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
                         : p.xk + (static_cast<size_t>(chunk0) * p.T + tok[ct]) * 8;
     f32x4 acc[RT][NT];
     zero(acc);
-    wave_dot(w, pa, tstride, pb, gathered ? 32 : bstep, steps, acc, p0 > 0 && steps <= KMAX);
+    wave_dot<true>(w, pa, tstride, pb, gathered ? 32 : bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -231,7 +231,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
     }
     f32x4 acc[RT][NT];
     zero(acc);
-    wave_dot(w, pa, tstride, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
+    wave_dot<true>(w, pa, tstride, pb, bstep, steps, acc, p0 > 0 && steps <= KMAX);
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
@@ -307,14 +307,12 @@ constexpr int kTileTok = 8;       // token tiles per workgroup (128 tokens)
 constexpr int kStageSteps = 2;    // K-steps per LDS stage (two: 32 KB of LDS, three workgroups per CU)
 static_assert(kTileTok * 16 == DMOE_WORK_ROWS, "a tile workgroup covers one work item's rows");
 
-template <bool kGateUp, int kRowTiles>
-__global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p, int gx) {
+// The workgroup's work once its item is known (kStream: weights loaded
+// non-temporally).
+template <bool kGateUp, int kRowTiles, bool kStream>
+__device__ __forceinline__ void tile_body(const FfnParams& p, const Group& g, int bx,
+                                          bf16x8 (&stage)[2][kStageSteps][kTileTok][kWave]) {
   constexpr int kTileRows = 4 * kRowTiles;  // weight tiles per workgroup
-  int item, bx;
-  if (!map_item(p, gx, item, bx)) return;
-  Group g;
-  if (!decode_item(item, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, p.E, g)) return;
-  if (g.piece == 0 && g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
   const int H = p.H;
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int Kd = kGateUp ? H : Iw;                    // reduction length
@@ -362,7 +360,6 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p,
                      : src + (static_cast<size_t>(pq) * rows_b + row[h]) * 8;
   const int bstep = gathered ? 32 : 32 * rows_b;
 
-  __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 64 KiB
   f32x4 acc[kRowTiles][kTileTok];
 #pragma unroll
   for (int m = 0; m < kRowTiles; ++m)
@@ -378,7 +375,9 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p,
 #pragma unroll
     for (int s = 0; s < kStageSteps; ++s)
 #pragma unroll
-      for (int m = 0; m < kRowTiles; ++m) a[s][m] = ld_bf16x8(pa + m * tstride + (st * kStageSteps + s) * kFrag);
+      for (int m = 0; m < kRowTiles; ++m)
+        a[s][m] = kStream ? ld_bf16x8_stream(pa + m * tstride + (st * kStageSteps + s) * kFrag)
+                          : ld_bf16x8(pa + m * tstride + (st * kStageSteps + s) * kFrag);
   };
   auto load_b = [&](int st) {
 #pragma unroll
@@ -467,6 +466,33 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p,
       }
     }
   }
+}
+
+
+template <bool kGateUp, int kRowTiles>
+__global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p, int gx) {
+  int item, bx;
+  if (!map_item(p, gx, item, bx)) return;
+  Group g;
+  if (!decode_item(item, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, p.E, g)) return;
+  if (g.piece == 0 && g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
+  __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 32 KiB
+  // An expert whose rows are one item is the only reader of its weights in
+  // the launch (each row block reads its own rows once): they are streamed
+  // non-temporally, which measured faster.  The items of an expert with more
+  // rows read the same weights one after the other, through the L2 of the
+  // XCD they share (non-temporal loads there measured slower).
+  bool single;
+  if (g.expert >= 0) {
+    const int nw = min(*p.n_work, p.max_work);
+    single = g.piece == 0 && !(item + 1 < nw && reinterpret_cast<const int4*>(p.work)[item + 1].x == g.expert);
+  } else {
+    single = p.T <= DMOE_WORK_ROWS;
+  }
+  if (single)
+    tile_body<kGateUp, kRowTiles, true>(p, g, bx, stage);
+  else
+    tile_body<kGateUp, kRowTiles, false>(p, g, bx, stage);
 }
 
 // ---- f32 path -------------------------------------------------------------

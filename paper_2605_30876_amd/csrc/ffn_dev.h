@@ -23,14 +23,16 @@ struct WaveOps {
 };
 
 // A: packed tiles, step s of tile r at pa + r*tstride + s*kFrag (one
-// contiguous burst per tile).
-template <int NT, int KMAX, int BC, int RT>
+// contiguous burst per tile).  kStream: non-temporal loads, for weights no
+// other workgroup of the launch reads again.
+template <bool kStream, int NT, int KMAX, int BC, int RT>
 __device__ __forceinline__ void issue_a(WaveOps<NT, KMAX, BC, RT>& w, const bf16_t* pa, size_t tstride, int ns) {
 #pragma unroll
   for (int r = 0; r < RT; ++r)
 #pragma unroll
     for (int s = 0; s < KMAX; ++s)
-      if (s < ns) w.a[r][s] = ld_bf16x8(pa + r * tstride + s * kFrag);
+      if (s < ns)
+        w.a[r][s] = kStream ? ld_bf16x8_stream(pa + r * tstride + s * kFrag) : ld_bf16x8(pa + r * tstride + s * kFrag);
 }
 
 // B: chunk-major rows, step s at pb[ct] + s*bstep.
@@ -70,7 +72,8 @@ __device__ __forceinline__ void mma_chunk(WaveOps<NT, KMAX, BC, RT>& w, const bf
 // steps: token chunk 0, the weight burst, then the remaining token chunks.
 // With a_held (the slice is one burst, steps <= KMAX, already in w.a from
 // the previous pass over the same weights) the weights are not loaded again.
-template <int NT, int KMAX, int BC, int RT>
+// kStream: the weights are loaded non-temporally (see issue_a).
+template <bool kStream, int NT, int KMAX, int BC, int RT>
 __device__ __forceinline__ void wave_dot(WaveOps<NT, KMAX, BC, RT>& w, const bf16_t* pa, size_t tstride,
                                          const bf16_t* const* pb, int bstep, int steps, f32x4 (&acc)[RT][NT],
                                          bool a_held) {
@@ -80,7 +83,7 @@ __device__ __forceinline__ void wave_dot(WaveOps<NT, KMAX, BC, RT>& w, const bf1
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) pbs[ct] = pb[ct] + sc * bstep;
     issue_b<0>(w, pbs, bstep, 0, ns);
-    if (!a_held) issue_a(w, pa + sc * kFrag, tstride, ns);
+    if (!a_held) issue_a<kStream>(w, pa + sc * kFrag, tstride, ns);
     __builtin_amdgcn_sched_barrier(0);
     mma_chunk<0>(w, pbs, bstep, ns, acc);
   }

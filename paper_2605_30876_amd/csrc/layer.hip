@@ -367,7 +367,7 @@ __device__ void shared_gateup_tiles(const LayerParams& p, int it0, f32x4 (*red)[
   f32x4 acc[kRT][NT];
   fdev::zero(acc);
   fdev::WaveOps<NT, 16, 4, kRT> w;
-  fdev::wave_dot(w, pa, static_cast<size_t>(ksteps) * kFrag, pb, 32 * T, steps, acc, false);
+  fdev::wave_dot<true>(w, pa, static_cast<size_t>(ksteps) * kFrag, pb, 32 * T, steps, acc, false);
   fdev::reduce_waves(acc, red, wave, lane);
   if (wave != 0) return;
 #pragma unroll
@@ -447,7 +447,7 @@ __global__ __launch_bounds__(kThreads, 2) void layer_route_gateup_kernel(LayerPa
   f32x4 acc[kRT][NT];
   fdev::zero(acc);
   fdev::WaveOps<NT, 16, 4, kRT> w;
-  fdev::wave_dot(w, pa, static_cast<size_t>(ksteps) * kFrag, pb, 32 * T, steps, acc, false);
+  fdev::wave_dot<true>(w, pa, static_cast<size_t>(ksteps) * kFrag, pb, 32 * T, steps, acc, false);
 
   // 6. the routing outputs (workgroup (0, 0), while the other workgroups
   //    stream): the selection, gap, every token's combine weights (its
@@ -532,7 +532,7 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
   f32x4 acc[1][NT];
   fdev::zero(acc);
   fdev::WaveOps<NT, 16, kTokChunk<NT>, 1> w;
-  fdev::wave_dot(w, pa, 0, pb, 32 * T, ksteps, acc, false);
+  fdev::wave_dot<true>(w, pa, 0, pb, 32 * T, ksteps, acc, false);
   if (wave > 0) {
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) red[wave - 1][ct][lane] = acc[0][ct];
