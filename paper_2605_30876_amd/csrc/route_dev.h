@@ -575,9 +575,10 @@ __device__ inline void schedule_totals(int c, int gs, int E, const dmoe_schedule
 //      running count plus the entries below it in the round's per-expert
 //      bitmask (read as four 128-bit words), so each expert's rows come out
 //      in token order and the schedule is identical on every run; then all
-//      threads write the round's rows.
+//      threads write the round's rows.  With place_rows false step 3 is left
+//      to a many-workgroup launch (schedule_rows_kernel).
 __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs, int k, int E, int* lds,
-                                   const dmoe_schedule& sched) {
+                                   const dmoe_schedule& sched, bool place_rows = true) {
   int32_t* const row_token = sched.row_token;
   int32_t* const row_slot = sched.row_slot;
   const int Ep = pad4(E);
@@ -606,6 +607,7 @@ __device__ inline void schedule_wg(const int32_t* experts, int n_groups, int gs,
 
   schedule_totals(tid < E ? cnt[tid] : 0, gs, E, sched, base);
   __syncthreads();
+  if (!place_rows) return;
 
   const int word = tid >> 5;
   const unsigned bit = 1u << (tid & 31);

@@ -7,6 +7,9 @@
 // the expert FFN's work items).  Token schedules with many entries and a
 // scratch array run the same steps over many workgroups (count, scan,
 // place); the placement rule is the same, so the results are identical.
+// Block schedules with many rows leave the rows to one workgroup per group
+// (the single workgroup's stores of thousands of rows were the long pole:
+// 64 blocks of 64 tokens, 32768 rows, took ~20 us).
 #include <algorithm>
 
 #include "route_dev.h"
@@ -15,9 +18,63 @@ namespace dmoe {
 namespace {
 
 __global__ __launch_bounds__(dev::kSchedThreads) void schedule_kernel(
-    const int32_t* __restrict__ experts, int n_groups, int gs, int k, int E, dmoe_schedule sched) {
+    const int32_t* __restrict__ experts, int n_groups, int gs, int k, int E, dmoe_schedule sched, int place_rows) {
   extern __shared__ int lds[];
-  dev::schedule_wg(experts, n_groups, gs, k, E, lds, sched);
+  dev::schedule_wg(experts, n_groups, gs, k, E, lds, sched, place_rows != 0);
+}
+
+// ---- rows of a block schedule, one workgroup per group --------------------
+// Entry (g, j) (expert e = experts[g*k + j]) starts at row
+//   offsets[u] + gs * (entries before it, in index order, naming e),
+// u the rank of e among the unique ids: the rows dev::schedule_wg places.
+// Workgroup g counts the earlier entries naming each of its k experts (LDS
+// counters), finds u by binary search in the ascending unique list, and
+// writes the gs rows of each of its entries.
+constexpr int kRowsThreads = 256;
+constexpr int kRowsMinRows = 2048;  // rows (n_groups * gs * k) from which the rows get their own launch
+
+__global__ __launch_bounds__(kRowsThreads) void schedule_rows_kernel(const int32_t* __restrict__ experts, int gs,
+                                                                     int k, int E, dmoe_schedule sched) {
+  __shared__ int mine[kWave], cnt[kWave], pos[kWave];
+  const int g = blockIdx.x, tid = threadIdx.x;
+  if (tid < k) {
+    mine[tid] = experts[static_cast<size_t>(g) * k + tid];
+    cnt[tid] = 0;
+  }
+  __syncthreads();
+  const int before = g * k;
+  for (int i = tid; i < before; i += kRowsThreads) {
+    const int v = experts[i];
+    for (int j = 0; j < k; ++j)
+      if (mine[j] == v) atomicAdd(&cnt[j], 1);
+  }
+  __syncthreads();
+  if (tid < k) {
+    const int e = mine[tid];
+    int p = -1;  // an id outside [0, E): no rows
+    if (e >= 0 && e < E) {
+      int r = cnt[tid];
+      for (int j = 0; j < tid; ++j) r += mine[j] == e ? 1 : 0;  // earlier entries of this group
+      int lo = 0, hi = *sched.n_unique;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (sched.unique[mid] < e)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      p = sched.offsets[lo] + r * gs;
+    }
+    pos[tid] = p;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < k * gs; idx += kRowsThreads) {
+    const int j = idx / gs, tl = idx - j * gs;
+    const int p = pos[j];
+    if (p < 0) continue;
+    sched.row_token[p + tl] = g * gs + tl;
+    sched.row_slot[p + tl] = j;
+  }
 }
 
 // ---- many workgroups (group size 1, many entries) -------------------------
@@ -146,7 +203,11 @@ hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, 
     return hipGetLastError();
   }
   const size_t lds = dev::schedule_lds_ints(E) * sizeof(int);
-  schedule_kernel<<<1, dev::kSchedThreads, lds, s>>>(experts, n_groups, gs, k, E, sched);
+  const bool rows_apart = gs > 1 && n_groups > 1 && static_cast<long>(n_entries) * gs >= kRowsMinRows;
+  schedule_kernel<<<1, dev::kSchedThreads, lds, s>>>(experts, n_groups, gs, k, E, sched, rows_apart ? 0 : 1);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || !rows_apart) return err;
+  schedule_rows_kernel<<<n_groups, kRowsThreads, 0, s>>>(experts, gs, k, E, sched);
   return hipGetLastError();
 }
 

@@ -62,6 +62,25 @@ def test_tile_kernel_parity(gpu_lib, name, routing):
     _say("  ", {k: v for k, v in rep.items() if k != "near_ties"})
 
 
+# Shapes whose router takes the LDS-staged tiles (T >= 256) with ragged token
+# and expert tails: 64-token tiles in four slices (1500 tokens, 200 experts),
+# 128-token tiles in four slices (2100 tokens), and 32-token tiles where no
+# shape reaches one workgroup per CU (300 tokens, 64 experts).
+ROUTER_TILE = {"router_t1500_e200": dict(H=512, E=200, I=128, I_s=128, k=8, NB=60, bs=25),
+               "router_t2100_e200": dict(H=512, E=200, I=128, I_s=0, k=4, NB=70, bs=30),
+               "router_t300_e64": dict(H=768, E=64, I=128, I_s=128, k=8, NB=12, bs=25)}
+
+
+@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("name", list(ROUTER_TILE))
+def test_router_tile_parity(gpu_lib, name, routing):
+    cfg = get_config("small_bf16").with_(name=name, **ROUTER_TILE[name])
+    _say("case", name, routing)
+    d = _to_gpu(make_inputs(cfg, seed=4))
+    rep = run_and_check(cfg, d, routing, _layer(cfg))
+    _say("  ", {k: v for k, v in rep.items() if k != "near_ties"})
+
+
 # Full-size layers: routing, schedule and the output of every token are
 # checked against the oracle, and a second forward must equal the first
 # bitwise (the combine is a fixed-order gather-sum, no atomics).

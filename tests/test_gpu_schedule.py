@@ -43,3 +43,37 @@ def test_split_schedule_matches_single_workgroup(gpu_lib, T, k, E, skew):
     rt, rs = a.row_token.cpu().numpy(), a.row_slot.cpu().numpy()
     for u, e in enumerate(uniq.tolist()):
         assert list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist())) == rows[e]
+
+
+@pytest.mark.parametrize("NB,bs,k,E,skew", [(64, 64, 8, 256, 1.0), (16, 32, 8, 256, 2.0), (20, 25, 5, 12, 1.0),
+                                            (40, 24, 8, 64, 4.0), (3, 700, 1, 5, 1.0)])
+def test_block_schedule_rows(gpu_lib, NB, bs, k, E, skew):
+    """Block schedules of at least 2048 rows place their rows one workgroup per
+    block; every expert's rows, the unique list and the work items must be
+    the oracle's."""
+    print("case", NB, bs, k, E, skew, flush=True)
+    ids = _lists(NB, k, E, seed=NB * bs + E, skew=skew)
+    assert NB * bs * k >= 2048 and NB > 1  # takes the many-workgroup row placement
+    dev = torch.from_numpy(ids).cuda()
+    mw = lib.dmoe_schedule_max_work(NB, bs, k, E)
+    s = lib.Schedule.empty(E, NB * bs * k, "cuda", mw, scratch=False)
+    s.row_token.fill_(-1)
+    s.row_slot.fill_(-1)
+    lib.dmoe_build_expert_schedule(dev, NB, bs, k, E, s)
+    torch.cuda.synchronize()
+    uniq = O.unique_experts(ids)
+    n_u = int(s.n_unique[0])
+    assert n_u == uniq.size and s.unique[:n_u].cpu().numpy().tolist() == uniq.tolist()
+    rows = O.expert_rows(ids, bs)
+    offs = s.offsets.cpu().numpy()
+    assert offs[n_u] == NB * bs * k
+    rt, rs = s.row_token.cpu().numpy(), s.row_slot.cpu().numpy()
+    for u, e in enumerate(uniq.tolist()):
+        assert list(zip(rt[offs[u]:offs[u + 1]].tolist(), rs[offs[u]:offs[u + 1]].tolist())) == rows[e], e
+    items, r0 = [], 0
+    for e in uniq.tolist():
+        n = len(rows[e])
+        items += [[e, r0 + c, min(lib.WORK_ROWS, n - c), c // lib.WORK_ROWS] for c in range(0, n, lib.WORK_ROWS)]
+        r0 += n
+    n_work = int(s.n_work[0])
+    assert n_work == len(items) and s.work[:n_work].cpu().numpy().tolist() == items
