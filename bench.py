@@ -70,6 +70,8 @@ def parse():
     ap.add_argument("--ffn-only", action="store_true",
                     help="only replay the expert FFN (for hardware-counter runs)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--slot-format", choices=["f16s", "f32"], default=None,
+                    help="storage of the per-slot expert outputs (default: f16s for bf16 layers, f32 for fp32)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB buffer a few times (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -156,7 +158,7 @@ def auto_layers(torch, cfg, B_e, B_s, min_bytes=1.5 * 2**30, cap=64):
     return max(2, min(cap, -(-int(min_bytes) // per_step), int(0.5 * free // layer_bytes)))
 
 
-def build_layers(torch, cfg, NL, seed, dev, top_p, keep_host0=False):
+def build_layers(torch, cfg, NL, seed, dev, top_p, keep_host0=False, slot_format=None):
     from dmoe_synth import make_inputs
     from paper_2605_30876_amd.layer import MoELayer, pack_weights
 
@@ -168,7 +170,8 @@ def build_layers(torch, cfg, NL, seed, dev, top_p, keep_host0=False):
             host0 = {k: (None if v is None else v.to("cpu")) for k, v in d.items()}
         w = pack_weights(d)  # the layer keeps only the packed expert weights
         layers.append((d["x"], w, MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt,
-                                           device=dev, out_dtype=torch.float32, top_p=top_p)))
+                                           device=dev, out_dtype=torch.float32, top_p=top_p,
+                                           slot_format=slot_format)))
         del d
     torch.cuda.synchronize()
     return layers, host0
@@ -276,7 +279,7 @@ def workload_figures(torch, name, args, dev, modes):
 
     cfg = get_config(name)
     NL = auto_layers(torch, cfg, expert_bytes(cfg), shared_bytes(cfg), min_bytes=1.0 * 2**30, cap=8)
-    layers, _ = build_layers(torch, cfg, NL, args.seed, dev, args.top_p)
+    layers, _ = build_layers(torch, cfg, NL, args.seed, dev, args.top_p, slot_format=args.slot_format)
     steps = max(2 * NL, 16)
     res = measure_modes(torch, cfg, layers, modes, steps, NL, not args.no_graph)
     out = {"workload": f"hidden {cfg.H}, {cfg.E} experts of intermediate {cfg.I} + shared {cfg.I_s}, "
@@ -334,7 +337,8 @@ def main():
         f"{NL} layers ({NL * (cfg.E * B_e + B_s) / 2**30:.1f} GiB of weights), {steps} steps per mode")
 
     t0 = time.time()
-    layers, host0 = build_layers(torch, cfg, NL, args.seed, dev, args.top_p, keep_host0=not args.no_cpu_baseline)
+    layers, host0 = build_layers(torch, cfg, NL, args.seed, dev, args.top_p, keep_host0=not args.no_cpu_baseline,
+                                 slot_format=args.slot_format)
     log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
 
     modes = ["block", "token", "topp"] if args.routing == "all" else [args.routing]

@@ -93,6 +93,30 @@ typedef enum dmoe_dtype {
 } dmoe_dtype;
 
 /*
+ * Storage of the per-slot expert outputs slot_out [T][k][H] that
+ * dmoe_expert_ffn writes and dmoe_combine reads (device memory, 16-byte
+ * aligned, dmoe_slot_out_bytes(T, H, k, format) bytes):
+ *   DMOE_SLOT_F32   float32 [T][k][H].
+ *   DMOE_SLOT_F16S  scaled half, for DMOE_BF16 layers (about half the bytes
+ *                   of the round trip through memory): uint16
+ *                   half[T][k][H] (IEEE binary16 bit patterns), then int8
+ *                   e[T][k][H/16]; value = half[t][j][h] * 2^e[t][j][h/16].
+ *                   Each sixteen consecutive outputs share e, chosen so
+ *                   that the largest finite magnitude of the sixteen lies in
+ *                   [2^14, 2^15): no overflow, 11 significant bits
+ *                   (relative error <= 2^-11) for every value within 2^28 of
+ *                   that maximum, smaller ones with absolute error below
+ *                   2^-25 of it; NaN and infinities are kept.  H % 16 == 0.
+ */
+typedef enum dmoe_slot_format {
+  DMOE_SLOT_F32 = 0,
+  DMOE_SLOT_F16S = 1
+} dmoe_slot_format;
+
+/* Bytes of slot_out for these sizes in format f (0 on invalid sizes). */
+size_t dmoe_slot_out_bytes(int T, int H, int k, dmoe_slot_format f);
+
+/*
  * Unique-expert schedule of one forward (device arrays, caller-allocated).
  * Written by dmoe_build_expert_schedule (or dmoe_route_*), read by
  * dmoe_expert_ffn.
@@ -342,8 +366,9 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  * what they held, so a smaller value gives wrong results without an error.
  * The shared expert's T rows are cut into pieces of DMOE_WORK_ROWS the same
  * way.
- * slot_out [T][k][H] float32 (every (t, j) is written); shared_out [T][H]
- * float32 (NULL iff no shared expert).
+ * slot_out [T][k][H] in format slot_fmt (every (t, j) is written;
+ * DMOE_SLOT_F16S only with DMOE_BF16, else DMOE_ERR_UNSUPPORTED); shared_out
+ * [T][H] float32 (NULL iff no shared expert).
  * workspace: device scratch of at least dmoe_ffn_workspace_size(...) bytes,
  * ws_bytes its size.  Its contents on entry do not matter; calls that share
  * one workspace must not overlap in time (use one stream).
@@ -354,8 +379,9 @@ size_t dmoe_ffn_workspace_size(int T, int I, int I_s, int k, dmoe_dtype dt);
  */
 dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w13, const void* w2,
                             const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
-                            int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
-                            float* shared_out, void* workspace, size_t ws_bytes, void* stream);
+                            int I_s, int k, int max_work, dmoe_schedule sched, void* slot_out,
+                            dmoe_slot_format slot_fmt, float* shared_out, void* workspace, size_t ws_bytes,
+                            void* stream);
 
 /*
  * dmoe_expert_ffn without a workspace argument, for callers that cannot
@@ -375,8 +401,8 @@ dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w1
 #define DMOE_NOALLOC_SCRATCH_BYTES (16u << 20)
 dmoe_status dmoe_expert_ffn_noalloc(const void* x_chunked, const void* x, const void* w13, const void* w2,
                                     const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
-                                    int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
-                                    float* shared_out, void* stream);
+                                    int I_s, int k, int max_work, dmoe_schedule sched, void* slot_out,
+                                    dmoe_slot_format slot_fmt, float* shared_out, void* stream);
 
 /*
  * The shared expert alone (the I_s > 0 part of dmoe_expert_ffn; expert
@@ -409,12 +435,13 @@ dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, cons
  * selected experts renormalised to sum to 1, with no further scaling (the
  * paper leaves the weighting open; this is the reading taken), and the
  * shared expert enters with weight 1.
- * slot_out [T][k][H] float32; combine_w [T][k] float32; shared_out [T][H]
+ * slot_out [T][k][H] in format slot_fmt (scaled half values are decoded
+ * exactly to float32 first); combine_w [T][k] float32; shared_out [T][H]
  * float32 or NULL; y [T][H] of type dt.
- * Limits: T >= 1; 1 <= k <= 64; H >= 1; H % 4 == 0.
+ * Limits: T >= 1; 1 <= k <= 64; H >= 1; H % 4 == 0 (DMOE_SLOT_F16S: H % 16 == 0).
  */
-dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const float* shared_out,
-                         dmoe_dtype dt, int T, int H, int k, void* y, void* stream);
+dmoe_status dmoe_combine(const void* slot_out, dmoe_slot_format slot_fmt, const float* combine_w,
+                         const float* shared_out, dmoe_dtype dt, int T, int H, int k, void* y, void* stream);
 
 /*
  * The whole MoE layer forward in one call: routing (dmoe_routing), the
@@ -447,9 +474,9 @@ dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const fl
  * entry points the layer chains (experts is block_experts [n_blocks][k] for
  * block routing and token_experts [T][k] otherwise; gap is [n_blocks] or
  * [T]; coreset and coreset_size are used by topp only, else may be NULL;
- * slot_out [T][k][H] and shared_out [T][H] are scratch of the chained path
- * and are left untouched by the three-kernel path, shared_out NULL iff
- * I_s == 0).  y [T][H] of type y_dt.  workspace: at least
+ * slot_out [T][k][H] (format slot_fmt) and shared_out [T][H] are scratch
+ * of the chained path and are left untouched by the three-kernel path,
+ * shared_out NULL iff I_s == 0).  y [T][H] of type y_dt.  workspace: at least
  * dmoe_moe_forward_workspace_size bytes (contents on entry do not matter;
  * calls sharing one must not overlap in time).
  * Limits: those of the chained entry points (E <= 512; bf16: H, I, I_s
@@ -472,7 +499,8 @@ typedef struct dmoe_layer_buffers {
   int32_t* coreset;     /* topp: [n_blocks][E] */
   int32_t* coreset_size;/* topp: [n_blocks] */
   dmoe_schedule sched;
-  float* slot_out;
+  void* slot_out;       /* [T][k][H] in format slot_fmt */
+  dmoe_slot_format slot_fmt;
   float* shared_out;
   void* workspace;
   size_t ws_bytes;

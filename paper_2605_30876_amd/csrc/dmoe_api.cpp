@@ -34,6 +34,7 @@ dmoe_status hip_status(hipError_t err, const char* fn) {
 bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
 bool valid_dtype(dmoe_dtype dt) { return dt == DMOE_F32 || dt == DMOE_BF16; }
+bool valid_slot_format(dmoe_slot_format f) { return f == DMOE_SLOT_F32 || f == DMOE_SLOT_F16S; }
 
 constexpr int kMaxE = 4096;
 constexpr int kMaxScheduleE = 512;
@@ -401,8 +402,8 @@ namespace {
 // the host first; then (noalloc) the device scratch replaces the workspace.
 dmoe_status expert_ffn(const char* fn, const void* x_chunked, const void* x, const void* w13, const void* w2,
                        const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I, int I_s, int k,
-                       int max_work, dmoe_schedule sched, float* slot_out, float* shared_out, void* workspace,
-                       size_t ws_bytes, void* stream, bool noalloc) {
+                       int max_work, dmoe_schedule sched, void* slot_out, dmoe_slot_format slot_fmt,
+                       float* shared_out, void* workspace, size_t ws_bytes, void* stream, bool noalloc) {
 #undef DMOE_FN
 #define DMOE_FN fn  // messages name the entry point
   REQUIRE(x_chunked && w13 && w2 && slot_out && (workspace || noalloc),
@@ -411,6 +412,7 @@ dmoe_status expert_ffn(const char* fn, const void* x_chunked, const void* x, con
               sched.work,
           "every schedule array must be set");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(valid_slot_format(slot_fmt), "unknown slot format %d", static_cast<int>(slot_fmt));
   REQUIRE(T >= 1 && H >= 1 && I >= 1 && I_s >= 0, "T=%d, H=%d, I=%d must be >= 1 and I_s=%d >= 0",
           T, H, I, I_s);
   REQUIRE(E >= 1, "E=%d must be >= 1", E);
@@ -452,12 +454,13 @@ dmoe_status expert_ffn(const char* fn, const void* x_chunked, const void* x, con
     SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
             "bf16 experts need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
   }
+  SUPPORT(slot_fmt == DMOE_SLOT_F32 || dt == DMOE_BF16, "scaled-half slot outputs need DMOE_BF16 experts");
   if (noalloc) {
     const hipError_t err = dmoe::noalloc_scratch(&workspace);
     if (err != hipSuccess) return fail(DMOE_ERR_HIP, fn, "device scratch lookup failed: %s", hipGetErrorString(err));
   }
   dmoe::FfnArgs a{x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work,
-                  sched, slot_out, shared_out, workspace};
+                  sched, slot_out, slot_fmt, shared_out, workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), fn);
 }
 #undef DMOE_FN
@@ -469,18 +472,19 @@ extern "C" {
 
 dmoe_status dmoe_expert_ffn(const void* x_chunked, const void* x, const void* w13, const void* w2,
                             const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
-                            int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
-                            float* shared_out, void* workspace, size_t ws_bytes, void* stream) {
+                            int I_s, int k, int max_work, dmoe_schedule sched, void* slot_out,
+                            dmoe_slot_format slot_fmt, float* shared_out, void* workspace, size_t ws_bytes,
+                            void* stream) {
   return expert_ffn(__func__, x_chunked, x, w13, w2, ws13, ws2, dt, T, H, E, I, I_s, k, max_work, sched, slot_out,
-                    shared_out, workspace, ws_bytes, stream, false);
+                    slot_fmt, shared_out, workspace, ws_bytes, stream, false);
 }
 
 dmoe_status dmoe_expert_ffn_noalloc(const void* x_chunked, const void* x, const void* w13, const void* w2,
                                     const void* ws13, const void* ws2, dmoe_dtype dt, int T, int H, int E, int I,
-                                    int I_s, int k, int max_work, dmoe_schedule sched, float* slot_out,
-                                    float* shared_out, void* stream) {
+                                    int I_s, int k, int max_work, dmoe_schedule sched, void* slot_out,
+                                    dmoe_slot_format slot_fmt, float* shared_out, void* stream) {
   return expert_ffn(__func__, x_chunked, x, w13, w2, ws13, ws2, dt, T, H, E, I, I_s, k, max_work, sched, slot_out,
-                    shared_out, nullptr, 0, stream, true);
+                    slot_fmt, shared_out, nullptr, 0, stream, true);
 }
 
 size_t dmoe_shared_ffn_workspace_size(int T, int I_s, dmoe_dtype dt) {
@@ -510,23 +514,30 @@ dmoe_status dmoe_shared_expert_ffn(const void* x_chunked, const void* ws13, cons
             "bf16 experts need H and I_s to be multiples of 128 (H=%d, I_s=%d)", H, I_s);
   }
   const dmoe_schedule none{};
-  dmoe::FfnArgs a{x_chunked, nullptr, nullptr, nullptr, ws13, ws2, T, H, 1, 0, I_s, 0, 0, none, nullptr, shared_out,
-                  workspace};
+  dmoe::FfnArgs a{x_chunked, nullptr, nullptr, nullptr, ws13, ws2, T, H, 1, 0, I_s, 0, 0, none, nullptr,
+                  DMOE_SLOT_F32, shared_out, workspace};
   return hip_status(dmoe::launch_ffn(a, dt, static_cast<hipStream_t>(stream)), __func__);
 }
 
-dmoe_status dmoe_combine(const float* slot_out, const float* combine_w, const float* shared_out,
-                         dmoe_dtype dt, int T, int H, int k, void* y, void* stream) {
+size_t dmoe_slot_out_bytes(int T, int H, int k, dmoe_slot_format f) {
+  if (T < 1 || H < 1 || k < 1 || k > kMaxK || !valid_slot_format(f) || (f == DMOE_SLOT_F16S && H % 16)) return 0;
+  return dmoe::slot_out_bytes(T, H, k, f);
+}
+
+dmoe_status dmoe_combine(const void* slot_out, dmoe_slot_format slot_fmt, const float* combine_w,
+                         const float* shared_out, dmoe_dtype dt, int T, int H, int k, void* y, void* stream) {
   REQUIRE(slot_out && combine_w && y, "slot_out, combine_w and y must not be NULL");
   REQUIRE(valid_dtype(dt), "unknown dtype %d", static_cast<int>(dt));
+  REQUIRE(valid_slot_format(slot_fmt), "unknown slot format %d", static_cast<int>(slot_fmt));
   REQUIRE(T >= 1 && H >= 1, "T=%d and H=%d must be >= 1", T, H);
-  REQUIRE(H % 4 == 0, "H=%d must be a multiple of 4", H);
+  REQUIRE(H % (slot_fmt == DMOE_SLOT_F16S ? 16 : 4) == 0, "H=%d must be a multiple of %d", H,
+          slot_fmt == DMOE_SLOT_F16S ? 16 : 4);
   REQUIRE(k >= 1 && k <= kMaxK, "k=%d must be in [1, %d]", k, kMaxK);
   ALIGNED(slot_out);
   ALIGNED(combine_w);
   ALIGNED(shared_out);
   ALIGNED(y);
-  return hip_status(dmoe::launch_combine(slot_out, combine_w, shared_out, dt, T, H, k, y,
+  return hip_status(dmoe::launch_combine(slot_out, slot_fmt, combine_w, shared_out, dt, T, H, k, y,
                                          static_cast<hipStream_t>(stream)),
                     __func__);
 }
@@ -581,6 +592,7 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
               sched.work,
           "every schedule array must be set");
   REQUIRE(valid_dtype(dt) && valid_dtype(y_dt), "unknown dtype %d / %d", static_cast<int>(dt), static_cast<int>(y_dt));
+  REQUIRE(valid_slot_format(buf->slot_fmt), "unknown slot format %d", static_cast<int>(buf->slot_fmt));
   REQUIRE(routing == DMOE_ROUTE_BLOCK || routing == DMOE_ROUTE_TOKEN || routing == DMOE_ROUTE_TOPP,
           "unknown routing %d", static_cast<int>(routing));
   REQUIRE(n_blocks >= 1, "n_blocks=%d must be >= 1", n_blocks);
@@ -638,6 +650,7 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
     SUPPORT(H % 128 == 0 && I % 128 == 0 && I_s % 128 == 0,
             "bf16 layers need H, I and I_s to be multiples of 128 (H=%d, I=%d, I_s=%d)", H, I, I_s);
   }
+  SUPPORT(buf->slot_fmt == DMOE_SLOT_F32 || dt == DMOE_BF16, "scaled-half slot outputs need a DMOE_BF16 layer");
   if (routing == DMOE_ROUTE_TOPP) {
     SUPPORT(dmoe::topp_supported(block_size, E, k), "the Top-P kernels do not support block_size=%d, E=%d, k=%d",
             block_size, E, k);
@@ -668,10 +681,11 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
   const long mw = routing == DMOE_ROUTE_BLOCK ? dmoe::schedule_max_work(n_blocks, block_size, k, E)
                                               : dmoe::schedule_max_work(T, 1, k, E);
   dmoe::FfnArgs fa{buf->x_chunked, x, w13, w2, ws13, ws2, Ti, H, E, I, I_s, k, static_cast<int>(mw), sched,
-                   buf->slot_out, buf->shared_out, ffn_ws};
+                   buf->slot_out, buf->slot_fmt, buf->shared_out, ffn_ws};
   err = dmoe::launch_ffn(fa, dt, s);
   if (err != hipSuccess) return hip_status(err, __func__);
-  return hip_status(dmoe::launch_combine(buf->slot_out, buf->combine_w, buf->shared_out, y_dt, Ti, H, k, y, s),
+  return hip_status(dmoe::launch_combine(buf->slot_out, buf->slot_fmt, buf->combine_w, buf->shared_out, y_dt, Ti, H,
+                                         k, y, s),
                     __func__);
 }
 

@@ -58,6 +58,58 @@ __device__ __forceinline__ bf16x8 ld_bf16x8_stream(const bf16_t* p) {
 
 __device__ __forceinline__ float silu_f32(float a) { return a / (1.0f + expf(-a)); }
 
+// DMOE_SLOT_F16S: sixteen consecutive outputs share a power-of-two exponent
+// e (int8) and each is stored as the fp16 rounding (to nearest even) of
+// v * 2^-e.  e puts the largest finite |v| of the sixteen in [2^14, 2^15), so
+// nothing overflows and every value within 2^28 of that maximum keeps fp16's
+// 11 significant bits; NaN and infinities stay NaN and infinite.  A lane
+// holds four of the sixteen (a matrix-core output row of 16 features is
+// spread over the four lanes c, c + 16, c + 32, c + 48): f16s_group_max
+// combines their maxima, so all 64 lanes of the wave must call it.
+__device__ __forceinline__ float f16s_group_max(const f32x4& v) {
+  float m = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = fabsf(v[i]);
+    m = a <= 3.40282347e38f ? fmaxf(m, a) : m;  // finite values only (NaN compares false)
+  }
+  // lanes i and i ^ 32, then i and i ^ 16: the gfx950 lane-swap
+  // instructions (VALU, no LDS round trip) hand each lane the other half's value
+  const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  m = fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+  const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+}
+
+__device__ __forceinline__ int f16s_exponent(float m) {
+  int ex = 0;
+  if (m > 0.f) (void)frexpf(m, &ex);  // m = f * 2^ex, f in [0.5, 1)
+  return m > 0.f ? min(max(ex - 15, -127), 127) : 0;
+}
+
+__device__ __forceinline__ uint2 f16s_encode(const f32x4& v, int e) {
+  uint32_t b[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) b[i] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(ldexpf(v[i], -e)));
+  return make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
+}
+
+__device__ __forceinline__ f32x4 f16s_decode(uint2 h, int e) {
+  const uint32_t b[4] = {h.x & 0xffffu, h.x >> 16, h.y & 0xffffu, h.y >> 16};
+  f32x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    v[i] = ldexpf(static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(b[i]))), e);
+  return v;
+}
+
+// Bytes of slot outputs [T][k][H] in format f (DMOE_SLOT_F16S: the fp16
+// values, then one exponent byte per sixteen values).
+inline size_t slot_out_bytes(long T, long H, long k, dmoe_slot_format f) {
+  return f == DMOE_SLOT_F16S ? static_cast<size_t>(T * k * H * 2 + T * k * (H / 16))
+                             : static_cast<size_t>(T * k * H * 4);
+}
+
 constexpr int kWave = 64;  // CDNA wavefront width
 
 // ---------------------------------------------------------------------------
@@ -136,7 +188,8 @@ struct FfnArgs {
   const void* ws2;   // packed shared-expert down (or nullptr)
   int T, H, E, I, I_s, k, max_work;
   dmoe_schedule sched;
-  float* slot_out;
+  void* slot_out;
+  dmoe_slot_format slot_fmt;
   float* shared_out;
   void* workspace;  // SwiGLU activations of T*k (+ T) rows, max(I, I_s) wide, storage type
 };
@@ -175,7 +228,7 @@ bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, i
 size_t layer_fused_workspace_bytes(int T, int E, int I, int I_s, int k);
 hipError_t launch_layer_fused(const LayerArgs& a, hipStream_t s);
 
-hipError_t launch_combine(const float* slot_out, const float* w, const float* shared_out,
-                          dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);
+hipError_t launch_combine(const void* slot_out, dmoe_slot_format slot_fmt, const float* w,
+                          const float* shared_out, dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);
 
 }  // namespace dmoe

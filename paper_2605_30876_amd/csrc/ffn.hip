@@ -126,9 +126,34 @@ struct FfnParams {
   int split_rows;                          // > 0: decode kernels take items of <= split_rows rows,
                                            // the tile kernels the larger ones
   bf16_t* hk;                              // SwiGLU activations, chunk-major [ldh/8][R][8]
-  float* slot_out;
+  void* slot_out;                          // [T][k][H], float32 or scaled half (slot_f16s)
   float* shared_out;
+  int slot_f16s;
 };
+
+// Four consecutive outputs j0 .. j0+3 of schedule row r (token row_token[r],
+// slot row_slot[r]) into the slot outputs, float32 or scaled half with the
+// exponent e of their 16-feature group (written by the group's lane j0 % 16
+// == 0).
+__device__ __forceinline__ void store_slot(const FfnParams& p, int r, int j0, const f32x4& v, int e) {
+  const size_t row = static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r];
+  if (p.slot_f16s) {
+    uint16_t* hv = static_cast<uint16_t*>(p.slot_out);
+    *reinterpret_cast<uint2*>(hv + row * p.H + j0) = f16s_encode(v, e);
+    if ((j0 & 15) == 0) {
+      int8_t* ev = reinterpret_cast<int8_t*>(hv + static_cast<size_t>(p.T) * p.k * p.H);
+      ev[row * (p.H >> 4) + (j0 >> 4)] = static_cast<int8_t>(e);
+    }
+  } else {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(p.slot_out) + row * p.H + j0) = v;
+  }
+}
+
+// The shared exponent of the 16-feature group a lane's outputs belong to
+// (scaled-half slot outputs only; 0 otherwise).  All 64 lanes call it.
+__device__ __forceinline__ int slot_exponent(const FfnParams& p, const f32x4& v) {
+  return p.slot_f16s ? f16s_exponent(f16s_group_max(v)) : 0;
+}
 
 using namespace fdev;  // the wave-level operand helpers of ffn_dev.h
 
@@ -237,16 +262,18 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
 #pragma unroll
       for (int ct = 0; ct < NT; ++ct) {
         const int col = p0 + ct * 16 + c;
-        if (col < g.n) {
-          float* dst;
-          if (g.tok) {
-            const int r = g.r0 + col;
-            dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H;
-          } else {
-            dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H;
-          }
+        int ex[RT];
 #pragma unroll
-          for (int r = 0; r < RT; ++r) *reinterpret_cast<f32x4*>(dst + (jt + r) * 16 + 4 * q) = acc[r][ct];
+        for (int r = 0; r < RT; ++r) ex[r] = g.tok ? slot_exponent(p, acc[r][ct]) : 0;  // whole wave
+        if (col < g.n) {
+          if (g.tok) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) store_slot(p, g.r0 + col, (jt + r) * 16 + 4 * q, acc[r][ct], ex[r]);
+          } else {
+            float* dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H;
+#pragma unroll
+            for (int r = 0; r < RT; ++r) *reinterpret_cast<f32x4*>(dst + (jt + r) * 16 + 4 * q) = acc[r][ct];
+          }
         }
       }
     }
@@ -445,8 +472,10 @@ __device__ __forceinline__ void tile_body(const FfnParams& p, const Group& g, in
 #pragma unroll
     for (int ct = 0; ct < kTileTok; ++ct) {
       const int col = ct * 16 + c;
-      if (ct >= nt || col >= g.n) continue;
+      if (ct >= nt) continue;  // uniform
       const f32x4 v = acc[m][ct];
+      const int ex = !kGateUp && g.tok ? slot_exponent(p, v) : 0;  // whole wave, before the row guard
+      if (col >= g.n) continue;
       if (kGateUp) {
         // accumulators: (g_i, g_i+1, u_i, u_i+1) with i = 8*tile + 2q
         const uint32_t h0 = f32_to_bf16(silu_f32(v[0]) * v[2]);
@@ -455,14 +484,10 @@ __device__ __forceinline__ void tile_body(const FfnParams& p, const Group& g, in
         *reinterpret_cast<uint32_t*>(dst) = h0 | (h1 << 16);
       } else {
         const int j = tile * 16 + 4 * q;
-        float* dst;
-        if (g.tok) {
-          const int r = g.r0 + col;
-          dst = p.slot_out + (static_cast<size_t>(p.row_token[r]) * p.k + p.row_slot[r]) * H + j;
-        } else {
-          dst = p.shared_out + static_cast<size_t>(g.t0 + col) * H + j;
-        }
-        *reinterpret_cast<f32x4*>(dst) = v;
+        if (g.tok)
+          store_slot(p, g.r0 + col, j, v, ex);
+        else
+          *reinterpret_cast<f32x4*>(p.shared_out + static_cast<size_t>(g.t0 + col) * H + j) = v;
       }
     }
   }
@@ -754,7 +779,8 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 static_cast<const bf16_t*>(a.ws13),
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
                 a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
-                static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out};
+                static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out,
+                a.slot_fmt == DMOE_SLOT_F16S ? 1 : 0};
     if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
       const hipError_t err = launch_tile_bf16<true>(p, ldh, items, s);
       if (err != hipSuccess) return err;
@@ -787,8 +813,8 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
   if (err != hipSuccess) return err;
   ffn_down_f32_kernel<<<g_dn, kThreads, 0, s>>>(
       static_cast<const float*>(a.w2), static_cast<const float*>(a.ws2), a.sched.n_work, a.sched.work,
-      a.sched.row_token, a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, a.max_work, ldh, hbuf, a.slot_out,
-      a.shared_out);
+      a.sched.row_token, a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, a.max_work, ldh, hbuf,
+      static_cast<float*>(a.slot_out), a.shared_out);  // f32 layers: float32 slot outputs (checked by the API)
   return hipGetLastError();
 }
 

@@ -46,7 +46,7 @@ class MoELayer:
     def __init__(self, H: int, E: int, I: int, I_s: int, k: int, n_blocks: int, block_size: int,
                  dtype: torch.dtype = torch.bfloat16, device="cuda", keep_logits: bool = False,
                  out_dtype: torch.dtype = torch.float32, top_p: float = 0.6, min_coreset: int | None = None,
-                 overlap_shared: bool = False):
+                 overlap_shared: bool = False, slot_format: str | None = None):
         """Routing modes: "block" (block top-k), "token" (token top-k, the
         baseline) and "topp" (Alg. 1: a Top-P coreset per block with mass
         ``top_p`` and at least ``min_coreset`` (default k) experts, each token's
@@ -57,7 +57,11 @@ class MoELayer:
         the results are those of the single dmoe_expert_ffn call up to the
         fp32 summation order of the shared expert.  Off
         by default: replayed from a HIP graph, the two-stream forward of a
-        32-token decode step is slower (53 vs 40 us) than the one-stream one."""
+        32-token decode step is slower (53 vs 40 us) than the one-stream one.
+
+        slot_format: storage of the per-slot expert outputs between the FFN
+        and the combine, "f16s" (scaled half, the default for bf16 layers:
+        half the bytes) or "f32" (the only one for fp32 layers)."""
         self.H, self.E, self.I, self.I_s, self.k = H, E, I, I_s, k
         self.NB, self.bs = n_blocks, block_size
         self.T = T = n_blocks * block_size
@@ -83,7 +87,16 @@ class MoELayer:
                           "token": lib.dmoe_schedule_max_work(T, 1, k, E)}
         self._max_work["topp"] = self._max_work["token"]
         self.sched = lib.Schedule.empty(E, T * k, device, max(self._max_work.values()))
-        self.slot_out = torch.empty((T, k, H), **f32)
+        if slot_format is None:
+            slot_format = "f32" if dtype == torch.float32 else "f16s"
+        if slot_format == "f16s":
+            nb = lib.dmoe_slot_out_bytes(T, H, k, lib.DMOE_SLOT_F16S)
+            self.slot_out = torch.empty((nb,), dtype=torch.uint8, device=device)
+        elif slot_format == "f32":
+            self.slot_out = torch.empty((T, k, H), **f32)
+        else:
+            raise ValueError(f"slot_format must be 'f16s' or 'f32', not {slot_format!r}")
+        self.slot_format = slot_format
         self.shared_out = torch.empty((T, H), **f32) if I_s > 0 else None
         dt = lib.DMOE_F32 if dtype == torch.float32 else lib.DMOE_BF16
         rbytes = lib.dmoe_router_workspace_size(T, H, E, dt)

@@ -23,6 +23,7 @@ LIB_PATH = os.path.join(_PKG, "libdmoe.so")
 
 DMOE_OK, DMOE_ERR_INVALID_ARG, DMOE_ERR_UNSUPPORTED, DMOE_ERR_HIP = 0, -1, -2, -3
 DMOE_F32, DMOE_BF16 = 0, 1
+DMOE_SLOT_F32, DMOE_SLOT_F16S = 0, 1  # slot-output storage (dmoe_slot_format)
 
 STATUS_NAMES = {DMOE_OK: "DMOE_OK", DMOE_ERR_INVALID_ARG: "DMOE_ERR_INVALID_ARG",
                 DMOE_ERR_UNSUPPORTED: "DMOE_ERR_UNSUPPORTED", DMOE_ERR_HIP: "DMOE_ERR_HIP"}
@@ -32,7 +33,7 @@ EXPORTS = ("dmoe_router_workspace_size", "dmoe_router_logits", "dmoe_block_aggre
            "dmoe_block_topp_route", "dmoe_build_expert_schedule", "dmoe_schedule_max_work",
            "dmoe_schedule_scratch_ints", "dmoe_route_block",
            "dmoe_route_token", "dmoe_route_topp", "dmoe_pack_activations", "dmoe_pack_expert_weights", "dmoe_ffn_workspace_size",
-           "dmoe_expert_ffn", "dmoe_expert_ffn_noalloc", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
+           "dmoe_slot_out_bytes", "dmoe_expert_ffn", "dmoe_expert_ffn_noalloc", "dmoe_shared_ffn_workspace_size", "dmoe_shared_expert_ffn", "dmoe_combine",
            "dmoe_moe_forward_workspace_size", "dmoe_moe_forward_fused", "dmoe_moe_forward", "dmoe_last_error",
            "dmoe_version")
 
@@ -61,7 +62,8 @@ class dmoe_layer_buffers(ctypes.Structure):
     _fields_ = [("logits", ctypes.c_void_p), ("probs", ctypes.c_void_p), ("x_chunked", ctypes.c_void_p),
                 ("block_scores", ctypes.c_void_p), ("experts", ctypes.c_void_p), ("combine_w", ctypes.c_void_p),
                 ("gap", ctypes.c_void_p), ("coreset", ctypes.c_void_p), ("coreset_size", ctypes.c_void_p),
-                ("sched", dmoe_schedule), ("slot_out", ctypes.c_void_p), ("shared_out", ctypes.c_void_p),
+                ("sched", dmoe_schedule), ("slot_out", ctypes.c_void_p), ("slot_fmt", ctypes.c_int),
+                ("shared_out", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t)]
 
 
@@ -85,11 +87,12 @@ _SIGS = {
     "dmoe_pack_activations": ([_P, _I, _I, _I, _P, _P], _I),
     "dmoe_pack_expert_weights": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _P], _I),
     "dmoe_ffn_workspace_size": ([_I, _I, _I, _I, _I], _S),
-    "dmoe_expert_ffn": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _P, _S, _P], _I),
-    "dmoe_expert_ffn_noalloc": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _P, _P], _I),
+    "dmoe_slot_out_bytes": ([_I, _I, _I, _I], _S),
+    "dmoe_expert_ffn": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _I, _P, _P, _S, _P], _I),
+    "dmoe_expert_ffn_noalloc": ([_P] * 6 + [_I] * 8 + [dmoe_schedule, _P, _I, _P, _P], _I),
     "dmoe_shared_ffn_workspace_size": ([_I, _I, _I], _S),
     "dmoe_shared_expert_ffn": ([_P, _P, _P, _I, _I, _I, _I, _P, _P, _S, _P], _I),
-    "dmoe_combine": ([_P, _P, _P, _I, _I, _I, _I, _P, _P], _I),
+    "dmoe_combine": ([_P, _I, _P, _P, _I, _I, _I, _I, _P, _P], _I),
     "dmoe_moe_forward_workspace_size": ([_I] * 7 + [_I], _S),
     "dmoe_moe_forward_fused": ([_I] * 9, _I),
     "dmoe_moe_forward": ([_P] * 7 + [_I] * 8 + [_I, ctypes.c_float, _I, ctypes.POINTER(dmoe_layer_buffers), _P, _I, _P],
@@ -274,12 +277,27 @@ def dmoe_shared_expert_ffn(x_chunked, ws13, ws2, T, H, I_s, shared_out, workspac
                                          workspace.numel() * workspace.element_size(), stream_handle(stream)))
 
 
+def slot_format_code(slot_out) -> int:
+    """The slot-output format a buffer holds: float32 tensors are
+    DMOE_SLOT_F32, byte tensors (dmoe_slot_out_bytes long) DMOE_SLOT_F16S."""
+    if slot_out.dtype == torch.float32:
+        return DMOE_SLOT_F32
+    if slot_out.dtype == torch.uint8:
+        return DMOE_SLOT_F16S
+    raise TypeError(f"slot_out must be float32 or uint8, got {slot_out.dtype}")
+
+
+def dmoe_slot_out_bytes(T, H, k, fmt: int) -> int:
+    return int(load().dmoe_slot_out_bytes(T, H, k, fmt))
+
+
 def dmoe_expert_ffn(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k, max_work, sched: Schedule,
                     slot_out, shared_out, workspace, stream=None):
-    """x: the row-major hidden states (or None); gathered token rows are read from it."""
+    """x: the row-major hidden states (or None); gathered token rows are read from it.
+    slot_out: float32 [T, k, H] or a uint8 buffer of scaled-half slot outputs."""
     _check(load().dmoe_expert_ffn(ptr(x_chunked), ptr(x), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
                                   dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
-                                  ptr(slot_out), ptr(shared_out), ptr(workspace),
+                                  ptr(slot_out), slot_format_code(slot_out), ptr(shared_out), ptr(workspace),
                                   workspace.numel() * workspace.element_size(), stream_handle(stream)))
 
 
@@ -291,12 +309,13 @@ def dmoe_expert_ffn_noalloc(x_chunked, x, w13, w2, ws13, ws2, T, H, E, I, I_s, k
     """dmoe_expert_ffn with the library's device scratch instead of a workspace."""
     _check(load().dmoe_expert_ffn_noalloc(ptr(x_chunked), ptr(x), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
                                           dtype_code(x_chunked), T, H, E, I, I_s, k, max_work, sched.as_c(),
-                                          ptr(slot_out), ptr(shared_out), stream_handle(stream)))
+                                          ptr(slot_out), slot_format_code(slot_out), ptr(shared_out),
+                                          stream_handle(stream)))
 
 
 def dmoe_combine(slot_out, combine_w, shared_out, T, H, k, y, stream=None):
-    _check(load().dmoe_combine(ptr(slot_out), ptr(combine_w), ptr(shared_out), dtype_code(y), T, H,
-                               k, ptr(y), stream_handle(stream)))
+    _check(load().dmoe_combine(ptr(slot_out), slot_format_code(slot_out), ptr(combine_w), ptr(shared_out),
+                               dtype_code(y), T, H, k, ptr(y), stream_handle(stream)))
 
 
 def dmoe_moe_forward_workspace_size(n_blocks, block_size, H, E, I, I_s, k, dt) -> int:
@@ -315,7 +334,7 @@ def dmoe_moe_forward(x, w_router, bias, w13, w2, ws13, ws2, n_blocks, block_size
     buffers are gathered into a dmoe_layer_buffers (a host struct)."""
     buf = dmoe_layer_buffers(ptr(logits), ptr(probs), ptr(x_chunked), ptr(block_scores), ptr(experts),
                              ptr(combine_w), ptr(gap), ptr(coreset), ptr(coreset_size), sched.as_c(), ptr(slot_out),
-                             ptr(shared_out), ptr(workspace), _nbytes(workspace))
+                             slot_format_code(slot_out), ptr(shared_out), ptr(workspace), _nbytes(workspace))
     _check(load().dmoe_moe_forward(ptr(x), ptr(w_router), ptr(bias), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
                                    dtype_code(x), n_blocks, block_size, H, E, I, I_s, k, ROUTING[routing],
                                    float(top_p), min_coreset, ctypes.byref(buf), ptr(y), dtype_code(y),

@@ -22,6 +22,30 @@ F32_TOL = 1e-4    # ... <= 1e-4 * RMS(y_ref) for the fp32 layer
 PROB_TOL = 1e-6   # router probabilities, combine weights, block scores, gaps (absolute)
 
 
+SLOT_POISON = 0x7E  # as bytes of a scaled-half slot buffer: fp16 0x7E7E is a NaN
+
+
+def poisoned(buf):
+    """A buffer shaped like ``buf`` filled with NaN (float32) or with the
+    byte pattern whose fp16 values are NaN (scaled-half slot outputs)."""
+    if buf.dtype == torch.uint8:
+        return torch.full_like(buf, SLOT_POISON)
+    return torch.full_like(buf, float("nan"))
+
+
+def slot_values(buf, T, k, H):
+    """Slot outputs [T, k, H] as float32 on the host.  A uint8 buffer holds
+    the documented scaled-half layout: fp16 values [T][k][H], then one int8
+    exponent per sixteen values; value = half * 2^exponent."""
+    b = buf.detach().to("cpu")
+    if b.dtype == torch.float32:
+        return b.reshape(T, k, H)
+    n = T * k * H
+    half = b[:2 * n].view(torch.float16).float().reshape(T, k, H)
+    ex = b[2 * n:2 * n + n // 16].view(torch.int8).to(torch.int32).reshape(T, k, H // 16)
+    return torch.ldexp(half, ex.repeat_interleave(16, dim=2).float())
+
+
 def tol_for(cfg) -> float:
     return F32_TOL if cfg.dtype == "f32" else BF16_TOL
 

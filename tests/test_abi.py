@@ -114,10 +114,11 @@ def test_schedule_validation(L, buf):
 
 def _ffn(L, p, **over):
     a = dict(x=p, xr=p, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512, k=8,
-             max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, shared=p, ws=p, ws_bytes=1 << 30)
+             max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, fmt=lib.DMOE_SLOT_F16S, shared=p,
+             ws=p, ws_bytes=1 << 30)
     a.update(over)
     return status(L, "dmoe_expert_ffn", a["x"], a["xr"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"], a["T"],
-                  a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"],
+                  a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"], a["fmt"],
                   a["shared"], a["ws"], a["ws_bytes"], None)
 
 
@@ -140,6 +141,9 @@ def test_ffn_validation(L, buf):
     st, msg = _ffn(L, p, ws_bytes=100)
     assert st == INV and "workspace" in msg
     assert _ffn(L, p, slot=p + 4)[0] == INV
+    assert _ffn(L, p, fmt=2)[0] == INV               # unknown slot format
+    st, msg = _ffn(L, p, dt=lib.DMOE_F32, H=96, I=40, I_s=24)
+    assert st == UNS and "scaled-half" in msg          # scaled-half slots need bf16 experts
     assert _ffn(L, p, w2=p + 8)[0] == INV
     assert _ffn(L, p, sched=lib.dmoe_schedule(p, None, p, p, p, p, p))[0] == INV
     assert _ffn(L, p, H=2004)[0] == INV              # not a whole number of 16-byte chunks
@@ -182,11 +186,24 @@ def test_pack_expert_weights_validation(L, buf):
 def test_combine_validation(L, buf):
     _, p = buf
     f = "dmoe_combine"
-    assert status(L, f, None, p, None, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, f, p, p, None, 1, 32, 2046, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, f, p, p, None, 1, 32, 2048, 65, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, f, p, p, None, 9, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
-    assert status(L, f, p, p, p + 4, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    S16 = lib.DMOE_SLOT_F16S
+    assert status(L, f, None, S16, p, None, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, S16, p, None, 1, 32, 2046, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, S16, p, None, 1, 32, 2048, 65, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, S16, p, None, 9, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, S16, p, p + 4, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, 5, p, None, 1, 32, 2048, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+    assert status(L, f, p, S16, p, None, 1, 32, 2040, 8, p, None)[0] == lib.DMOE_ERR_INVALID_ARG
+
+
+def test_slot_out_bytes():
+    # scaled half: 2 bytes per value plus one exponent byte per sixteen values
+    assert lib.dmoe_slot_out_bytes(32, 2048, 8, lib.DMOE_SLOT_F16S) == 32 * 8 * 2048 * 2 + 32 * 8 * 128
+    assert lib.dmoe_slot_out_bytes(32, 2048, 8, lib.DMOE_SLOT_F32) == 32 * 8 * 2048 * 4
+    assert lib.dmoe_slot_out_bytes(5, 96, 3, lib.DMOE_SLOT_F32) == 5 * 3 * 96 * 4
+    assert lib.dmoe_slot_out_bytes(0, 2048, 8, lib.DMOE_SLOT_F16S) == 0
+    assert lib.dmoe_slot_out_bytes(32, 2040, 8, lib.DMOE_SLOT_F16S) == 0  # H % 16 != 0
+    assert lib.dmoe_slot_out_bytes(32, 2048, 8, 4) == 0
 
 
 def _route(L, p, routing, **over):
@@ -314,7 +331,8 @@ def test_router_workspace_size():
     # decode step: the hidden dimension is split, one fp32 partial plane per slice
     n = lib.dmoe_router_workspace_size(32, 2048, 256, lib.DMOE_BF16)
     assert n == 4 * 32 * 256 * 4  # 4 partial logit planes
-    assert lib.dmoe_router_workspace_size(4096, 2048, 256, lib.DMOE_BF16) == 0
+    # 4096 tokens: 128-token x 64-expert tiles in two slices (256 workgroups)
+    assert lib.dmoe_router_workspace_size(4096, 2048, 256, lib.DMOE_BF16) == 2 * 4096 * 256 * 4
     assert lib.dmoe_router_workspace_size(8, 256, 16, lib.DMOE_F32) == 0
     assert lib.dmoe_router_workspace_size(0, 2048, 256, lib.DMOE_BF16) == 0
 
@@ -328,7 +346,7 @@ def test_workspace_size():
 
 def test_last_error_cleared_per_thread(L, buf):
     _, p = buf
-    L.dmoe_combine(None, p, None, 1, 32, 2048, 8, p, None)
+    L.dmoe_combine(None, lib.DMOE_SLOT_F32, p, None, 1, 32, 2048, 8, p, None)
     assert L.dmoe_last_error().decode().startswith("dmoe_combine")
 
 
@@ -343,10 +361,10 @@ def test_schedule_scratch_ints():
 
 def _ffn_noalloc(L, p, **kw):
     a = dict(x=p, xr=None, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, T=32, H=2048, E=256, I=512, I_s=512,
-             k=8, max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, shared=p)
+             k=8, max_work=8, sched=lib.dmoe_schedule(p, p, p, p, p, p, p), slot=p, fmt=lib.DMOE_SLOT_F16S, shared=p)
     a.update(kw)
     return status(L, "dmoe_expert_ffn_noalloc", a["x"], a["xr"], a["w13"], a["w2"], a["ws13"], a["ws2"], a["dt"],
-                  a["T"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"],
+                  a["T"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["max_work"], a["sched"], a["slot"], a["fmt"],
                   a["shared"], None)
 
 
@@ -371,11 +389,12 @@ def test_ffn_noalloc_validation(L, buf):
 def _moe(L, p, ws_bytes=1 << 30, **kw):
     a = dict(x=p, wr=p, bias=None, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, NB=1, bs=32, H=2048, E=256, I=512,
              I_s=512, k=8, routing=lib.DMOE_ROUTE_BLOCK, top_p=0.6, min_c=8, y=p, y_dt=lib.DMOE_F32)
-    bufkw = {f: kw.pop(f) for f in list(kw) if f in ("probs", "coreset", "shared_out", "workspace")}
+    bufkw = {f: kw.pop(f) for f in list(kw) if f in ("probs", "coreset", "shared_out", "workspace", "slot_fmt")}
     a.update(kw)
     sched = lib.dmoe_schedule(p, p, p, p, p, p, p, None)
     buf = lib.dmoe_layer_buffers(None, bufkw.get("probs", p), p, None, p, p, None, bufkw.get("coreset", None), None,
-                                 sched, p, bufkw.get("shared_out", p), bufkw.get("workspace", p), ws_bytes)
+                                 sched, p, bufkw.get("slot_fmt", lib.DMOE_SLOT_F16S), bufkw.get("shared_out", p),
+                                 bufkw.get("workspace", p), ws_bytes)
     return status(L, "dmoe_moe_forward", a["x"], a["wr"], a["bias"], a["w13"], a["w2"], a["ws13"], a["ws2"],
                   a["dt"], a["NB"], a["bs"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["routing"], a["top_p"],
                   a["min_c"], ctypes.byref(buf), a["y"], a["y_dt"], None)
@@ -396,6 +415,8 @@ def test_moe_forward_validation(L, buf):
     assert _moe(L, p, k=0)[0] == INV
     assert _moe(L, p, I=500)[0] == UNS
     assert _moe(L, p, E=600)[0] == UNS
+    assert _moe(L, p, slot_fmt=3)[0] == INV
+    assert _moe(L, p, dt=lib.DMOE_F32, H=256, I=128, I_s=128)[0] == UNS  # scaled-half slots in an fp32 layer
     st = L.dmoe_moe_forward(p, p, None, p, p, p, p, lib.DMOE_BF16, 1, 32, 2048, 256, 512, 512, 8, 0, 0.6, 8, None, p,
                             lib.DMOE_F32, None)
     assert st == INV  # buf is NULL
