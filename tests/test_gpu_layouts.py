@@ -90,7 +90,10 @@ def test_pack_activations(gpu_lib, dtype, T, H):
 
 
 @pytest.mark.parametrize("dtype,T,H,E", [(torch.bfloat16, 72, 512, 64), (torch.bfloat16, 32, 2048, 256),
-                                         (torch.bfloat16, 5, 256, 48), (torch.float32, 15, 96, 12)])
+                                         (torch.bfloat16, 5, 256, 48), (torch.float32, 15, 96, 12),
+                                         # LDS-staged router tiles (T >= 256), ragged tails
+                                         (torch.bfloat16, 300, 768, 64), (torch.bfloat16, 1500, 512, 200),
+                                         (torch.bfloat16, 4096, 2048, 256)])
 def test_router_writes_chunked_x(gpu_lib, dtype, T, H, E):
     """The router's x_chunked side output equals dmoe_pack_activations."""
     g = torch.Generator().manual_seed(T * H + E)
@@ -106,3 +109,23 @@ def test_router_writes_chunked_x(gpu_lib, dtype, T, H, E):
     torch.cuda.synchronize()
     assert torch.equal(xc.cpu(), ref.cpu())
     assert torch.equal(xc.cpu(), _chunked(x.cpu(), 8 if dtype == torch.bfloat16 else 4))
+
+
+@pytest.mark.parametrize("T,H,E", [(300, 768, 64), (1500, 512, 200), (4096, 2048, 256), (513, 1024, 40)])
+def test_router_tiles_with_and_without_workspace(gpu_lib, T, H, E):
+    """Router tiles of larger forwards: probabilities with the workspace (the
+    hidden dimension in slices) and without it (one slice, in place) both
+    match the oracle within 1e-6."""
+    import oracle as O
+    from parity import PROB_TOL
+    g = torch.Generator().manual_seed(T + H + E)
+    x = torch.randn((T, H), generator=g).to(torch.bfloat16)
+    w = (0.02 * torch.randn((E, H), generator=g)).to(torch.bfloat16)
+    ref = O.softmax_rows(O.router_logits(x.float().numpy(), w.float().numpy(), None))
+    nbytes = lib.dmoe_router_workspace_size(T, H, E, lib.DMOE_BF16)
+    for ws in (torch.empty((max(nbytes, 16),), dtype=torch.uint8, device="cuda"), None):
+        probs = torch.full((T, E), float("nan"), device="cuda")
+        lib.dmoe_router_logits(x.cuda(), w.cuda(), None, T, H, E, None, probs, None, ws)
+        torch.cuda.synchronize()
+        err = float((probs.cpu().double() - torch.from_numpy(ref).double()).abs().max())
+        assert err <= PROB_TOL, (ws is None, err)
