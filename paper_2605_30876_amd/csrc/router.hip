@@ -148,7 +148,7 @@ __global__ __launch_bounds__(256) void router_tile_bf16_kernel(
   constexpr int NTw = TTt / WT, NEw = TEt / WE;         // output tiles per wave
   constexpr int XP = TT * 8 / 256, WP = TE * 8 / 256;   // 16-byte pieces per thread per stage
   static_assert(NTw * WT == TTt && NEw * WE == TEt && XP >= 1 && WP >= 1, "tile shape");
-  static_assert(RING == 4 || RING == 6 || RING == 8, "register ring");
+  static_assert(RING == 4 || RING == 8, "register ring");
   __shared__ __align__(16) bf16_t lx[2][TT][kLdsRow];
   __shared__ __align__(16) bf16_t lw[2][TE][kLdsRow];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, q = lane >> 4, c = lane & 15;
@@ -231,11 +231,9 @@ __global__ __launch_bounds__(256) void router_tile_bf16_kernel(
     if (st + 1 < nst) run_stage(std::integral_constant<int, 1>{}, st + 1);
     if (st + 2 < nst) run_stage(std::integral_constant<int, 2>{}, st + 2);
     if (st + 3 < nst) run_stage(std::integral_constant<int, 3>{}, st + 3);
-    if constexpr (RING > 4) {
+    if constexpr (RING == 8) {
       if (st + 4 < nst) run_stage(std::integral_constant<int, 4 % RING>{}, st + 4);
       if (st + 5 < nst) run_stage(std::integral_constant<int, 5 % RING>{}, st + 5);
-    }
-    if constexpr (RING > 6) {
       if (st + 6 < nst) run_stage(std::integral_constant<int, 6 % RING>{}, st + 6);
       if (st + 7 < nst) run_stage(std::integral_constant<int, 7 % RING>{}, st + 7);
     }
