@@ -55,8 +55,11 @@ def cpu(t):
 
 
 def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: list, what: str):
-    """Per group: the oracle's own top-k list, or (near-tie) the oracle-valid
-    set that the GPU picked, ranked by the oracle's scores."""
+    """Per group: the oracle's own top-k set in the GPU's slot order, or
+    (near-tie) the oracle-valid set that the GPU picked, ranked by the
+    oracle's scores.  The slot order inside the set is checked separately
+    (descending oracle score up to NEAR_TIE): two selected experts whose
+    scores lie within the tolerance may take either slot."""
     out = np.zeros((scores.shape[0], k), dtype=np.int32)
     for g in range(scores.shape[0]):
         idx, gap = O.topk(scores[g], k)
@@ -64,7 +67,9 @@ def accepted_selection(scores: np.ndarray, gpu_sel: np.ndarray, k: int, log: lis
             assert set(gpu_sel[g].tolist()) == set(idx.tolist()), (
                 f"{what} group {g}: GPU set {sorted(gpu_sel[g].tolist())} != oracle {sorted(idx.tolist())}"
                 f" (gap {gap:.3g})")
-            out[g] = idx
+            sc = scores[g][gpu_sel[g]]
+            assert np.all(sc[:-1] >= sc[1:] - O.NEAR_TIE), f"{what} group {g}: slots not in descending score order"
+            out[g] = gpu_sel[g]
         else:
             gs = frozenset(gpu_sel[g].tolist())
             assert O.valid_topk_set(scores[g], gpu_sel[g].tolist(), k), (

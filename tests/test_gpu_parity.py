@@ -68,7 +68,12 @@ def test_tile_kernel_parity(gpu_lib, name, routing):
 # shape reaches one workgroup per CU (300 tokens, 64 experts).
 ROUTER_TILE = {"router_t1500_e200": dict(H=512, E=200, I=128, I_s=128, k=8, NB=60, bs=25),
                "router_t2100_e200": dict(H=512, E=200, I=128, I_s=0, k=4, NB=70, bs=30),
-               "router_t300_e64": dict(H=768, E=64, I=128, I_s=128, k=8, NB=12, bs=25)}
+               "router_t300_e64": dict(H=768, E=64, I=128, I_s=128, k=8, NB=12, bs=25),
+               # the largest expert count the schedule takes
+               "router_t260_e512": dict(H=256, E=512, I=128, I_s=128, k=8, NB=10, bs=26),
+               # k = E = 64: every expert in every block, 16384 schedule rows placed
+               # one workgroup per block
+               "router_t256_k64": dict(H=256, E=64, I=128, I_s=128, k=64, NB=4, bs=64)}
 
 
 @pytest.mark.parametrize("routing", ["block", "token"])
