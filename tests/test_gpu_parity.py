@@ -234,3 +234,17 @@ def test_error_status_on_gpu(gpu_lib):
     with pytest.raises(lib.DmoeError) as ei:
         lib.dmoe_token_topk(layer.probs, cfg.T, cfg.E, cfg.E + 1, layer.token_experts, layer.combine_w, None)
     assert ei.value.status == lib.DMOE_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("routing", ["block", "token"])
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_parity_more_seeds(gpu_lib, name, routing, seed):
+    """Full size on two more seeds (every token checked)."""
+    cfg = get_config(name)
+    _say("case", name, routing, "seed", seed)
+    d = make_inputs(cfg, seed=seed, device="cuda")
+    rep = run_and_check(cfg, d, routing, _layer(cfg), check_determinism=False)
+    _say("  ", {k: v for k, v in rep.items() if k != "near_ties"}, "near_ties:", len(rep["near_ties"]))
+    del d
+    torch.cuda.empty_cache()
