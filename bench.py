@@ -235,6 +235,18 @@ def measure_modes(torch, cfg, layers, modes, steps, warmup, use_graph, ffn_only=
     return results
 
 
+def mall_resident(torch, layers, routing, use_graph, steps=256):
+    """One layer replayed over and over: its experts (57.9 MB for the decode
+    layer's block routing) stay in the 256 MB memory-side cache, so this is
+    the step's floor with warm weights, not an HBM figure."""
+    x, w, m = layers[0]
+    r = Runner(torch, 1, lambda _i: m.forward(x, w, routing), use_graph)
+    r.time(32)
+    wall, _ = r.time(steps)
+    r.close()
+    return round(wall / steps * 1e6, 3)
+
+
 def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
     """A decode step of STEP_LAYERS chained MoE layers (the step's input
     plus layer l's output is layer l+1's input), timed per mode; the adds
@@ -346,6 +358,11 @@ def main():
     if args.ffn_only:
         print(json.dumps({"ffn_only": results, "config": cfg.name, "layers": NL, "steps": steps}))
         return 0
+    if "block" in results:
+        # labelled separately: weights served from the memory-side cache
+        results["block"]["mall_resident_us_per_step"] = mall_resident(torch, layers, "block", not args.no_graph)
+        log(f"[bench] {cfg.name} block, one layer replayed (weights cache-resident): "
+            f"{results['block']['mall_resident_us_per_step']} us/step")
 
     chain = None
     if not args.no_extras and NL >= STEP_LAYERS:
