@@ -50,7 +50,7 @@ def cmd_trace(a):
     rows = list(c.execute("select name, count(*), sum(duration), avg(duration), min(duration), max(duration) "
                           "from kernels group by name order by sum(duration) desc"))
     total = sum(r[2] for r in rows)
-    print(f"# {a.title}\n\nCommand (from the repository root on the GPU box):\n\n```\n{a.cmd}\n```\n")
+    print(f"# {a.title}\n\nCommand (from the repository root on the MI355X host):\n\n```\n{a.cmd}\n```\n")
     print("Durations in microseconds, from the kernel trace (`rocprofv3 --kernel-trace --stats`).\n")
     print("| kernel | calls | avg | min | max | total | % GPU time |\n|---|---|---|---|---|---|---|")
     for n, calls, tot, avg, mn, mx in rows:
@@ -134,7 +134,7 @@ def cmd_traffic(a):
     w_scale = a.copy_bytes / copy_write
     print(f"# HBM traffic per MoE-layer forward, {a.config}\n")
     if a.cmd:
-        print(f"Commands (from the repository root on the GPU box):\n\n```\n{a.cmd}\n```\n")
+        print(f"Commands (from the repository root on the MI355X host):\n\n```\n{a.cmd}\n```\n")
     print(f"FETCH_SIZE and WRITE_SIZE (KiB per dispatch, two runs) are scaled by what they read for a plain copy "
           f"of {a.copy_bytes} bytes: reads x{f_scale:.4f}, writes x{w_scale:.4f}. A group's bytes per launch are "
           "the sum over its kernels of the mean per dispatch. Algorithmic bytes: the selected experts' and the "
@@ -209,7 +209,7 @@ def cmd_mfma(a):
 def cmd_sweep(a):
     with open(a.json) as fh:
         sw = json.loads(fh.read().strip().splitlines()[-1])["sweep"]
-    print(f"# Sweeps on the {sw['workload']}\n\nCommand (from the repository root on the GPU box):\n\n"
+    print(f"# Sweeps on the {sw['workload']}\n\nCommand (from the repository root on the MI355X host):\n\n"
           f"```\n{a.cmd}\n```\n")
     print(f"Every time is a HIP-graph replay over {sw['layers_rotated']} layers with distinct weights "
           f"(cache-cold expert streams), {sw['steps_per_point']} steps per point, bf16.\n")
@@ -237,7 +237,7 @@ def cmd_sweep(a):
 
 def cmd_configs(a):
     print("# Bench, every configuration (one MI355X)\n\nCommand, per configuration (from the repository root on the "
-          f"GPU box):\n\n```\n{a.cmd}\n```\n")
+          f"MI355X host):\n\n```\n{a.cmd}\n```\n")
     print("Graph-replayed steps rotating over distinct layers (experts streamed from HBM, not the 256 MB "
           "memory-side cache). `bytes` = algorithmic HBM bytes per step (selected experts once + shared expert + "
           "router + x in/y out); GB/s = bytes / wall time. Top-P routing uses p = 0.6.\n")
