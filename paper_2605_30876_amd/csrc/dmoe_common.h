@@ -127,13 +127,16 @@ hipError_t launch_router_partials(const void* x, const void* w, dmoe_dtype dt, i
                                   hipStream_t s, float** part, int* S);
 hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, float* scores,
                              int32_t* experts, float* w, float* gap, hipStream_t s);
+// raw: w holds the selected probabilities themselves, not renormalised
+// (the Top-P coreset's input; its final selection overwrites them).
 hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* experts, float* w,
-                             float* gap, hipStream_t s);
+                             float* gap, hipStream_t s, bool raw = false);
 // Softmax of the router's S partial logit planes and token top-k in one
 // launch (E <= 512); probs, weights and selections as the two-step chain.
 bool softmax_token_topk_fits(int E);
 hipError_t launch_softmax_token_topk(const float* part, int S, const float* bias, int T, int E, int k, float* probs,
-                                     float* logits, int32_t* experts, float* w, float* gap, hipStream_t s);
+                                     float* logits, int32_t* experts, float* w, float* gap, hipStream_t s,
+                                     bool raw = false);
 hipError_t launch_schedule(const int32_t* experts, int n_groups, int gs, int k, int E,
                            dmoe_schedule sched, hipStream_t s);
 hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, float p, int min_c,

@@ -205,7 +205,7 @@ static hipError_t launch_route_topp(const RouteArgs& a, dmoe_dtype dt, hipStream
                                  &part, &S);
     if (err != hipSuccess) return err;
     err = launch_softmax_token_topk(part, S, a.bias, a.T, a.E, a.k, a.probs, a.logits, a.experts, a.combine_w,
-                                    nullptr, s);
+                                    nullptr, s, true);  // the selected probabilities, for the coreset
     own_done = true;
   } else {
     err = launch_router(a.x, a.w, a.bias, dt, a.T, a.H, a.E, a.logits, a.probs, a.x_chunked, a.workspace,

@@ -128,7 +128,7 @@ __global__ __launch_bounds__(256) void token_topk_kernel(const float* __restrict
                                                          int E, int k,
                                                          int32_t* __restrict__ experts,
                                                          float* __restrict__ w,
-                                                         float* __restrict__ gap) {
+                                                         float* __restrict__ gap, int raw) {
   extern __shared__ float rows[];
   __shared__ int sel[4][kMaxK + 1];
   __shared__ float selv[4][kMaxK + 1];
@@ -161,7 +161,8 @@ __global__ __launch_bounds__(256) void token_topk_kernel(const float* __restrict
   __syncthreads();
   if (live && lane < k) {
     experts[static_cast<size_t>(t) * k + lane] = sel[wave][lane];
-    w[static_cast<size_t>(t) * k + lane] = selv[wave][lane] / denom_s[wave];
+    // raw: the staged row's own value (the stored probability, bit for bit)
+    w[static_cast<size_t>(t) * k + lane] = raw ? row[sel[wave][lane]] : selv[wave][lane] / denom_s[wave];
   }
 }
 
@@ -175,7 +176,8 @@ __global__ __launch_bounds__(256) void softmax_token_topk_kernel(const float* pa
                                                                  const float* __restrict__ bias, int T, int E, int k,
                                                                  float* probs, float* __restrict__ logits,
                                                                  int32_t* __restrict__ experts,
-                                                                 float* __restrict__ w, float* __restrict__ gap) {
+                                                                 float* __restrict__ w, float* __restrict__ gap,
+                                                                 int raw) {
   extern __shared__ float rows[];
   __shared__ int sel[4][kMaxK + 1];
   __shared__ float selv[4][kMaxK + 1];
@@ -211,7 +213,8 @@ __global__ __launch_bounds__(256) void softmax_token_topk_kernel(const float* pa
   __syncthreads();
   if (live && lane < k) {
     experts[static_cast<size_t>(t) * k + lane] = sel[wave][lane];
-    w[static_cast<size_t>(t) * k + lane] = selv[wave][lane] / denom_s[wave];
+    // raw: the staged row's own value (the stored probability, bit for bit)
+    w[static_cast<size_t>(t) * k + lane] = raw ? row[sel[wave][lane]] : selv[wave][lane] / denom_s[wave];
   }
 }
 
@@ -220,13 +223,16 @@ __global__ __launch_bounds__(256) void softmax_token_topk_kernel(const float* pa
 bool softmax_token_topk_fits(int E) { return E <= dev::kRegSoftmaxMaxE && E <= kRadixMaxE; }
 
 hipError_t launch_softmax_token_topk(const float* part, int S, const float* bias, int T, int E, int k, float* probs,
-                                     float* logits, int32_t* experts, float* w, float* gap, hipStream_t s) {
+                                     float* logits, int32_t* experts, float* w, float* gap, hipStream_t s,
+                                     bool raw) {
   const unsigned blocks = (T + 3) / 4;
   const size_t lds = static_cast<size_t>(4) * E * sizeof(float);
   if (E <= 256)
-    softmax_token_topk_kernel<1><<<blocks, 256, lds, s>>>(part, S, bias, T, E, k, probs, logits, experts, w, gap);
+    softmax_token_topk_kernel<1><<<blocks, 256, lds, s>>>(part, S, bias, T, E, k, probs, logits, experts, w, gap,
+                                                           raw ? 1 : 0);
   else
-    softmax_token_topk_kernel<2><<<blocks, 256, lds, s>>>(part, S, bias, T, E, k, probs, logits, experts, w, gap);
+    softmax_token_topk_kernel<2><<<blocks, 256, lds, s>>>(part, S, bias, T, E, k, probs, logits, experts, w, gap,
+                                                           raw ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -238,9 +244,9 @@ hipError_t launch_block_topk(const float* probs, int nb, int bs, int E, int k, f
 }
 
 hipError_t launch_token_topk(const float* probs, int T, int E, int k, int32_t* experts, float* w,
-                             float* gap, hipStream_t s) {
+                             float* gap, hipStream_t s, bool raw) {
   token_topk_kernel<<<(T + 3) / 4, 256, static_cast<size_t>(4) * E * sizeof(float), s>>>(
-      probs, T, E, k, experts, w, gap);
+      probs, T, E, k, experts, w, gap, raw ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -19,89 +19,140 @@ namespace dmoe {
 namespace {
 
 constexpr int kCoreThreads = 512;
-constexpr size_t kCoreLdsBudget = 64 * 1024 - 256;  // dynamic LDS bytes (the kernel has no static LDS)
+constexpr int kCoreWaves = kCoreThreads / kWave;
+constexpr int kCoreCols = 2;        // experts per thread (E <= 1024)
+constexpr int kCoreTokChunk = 32;   // tokens per masked-sum chunk, at most
+constexpr int kCoreMWords = 8192;   // LDS words of a chunk's masked probability rows (32 KiB)
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 // Dynamic LDS of the coreset kernel, in 4-byte words (the only LDS of the
 // kernel, so word 0 is 16-byte aligned).  Rows of Ep = pad4(E) words keep
-// the 128-bit reads of S and Sv aligned.
+// the 128-bit reads aligned.  tc: tokens per masked-sum chunk (at most one
+// selection entry per thread, at most kCoreMWords of probabilities).
 struct CoreLayout {
-  int Ep, tc;  // padded row, tokens per masked-sum chunk
-  size_t misc, S, Sv, order, M, total;
+  int Ep, tc, tc8;
+  size_t misc, wcnt, S, Sv, order, keys, rankc, M, total;
 };
 
-__host__ __device__ inline CoreLayout core_layout(int bs, int E) {
+__host__ __device__ inline CoreLayout core_layout(int bs, int E, int k) {
   CoreLayout L;
   L.Ep = dev::pad4(E);
-  L.misc = 0;              // the block's total, the coreset size
-  L.S = 4;                 // block sums, then Sn in place
-  L.Sv = L.S + L.Ep;       // Sn in rank order
-  L.order = L.Sv + L.Ep;   // expert ids in rank order
-  L.M = L.order + L.Ep;    // [tc][Ep] masked-sum chunk, then rank counters
-  const size_t budget = kCoreLdsBudget / 4;
-  const size_t room = budget > L.M ? (budget - L.M) / L.Ep : 0;
-  L.tc = static_cast<int>(room < static_cast<size_t>(bs) ? room : static_cast<size_t>(bs));
-  L.total = L.M + static_cast<size_t>(L.tc) * L.Ep;
+  int tc = kCoreThreads / (k > 0 ? k : 1);
+  tc = tc < kCoreTokChunk ? tc : kCoreTokChunk;
+  tc = tc < kCoreMWords / L.Ep ? tc : kCoreMWords / L.Ep;
+  L.tc = tc < bs ? tc : bs;
+  L.misc = 0;                             // the block's total, the coreset size, keys below +0's
+  L.wcnt = 4;                             // per-wave ballot counts, kCoreCols * kCoreWaves
+  L.S = L.wcnt + kCoreCols * kCoreWaves;  // block sums, then Sn in place
+  L.Sv = L.S + L.Ep;                      // Sn in rank order, zeros up to a multiple of 64
+  L.order = L.Sv + ((L.Ep + kWave - 1) & ~(kWave - 1));  // expert ids in rank order
+  L.keys = L.order + L.Ep;                // the nonzero sums (total), then the listed experts'
+                                          // 64-bit ranking keys (2 Ep words)
+  L.rankc = L.keys + 2 * L.Ep;            // rank counters, then the Top-P walk's prefix sums
+  L.tc8 = (L.tc + 7) & ~7;                // rows of M, read in groups of 8
+  L.M = L.rankc + (L.Ep > kWave ? L.Ep : kWave);  // [tc8][Ep] masked probabilities of a chunk
+  L.total = L.M + static_cast<size_t>(L.tc8) * L.Ep;
   return L;
 }
 
 // One workgroup per block: S from the tokens' own top-k (own_sel [T][k], in
-// token order), Sn, the ranking, the Top-P cut and the coreset.
+// token order), Sn, the ranking, the Top-P cut and the coreset.  Every float
+// sum runs in the order the definition states; zeros are skipped only where
+// adding them is exact.
 __global__ __launch_bounds__(kCoreThreads) void block_coreset_kernel(
-    const float* __restrict__ probs, const int32_t* __restrict__ own_sel, int bs, int E, int k, float p,
+    const float* __restrict__ own_p, const int32_t* __restrict__ own_sel, int bs, int E, int k, float p,
     int min_c, float* __restrict__ block_scores, int32_t* __restrict__ coreset,
     int32_t* __restrict__ coreset_size) {
   extern __shared__ __align__(16) float lds[];
-  const CoreLayout L = core_layout(bs, E);
+  const CoreLayout L = core_layout(bs, E, k);
   const int Ep = L.Ep;
   float* S = lds + L.S;
   float* Sv = lds + L.Sv;
   int* order = reinterpret_cast<int*>(lds + L.order);
-  float* M = lds + L.M;
+  float* nzv = lds + L.keys;  // step 2 (the keys come later)
+  uint64_t* keys = reinterpret_cast<uint64_t*>(lds + L.keys);
+  int* rankc = reinterpret_cast<int*>(lds + L.rankc);
+  float* cumv = lds + L.rankc;  // step 6 (the counters are read by then)
+  int* wcnt = reinterpret_cast<int*>(lds + L.wcnt);
   float& s_total = lds[L.misc];
   int& s_csize = reinterpret_cast<int*>(lds)[L.misc + 1];
+  int& s_nbelow = reinterpret_cast<int*>(lds)[L.misc + 2];
 
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int b = blockIdx.x;
-  const float* pb = probs + static_cast<size_t>(b) * bs * E;
+  const float* pb = own_p + static_cast<size_t>(b) * bs * k;
   const int32_t* sb = own_sel + static_cast<size_t>(b) * bs * k;
 
   // 1. S[e]: the masked sums in token order.  Chunks of tc tokens are
   //    scattered into a dense [tc][Ep] matrix (zero where a token did not
-  //    select e, so adding it is exact), then each thread adds its column.
-  float acc[2] = {0.f, 0.f};  // columns tid and tid + 512 (E <= 1024)
+  //    select e, so adding it is exact), then each thread adds its column,
+  //    eight rows per batch with all reads first (rows past the chunk are
+  //    zero too).
+  float* M = lds + L.M;
+  if (tid == 0) s_nbelow = 0;
+  float acc[kCoreCols] = {0.f, 0.f};
   for (int c0 = 0; c0 < bs; c0 += L.tc) {
     const int nt = min(L.tc, bs - c0);
-    for (int i = tid; i < nt * Ep; i += kCoreThreads) M[i] = 0.f;
+    const bool has_sel = tid < nt * k;
+    const int e_sel = has_sel ? sb[static_cast<size_t>(c0) * k + tid] : 0;
+    const float p_sel = has_sel ? pb[static_cast<size_t>(c0) * k + tid] : 0.f;
+    for (int i = tid; i < L.tc8 * Ep; i += kCoreThreads) M[i] = 0.f;
     __syncthreads();
-    for (int i = tid; i < nt * k; i += kCoreThreads) {
-      const int tl = i / k;
-      const int e = sb[c0 * k + i];
-      M[tl * Ep + e] = pb[static_cast<size_t>(c0 + tl) * E + e];
-    }
+    if (has_sel && static_cast<unsigned>(e_sel) < static_cast<unsigned>(E)) M[(tid / k) * Ep + e_sel] = p_sel;
     __syncthreads();
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < kCoreCols; ++h) {
       const int e = tid + h * kCoreThreads;
       if (e < Ep)
-        for (int tl = 0; tl < nt; ++tl) acc[h] += M[tl * Ep + e];
+        for (int t0 = 0; t0 < nt; t0 += 8) {
+          float pv[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) pv[u] = M[(t0 + u) * Ep + e];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) acc[h] += pv[u];
+        }
     }
-    __syncthreads();
+    __syncthreads();  // the next chunk clears M
+  }
+
+  // 2. the total, in expert-id order.  Experts that no token selected have
+  //    S = +0, which adds nothing exactly, so only the nonzero sums are added
+  //    (listed in id order).
+  uint64_t m[kCoreCols];
+  bool fl[kCoreCols];
+#pragma unroll
+  for (int h = 0; h < kCoreCols; ++h) {
+    const int e = tid + h * kCoreThreads;
+    if (e < Ep) S[e] = acc[h];  // padding: 0
+    fl[h] = e < E && __float_as_uint(acc[h]) != 0u;
+    m[h] = __builtin_amdgcn_ballot_w64(fl[h]);
+    if (lane == 0) wcnt[h * kCoreWaves + wave] = __popcll(m[h]);
+  }
+  __syncthreads();
+  int before[kCoreCols] = {0, 0}, nlist = 0;
+#pragma unroll
+  for (int g = 0; g < kCoreCols * kCoreWaves; ++g) {
+    const int c = wcnt[g];
+#pragma unroll
+    for (int h = 0; h < kCoreCols; ++h) before[h] += g < h * kCoreWaves + wave ? c : 0;
+    nlist += c;
   }
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
-    if (tid + h * kCoreThreads < Ep) S[tid + h * kCoreThreads] = acc[h];  // padding: 0
+  for (int h = 0; h < kCoreCols; ++h)
+    if (fl[h]) nzv[before[h] + dev::lanes_below(m[h])] = acc[h];
+  if (tid < 4) nzv[nlist + tid] = 0.f;  // exact zeros up to a multiple of 4 (inside the keys)
   __syncthreads();
-
-  // 2. the sum, in expert-id order (padding adds exact zeros); the rank
-  //    counters of step 3 (in M, free now) start at zero
-  int* rankc = reinterpret_cast<int*>(M);
-  for (int e = tid; e < Ep; e += kCoreThreads) rankc[e] = 0;
   if (tid == 0) {
-    const float4* S4 = reinterpret_cast<const float4*>(S);
+    const float4* z4 = reinterpret_cast<const float4*>(nzv);
     float total = 0.f;
 #pragma unroll 8
-    for (int i = 0; i < Ep / 4; ++i) {
-      const float4 q = S4[i];
+    for (int i = 0; i < (nlist + 3) / 4; ++i) {
+      const float4 q = z4[i];
       total += q.x;
       total += q.y;
       total += q.z;
@@ -111,87 +162,135 @@ __global__ __launch_bounds__(kCoreThreads) void block_coreset_kernel(
   }
   __syncthreads();
 
-  // 3. Sn in place, then each expert's rank (Sn desc, id asc) by counting
-  //    over the order keys of Sn (staged in Sv, free until the ranks are
-  //    known); padding (ids >= E) takes key 0 and never ranks before a real
-  //    expert, so the ranks of the E experts are 0 .. E-1
+  // 3. Sn in place and each expert's order key (the key of Sn, at least 1).
+  //    The experts whose key differs from that of +0 -- those with a positive
+  //    Sn -- are listed in id order; the others all share +0's key and so
+  //    rank among themselves by id.  A listed expert's 64-bit ranking key is
+  //    its order key above the complement of its list index: a larger one
+  //    ranks first, so key ties go to the lower index, i.e. the lower id.
   const float total = s_total;
-  uint32_t* Sk = reinterpret_cast<uint32_t*>(Sv);
-  for (int e = tid; e < Ep; e += kCoreThreads) {
-    const float v = S[e] / total;
-    S[e] = v;
-    Sk[e] = e < E ? max(dev::order_key(v), 1u) : 0u;
-    if (block_scores && e < E) block_scores[static_cast<size_t>(b) * E + e] = v;
-  }
-  __syncthreads();
-  {
-    // `parts` threads per expert (a power of two, all 512 threads busy when
-    // E <= 256) each count the experts ranked before it in a slice of the
-    // row; the counts meet in LDS.
-    const int parts = Ep <= 64 ? 8 : Ep <= 128 ? 4 : Ep <= 256 ? 2 : 1;
-    const int n4 = Ep / 4, len = (n4 + parts - 1) / parts;
-    const uint4* K4 = reinterpret_cast<const uint4*>(Sk);
-    for (int idx = tid; idx < E * parts; idx += kCoreThreads) {
-      const int e = idx / parts, h = idx - e * parts;
-      const uint32_t kv = Sk[e];
-      const int m1 = min(n4, (h + 1) * len);
-      int r = 0;
-#pragma unroll 4
-      for (int m = h * len; m < m1; ++m) {
-        const uint4 q = K4[m];
-        r += (dev::key_before(q.x, 4 * m, kv, e) ? 1 : 0) + (dev::key_before(q.y, 4 * m + 1, kv, e) ? 1 : 0) +
-             (dev::key_before(q.z, 4 * m + 2, kv, e) ? 1 : 0) + (dev::key_before(q.w, 4 * m + 3, kv, e) ? 1 : 0);
-      }
-      if (r) atomicAdd(&rankc[e], r);
+  const uint32_t key0 = max(dev::order_key(0.f), 1u);
+  uint32_t kv[kCoreCols];
+#pragma unroll
+  for (int h = 0; h < kCoreCols; ++h) {
+    const int e = tid + h * kCoreThreads;
+    float v = 0.f;
+    if (e < Ep) {
+      v = S[e] / total;
+      S[e] = v;
+      if (block_scores && e < E) block_scores[static_cast<size_t>(b) * E + e] = v;
     }
+    kv[h] = e < E ? max(dev::order_key(v), 1u) : 0u;
+    fl[h] = e < E && kv[h] != key0;
+    m[h] = __builtin_amdgcn_ballot_w64(fl[h]);
+    if (lane == 0) wcnt[h * kCoreWaves + wave] = __popcll(m[h]);
+    if (fl[h] && kv[h] < key0) atomicAdd(&s_nbelow, 1);  // below +0: a NaN with its sign bit set
+  }
+  for (int i = tid; i < Ep; i += kCoreThreads) {
+    keys[i] = 0u;  // padding: below every real key, never counted
+    rankc[i] = 0;
   }
   __syncthreads();
-  for (int e = tid; e < E; e += kCoreThreads) {
-    const int r = rankc[e];
-    order[r] = e;
-    Sv[r] = S[e];
+  nlist = 0;
+  int below[kCoreCols] = {0, 0};  // listed experts with a lower id
+#pragma unroll
+  for (int g = 0; g < kCoreCols * kCoreWaves; ++g) {
+    const int c = wcnt[g];
+#pragma unroll
+    for (int h = 0; h < kCoreCols; ++h) below[h] += g < h * kCoreWaves + wave ? c : 0;
+    nlist += c;
+  }
+#pragma unroll
+  for (int h = 0; h < kCoreCols; ++h) {
+    below[h] += dev::lanes_below(m[h]);
+    if (fl[h]) keys[below[h]] = (static_cast<uint64_t>(kv[h]) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(below[h]));
   }
   __syncthreads();
 
-  // 4. the Top-P cut: cumulative Sn in rank order reaches p, at least min_c.
-  //    One thread adds in rank order, 32 values per batch: a straight chain
-  //    of adds (entries past E add an exact zero), then the first prefix
-  //    that qualifies.
-  if (tid == 0) {
-    const float4* Sv4 = reinterpret_cast<const float4*>(Sv);
+  // 4. ranks (Sn desc, id asc): a listed expert counts the listed ranking
+  //    keys above its own, `parts` threads per expert over slices of the
+  //    list, the counts meeting in LDS.
+  {
+    const int n2 = (nlist + 1) / 2;  // pairs of keys (the padding key is 0)
+    const int parts = nlist > 0 ? max(1, min(8, kCoreThreads / nlist)) : 1;
+    const int len = (n2 + parts - 1) / parts;
+    const ulonglong2* K2 = reinterpret_cast<const ulonglong2*>(keys);
+    for (int idx = tid; idx < nlist * parts; idx += kCoreThreads) {
+      const int i = idx / parts, hh = idx - i * parts;
+      const uint64_t ki = keys[i];
+      const int m1 = min(n2, (hh + 1) * len);
+      int r = 0;
+#pragma unroll 4
+      for (int mm = hh * len; mm < m1; ++mm) {
+        const ulonglong2 q = K2[mm];
+        r += (q.x > ki ? 1 : 0) + (q.y > ki ? 1 : 0);
+      }
+      if (r) atomicAdd(&rankc[i], r);
+    }
+  }
+  __syncthreads();
+
+  // 5. the ranked order.  Listed experts above +0's key take their count;
+  //    the unlisted ones follow in id order; listed ones below +0's key
+  //    (NaNs with the sign bit) come after those.
+  {
+    const int n_unlisted = E - nlist, n_above = nlist - s_nbelow;
+#pragma unroll
+    for (int h = 0; h < kCoreCols; ++h) {
+      const int e = tid + h * kCoreThreads;
+      if (e < E) {
+        const int r = fl[h] ? rankc[below[h]] + (kv[h] < key0 ? n_unlisted : 0) : n_above + (e - below[h]);
+        order[r] = e;
+        Sv[r] = S[e];
+      }
+    }
+    const int e64 = (E + kWave - 1) & ~(kWave - 1);
+    if (E + tid < e64) Sv[E + tid] = 0.f;  // the walk adds these exact zeros
+  }
+  __syncthreads();
+
+  // 6. the Top-P cut: cumulative Sn in rank order reaches p, at least min_c.
+  //    Lane 0 of wave 0 adds 64 ranked values per round, in rank order (a
+  //    straight chain; entries past E add exact zeros), into LDS; the wave
+  //    then finds the first prefix that qualifies with one ballot.
+  if (wave == 0) {
     float cum = 0.f;
     int n = 0;
-    for (int i0 = 0; i0 < E && n == 0; i0 += 32) {
-      float c[32];
+    for (int r0 = 0; r0 < E && n == 0; r0 += kWave) {
+      if (lane == 0) {
+        // all 16 reads first, then the chain (Sv holds exact zeros from E up
+        // to the next multiple of 64)
+        const float4* Sv4 = reinterpret_cast<const float4*>(Sv + r0);
+        float4* C4 = reinterpret_cast<float4*>(cumv);
+        float4 f[kWave / 4];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {  // within the Ep-word row
-        const float4 f = i0 + 4 * q < Ep ? Sv4[i0 / 4 + q] : float4{0.f, 0.f, 0.f, 0.f};
-        c[4 * q] = f.x;
-        c[4 * q + 1] = f.y;
-        c[4 * q + 2] = f.z;
-        c[4 * q + 3] = f.w;
+        for (int q = 0; q < kWave / 4; ++q) f[q] = Sv4[q];
+#pragma unroll
+        for (int q = 0; q < kWave / 4; ++q) {
+          float4 o;
+          cum += f[q].x;
+          o.x = cum;
+          cum += f[q].y;
+          o.y = cum;
+          cum += f[q].z;
+          o.z = cum;
+          cum += f[q].w;
+          o.w = cum;
+          C4[q] = o;
+        }
       }
-#pragma unroll
-      for (int u = 0; u < 32; ++u) {
-        cum += i0 + u < E ? c[u] : 0.f;
-        c[u] = cum;
-      }
-#pragma unroll
-      for (int u = 31; u >= 0; --u)
-        if (i0 + u < E && c[u] >= p && i0 + u + 1 >= min_c) n = i0 + u + 1;
+      wave_sync();
+      const int r = r0 + lane;
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(r < E && cumv[lane] >= p && r + 1 >= min_c);
+      if (hit) n = r0 + __builtin_ctzll(hit) + 1;  // uniform
+      wave_sync();  // every lane has read cumv before lane 0 overwrites it
     }
-    s_csize = n > 0 ? n : E;
+    if (lane == 0) s_csize = n > 0 ? n : E;
   }
   __syncthreads();
   const int csize = s_csize;
   if (tid == 0) coreset_size[b] = csize;
   for (int i = tid; i < csize; i += kCoreThreads) coreset[static_cast<size_t>(b) * E + i] = order[i];
-}
-
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // One wave per token, four per workgroup: the token's top-k inside its
@@ -240,7 +339,7 @@ __global__ __launch_bounds__(256) void topp_select_kernel(const float* __restric
 }  // namespace
 
 bool topp_supported(int bs, int E, int k) {
-  return E <= 64 * dev::kRadixMaxPerLane && k <= dev::kMaxK && core_layout(bs, E).tc >= 1;
+  return E <= 64 * dev::kRadixMaxPerLane && k <= dev::kMaxK && core_layout(bs, E, k).tc >= 1;
 }
 
 hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, float p, int min_c,
@@ -249,15 +348,16 @@ hipError_t launch_block_topp(const float* probs, int nb, int bs, int E, int k, f
   if (!topp_supported(bs, E, k)) return hipErrorInvalidValue;
   const int T = nb * bs;
   hipError_t err;
-  // 1. every token's own top-k, into `experts` (overwritten by step 3;
-  //    own_done: the caller's launch already put it there)
+  // 1. every token's own top-k, into `experts`, and the selected
+  //    probabilities into `w` (both overwritten by step 3; own_done: the
+  //    caller's launch already put them there)
   if (!own_done) {
-    err = launch_token_topk(probs, T, E, k, experts, w, nullptr, s);
+    err = launch_token_topk(probs, T, E, k, experts, w, nullptr, s, true);
     if (err != hipSuccess) return err;
   }
   // 2. one workgroup per block
-  block_coreset_kernel<<<nb, kCoreThreads, core_layout(bs, E).total * sizeof(float), s>>>(
-      probs, experts, bs, E, k, p, min_c, block_scores, coreset, coreset_size);
+  block_coreset_kernel<<<nb, kCoreThreads, core_layout(bs, E, k).total * sizeof(float), s>>>(
+      w, experts, bs, E, k, p, min_c, block_scores, coreset, coreset_size);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   // 3. one wave per token
