@@ -145,18 +145,23 @@ __global__ __launch_bounds__(kCoreThreads) void block_coreset_kernel(
 #pragma unroll
   for (int h = 0; h < kCoreCols; ++h)
     if (fl[h]) nzv[before[h] + dev::lanes_below(m[h])] = acc[h];
-  if (tid < 4) nzv[nlist + tid] = 0.f;  // exact zeros up to a multiple of 4 (inside the keys)
+  if (tid < kWave) nzv[nlist + tid] = 0.f;  // exact zeros up to a multiple of 64
   __syncthreads();
   if (tid == 0) {
+    // 64 values per round, all 16 reads first, then the chain
     const float4* z4 = reinterpret_cast<const float4*>(nzv);
     float total = 0.f;
-#pragma unroll 8
-    for (int i = 0; i < (nlist + 3) / 4; ++i) {
-      const float4 q = z4[i];
-      total += q.x;
-      total += q.y;
-      total += q.z;
-      total += q.w;
+    for (int r0 = 0; r0 < nlist; r0 += kWave) {
+      float4 q[kWave / 4];
+#pragma unroll
+      for (int j = 0; j < kWave / 4; ++j) q[j] = z4[r0 / 4 + j];
+#pragma unroll
+      for (int j = 0; j < kWave / 4; ++j) {
+        total += q[j].x;
+        total += q[j].y;
+        total += q[j].z;
+        total += q[j].w;
+      }
     }
     s_total = total;
   }
