@@ -123,8 +123,6 @@ struct FfnParams {
   const int* row_slot;
   int T, H, E, I, I_s, k, Tk, R, max_work;  // R: rows of the h buffer
   int shared_items;                        // grid rows of the shared expert's pieces (0: none)
-  int split_rows;                          // > 0: decode kernels take items of <= split_rows rows,
-                                           // the tile kernels the larger ones
   bf16_t* hk;                              // SwiGLU activations, chunk-major [ldh/8][R][8]
   void* slot_out;                          // [T][k][H], float32 or scaled half (slot_f16s)
   float* shared_out;
@@ -170,7 +168,6 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
                                  p.Tk, p.E, g))
     return;
-  if (p.split_rows > 0 && (g.n > p.split_rows || g.piece > 0)) return;  // a tile-kernel item
   const int Iw = g.expert >= 0 ? p.I : p.I_s;
   const int it = blockIdx.x * RT;  // first of the RT packed tiles (Iw / 8 is a multiple of 16)
   if (it * 8 >= Iw) return;
@@ -232,7 +229,6 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_down_bf16_kernel(FfnParams
   if (!decode_item<kSharedFirst>(blockIdx.y, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T,
                                  p.Tk, p.E, g))
     return;
-  if (p.split_rows > 0 && (g.n > p.split_rows || g.piece > 0)) return;  // a tile-kernel item
   const int Kd = g.expert >= 0 ? p.I : p.I_s;
   const int H = p.H;
   const int jt = blockIdx.x * RT;  // first of the RT packed tiles (H / 16 is a multiple of 8)
@@ -500,7 +496,6 @@ __global__ __launch_bounds__(kThreads, 2) void ffn_tile_bf16_kernel(FfnParams p,
   if (!map_item(p, gx, item, bx)) return;
   Group g;
   if (!decode_item(item, p.shared_items, p.max_work, p.n_work, p.work, p.row_token, p.T, p.Tk, p.E, g)) return;
-  if (g.piece == 0 && g.n <= p.split_rows) return;  // a decode-kernel item (split_rows 0: every item is ours)
   __shared__ bf16x8 stage[2][kStageSteps][kTileTok][kWave];  // 32 KiB
   // An expert whose rows are one item is the only reader of its weights in
   // the launch (each row block reads its own rows once): they are streamed
@@ -736,24 +731,7 @@ hipError_t launch_tile_bf16(const FfnParams& p, int ldh, int items, hipStream_t 
   return hipGetLastError();
 }
 
-constexpr int kSplitRows = 16;  // one-tile schedules: items of more than one pass go to the tile kernels
-
-// One-tile decode kernels for the items of <= p.split_rows rows and the tile
-// kernels for the others; each gate/up half runs before either down half.
-hipError_t launch_hybrid_bf16(const FfnParams& p, int ldh, int items, hipStream_t s) {
-  using S = Shape<1>;
-  ffn_gateup_bf16_kernel<1, S::kGuMax, S::kGuChunk, S::kGuWaves, S::kSharedFirst, S::kGuRows>
-      <<<dim3(ldh / (8 * S::kGuRows), items), kThreads, 0, s>>>(p);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  err = launch_tile_bf16<true>(p, ldh, items, s);
-  if (err != hipSuccess) return err;
-  ffn_down_bf16_kernel<1, S::kDnMax, S::kDnChunk, S::kDnWaves, S::kSharedFirst, S::kDnRows>
-      <<<dim3(p.H / (16 * S::kDnRows), items), kThreads, 0, s>>>(p);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  return launch_tile_bf16<false>(p, ldh, items, s);
-}
+constexpr int kPassRows = 16;  // token rows of one decode-kernel pass
 
 bool use_tile_kernels(int T, int k, int max_work, int items, int ldh) {
   return rows_per_item(T, k, max_work) >= 32 && static_cast<long>(ldh / 32) * items >= 512;
@@ -778,7 +756,7 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
                 static_cast<const bf16_t*>(a.w13), static_cast<const bf16_t*>(a.w2),
                 static_cast<const bf16_t*>(a.ws13),
                 static_cast<const bf16_t*>(a.ws2), a.sched.n_work, a.sched.work, a.sched.row_token,
-                a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items, 0,
+                a.sched.row_slot, a.T, a.H, a.E, a.I, a.I_s, a.k, Tk, R, a.max_work, shared_items,
                 static_cast<bf16_t*>(a.workspace), a.slot_out, a.shared_out,
                 a.slot_fmt == DMOE_SLOT_F16S ? 1 : 0};
     if (use_tile_kernels(a.T, a.k, a.max_work, items, ldh)) {
@@ -793,11 +771,14 @@ hipError_t launch_ffn(const FfnArgs& a, dmoe_dtype dt, hipStream_t s) {
         // shared expert over more than 16 tokens).  The decode kernels keep a
         // wave's weight slice in registers across 16-row passes when it is
         // one burst; when it is not, they would stream the weights once per
-        // pass, so items of more than one pass (16 rows) go to the tile
-        // kernels, launched beside them.
-        if (a.T > kSplitRows && (a.H / 128 > Shape<1>::kGuMax || ldh / 128 > Shape<1>::kDnMax)) {
-          p.split_rows = kSplitRows;
-          return launch_hybrid_bf16(p, ldh, items, s);
+        // pass, so such layers run every item on the tile kernels (measured
+        // faster than leaving the items of one pass to the decode kernels,
+        // whose grids, sized for the worst case, cost ~17 us each when few
+        // items are that small).
+        if (a.T > kPassRows && (a.H / 128 > Shape<1>::kGuMax || ldh / 128 > Shape<1>::kDnMax)) {
+          const hipError_t err = launch_tile_bf16<true>(p, ldh, items, s);
+          if (err != hipSuccess) return err;
+          return launch_tile_bf16<false>(p, ldh, items, s);
         }
         return launch_bf16<1>(p, ldh, items, s);
       case 2: return launch_bf16<2>(p, ldh, items, s);

@@ -4,8 +4,9 @@ dmoe_expert_ffn reads the token rows of scattered items (token-level routing)
 from the row-major hidden states when they are given, and from the
 chunk-major copy otherwise.  The same values reach the matrix instructions
 either way, so every output must be bitwise identical.  The cases cover the
-decode kernels (one and two token tiles), the tile kernels and the hybrid
-launch of one-tile schedules with large items.  Marked ``gpu``."""
+decode kernels (one and two token tiles), the tile kernels, and one-tile
+schedules at hidden 4096 with large items (all on the tile kernels).  Marked
+``gpu``."""
 import pytest
 import torch
 
@@ -18,8 +19,7 @@ from parity import poisoned, slot_values
 pytestmark = pytest.mark.gpu
 
 # hidden 4096, popular experts (Zipf bias) and a one-tile token schedule with
-# items of more than 16 rows: the decode kernels and the tile kernels share
-# one launch
+# items of more than 16 rows: the tile kernels take every item, a few rows or many
 HYBRID = MoEConfig("gather_hybrid", "bf16", H=4096, E=64, I=256, I_s=256, k=4, NB=2, bs=48, bias="zipf")
 
 
