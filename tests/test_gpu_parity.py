@@ -8,7 +8,7 @@ import oracle as O
 from dmoe_synth import get_config, make_inputs
 from paper_2605_30876_amd import lib
 from paper_2605_30876_amd.layer import MoELayer, pack_weights
-from parity import check_work, run_and_check
+from parity import check_work, run_and_check, run_and_check_topp
 
 pytestmark = pytest.mark.gpu
 
@@ -60,6 +60,30 @@ def test_tile_kernel_parity(gpu_lib, name, routing):
     d = _to_gpu(make_inputs(cfg, seed=3))
     rep = run_and_check(cfg, d, routing, _layer(cfg))
     _say("  ", {k: v for k, v in rep.items() if k != "near_ties"})
+
+
+# One-tile token-level schedules (a few rows per item) that still take the tile
+# kernels: at least one 16-row pass per expert on average (T*k >= 16 E), with
+# four and eight slots, and a hidden size whose weight slices need more than
+# one burst per wave (H = 2304); token routing and Alg. 1 with Top-P.
+ONE_TILE = {"onetile_pass_e16": dict(H=256, E=16, I=128, I_s=128, k=4, NB=2, bs=32),
+            "onetile_pass_e32_k8": dict(H=256, E=32, I=128, I_s=128, k=8, NB=2, bs=32),
+            "onetile_multiburst": dict(H=2304, E=32, I=128, I_s=128, k=4, NB=1, bs=24)}
+
+
+@pytest.mark.parametrize("routing", ["token", "topp"])
+@pytest.mark.parametrize("name", list(ONE_TILE))
+def test_one_tile_schedules_on_tile_kernels(gpu_lib, name, routing):
+    cfg = get_config("small_bf16").with_(name=name, **ONE_TILE[name])
+    _say("case", name, routing)
+    d = _to_gpu(make_inputs(cfg, seed=4))
+    if routing == "topp":
+        layer = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=torch.bfloat16,
+                         device="cuda", top_p=0.6)
+        rep = run_and_check_topp(cfg, d, layer)
+    else:
+        rep = run_and_check(cfg, d, routing, _layer(cfg))
+    _say("  ", {k: v for k, v in rep.items() if k not in ("near_ties", "coreset_sizes")})
 
 
 # Shapes whose router takes the LDS-staged tiles (T >= 256) with ragged token
