@@ -86,11 +86,14 @@ def test_topp_direct_ties(gpu_lib):
         assert out["ex"][b * bs:(b + 1) * bs].cpu().numpy().tolist() == R.tolist()
 
 
-@pytest.mark.parametrize("E,k,bs,nb,p", [(1024, 8, 64, 2, 0.6), (1000, 5, 33, 3, 0.8), (256, 8, 894, 1, 0.5)])
+@pytest.mark.parametrize("E,k,bs,nb,p", [(1024, 8, 64, 2, 0.6), (1000, 5, 33, 3, 0.8), (256, 8, 894, 1, 0.5),
+                                         (50, 3, 40, 2, 0.7), (600, 16, 40, 2, 0.9)])
 def test_topp_direct_shapes(gpu_lib, E, k, bs, nb, p):
     """Shapes whose masked sums take several LDS chunks (E = 1024 and 1000,
-    and a block of 894 tokens at E = 256); router-like rows (softmax of
-    N(0, 2^2) logits) given directly."""
+    a block of 894 tokens at E = 256, 40 tokens with 16 slots at E = 600),
+    an expert count that is not a multiple of 4 (E = 50) and experts past 512
+    (a second expert per thread); router-like rows (softmax of N(0, 2^2)
+    logits) given directly."""
     from parity import accepted_selection
 
     print("case", E, k, bs, nb, p, flush=True)
