@@ -68,7 +68,9 @@ def test_tile_kernel_parity(gpu_lib, name, routing):
 # one burst per wave (H = 2304); token routing and Alg. 1 with Top-P.
 ONE_TILE = {"onetile_pass_e16": dict(H=256, E=16, I=128, I_s=128, k=4, NB=2, bs=32),
             "onetile_pass_e32_k8": dict(H=256, E=32, I=128, I_s=128, k=8, NB=2, bs=32),
-            "onetile_multiburst": dict(H=2304, E=32, I=128, I_s=128, k=4, NB=1, bs=24)}
+            "onetile_multiburst": dict(H=2304, E=32, I=128, I_s=128, k=4, NB=1, bs=24),
+            # the smallest matrix-core shapes (H = I = 128), eight experts, top-2
+            "onetile_h128_e8": dict(H=128, E=8, I=128, I_s=128, k=2, NB=2, bs=32)}
 
 
 @pytest.mark.parametrize("routing", ["token", "topp"])
