@@ -251,9 +251,8 @@ def mall_resident(torch, layers, routing, use_graph, steps=290):
 
 def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
     """A decode step of STEP_LAYERS chained MoE layers (the step's input
-    plus layer l's output is layer l+1's input), timed per mode; the adds
-    alone are timed too, so the MoE part of the step is reported without
-    them."""
+    plus layer l's output is layer l+1's input, written by layer l's own
+    last kernel), timed per mode."""
     from paper_2605_30876_amd.layer import decode_step
 
     L = STEP_LAYERS
@@ -261,12 +260,7 @@ def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
     ms = [m for _, _, m in sub]
     ws = [w for _, w, _ in sub]
     xs = [sub[0][0]] + [torch.empty_like(sub[0][0]) for _ in range(L - 1)]
-    out = {"layers": L}
-
-    def glue(_i):
-        for l in range(L - 1):
-            torch.add(xs[0], ms[l].y, out=xs[l + 1])
-
+    out = {"layers": L, "residual_adds": "fused into each layer's last kernel"}
     for routing in modes:
         decode_step(ms, ws, xs, routing)
         torch.cuda.synchronize()
@@ -276,14 +270,7 @@ def chained_step(torch, cfg, layers, modes, use_graph, steps=8):
         U = statistics.mean(int(m.sched.n_unique[0]) for m in ms)
         out[routing] = {"us_per_step": round(wall / steps * 1e6, 2), "gpu_event_us_per_step": round(gpu_s / steps * 1e6, 2),
                         "unique_experts_per_layer": round(U, 2)}
-    r = Runner(torch, 1, glue, use_graph)
-    wall, _ = r.time(steps)
-    r.close()
-    out["residual_adds_us"] = round(wall / steps * 1e6, 2)
-    for routing in modes:
-        out[routing]["moe_us_per_step"] = round(out[routing]["us_per_step"] - out["residual_adds_us"], 2)
-    log(f"[bench] {L}-layer decode step: " + ", ".join(f"{m} {out[m]['us_per_step']} us" for m in modes)
-        + f" (residual adds {out['residual_adds_us']} us)")
+    log(f"[bench] {L}-layer decode step: " + ", ".join(f"{m} {out[m]['us_per_step']} us" for m in modes))
     return out
 
 

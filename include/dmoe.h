@@ -479,6 +479,13 @@ dmoe_status dmoe_combine(const void* slot_out, dmoe_slot_format slot_fmt, const 
  * shared_out NULL iff I_s == 0).  y [T][H] of type y_dt.  workspace: at least
  * dmoe_moe_forward_workspace_size bytes (contents on entry do not matter;
  * calls sharing one must not overlap in time).
+ * Residual (optional, for chaining layers: the next layer's input is a base
+ * stream plus this layer's output): with res_out set, the forward also
+ * writes res_out[t][h] = round_dt(res_in[t][h] + y[t][h]), y taken in
+ * float32 before its own rounding to y_dt, both [T][H] of type dt; res_in
+ * must then be set too, and neither may overlap y or x.  The three-kernel
+ * path writes it from the down projection's epilogue and the chained path
+ * from the combine, so no further kernel runs.  res_out NULL: not written.
  * Limits: those of the chained entry points (E <= 512; bf16: H, I, I_s
  * multiples of 128).
  */
@@ -504,6 +511,8 @@ typedef struct dmoe_layer_buffers {
   float* shared_out;
   void* workspace;
   size_t ws_bytes;
+  const void* res_in;   /* [T][H] of dt, or NULL (no residual output) */
+  void* res_out;        /* [T][H] of dt: round_dt(res_in + y), or NULL */
 } dmoe_layer_buffers;
 
 /* Bytes of dmoe_layer_buffers.workspace for these sizes (0 on invalid sizes). */

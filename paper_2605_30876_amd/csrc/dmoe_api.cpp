@@ -617,6 +617,20 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
   }
   const size_t need = layer_workspace_bytes(n_blocks, block_size, H, E, I, I_s, k, dt);
   REQUIRE(buf->ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", buf->ws_bytes, need);
+  REQUIRE(!buf->res_out || buf->res_in, "res_out needs res_in");
+  {
+    // the residual's arrays are [T][H] of dt and overlap neither x nor y
+    const size_t rb = static_cast<size_t>(T) * H * dmoe::dtype_bytes(dt);
+    const size_t yb = static_cast<size_t>(T) * H * dmoe::dtype_bytes(y_dt);
+    auto overlaps = [](const void* a, size_t na, const void* b, size_t nb) {
+      const char* pa = static_cast<const char*>(a);
+      const char* pb = static_cast<const char*>(b);
+      return pa < pb + nb && pb < pa + na;
+    };
+    REQUIRE(!buf->res_out || (!overlaps(buf->res_out, rb, y, yb) && !overlaps(buf->res_out, rb, x, rb) &&
+                              !overlaps(buf->res_in, rb, y, yb)),
+            "res_out and res_in must not overlap x or y");
+  }
   ALIGNED(x);
   ALIGNED(w_router);
   ALIGNED(bias);
@@ -637,6 +651,8 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
   ALIGNED(buf->slot_out);
   ALIGNED(buf->shared_out);
   ALIGNED(buf->workspace);
+  ALIGNED(buf->res_in);
+  ALIGNED(buf->res_out);
   ALIGNED(sched.n_unique);
   ALIGNED(sched.unique);
   ALIGNED(sched.offsets);
@@ -660,7 +676,7 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
   if (routing == DMOE_ROUTE_BLOCK && dmoe::layer_fused_fits(dt, n_blocks, Ti, H, E, I, I_s, k)) {
     dmoe::LayerArgs a{x, w_router, bias, w13, w2, ws13, ws2, Ti, H, E, I, I_s, k, buf->logits, buf->probs,
                       buf->x_chunked, buf->block_scores, buf->experts, buf->combine_w, buf->gap, sched,
-                      buf->workspace, y, y_dt};
+                      buf->workspace, y, y_dt, buf->res_in, buf->res_out};
     return hip_status(dmoe::launch_layer_fused(a, s), __func__);
   }
   const size_t rbytes = dmoe::router_workspace_bytes(Ti, H, E, dt);
@@ -685,7 +701,7 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
   err = dmoe::launch_ffn(fa, dt, s);
   if (err != hipSuccess) return hip_status(err, __func__);
   return hip_status(dmoe::launch_combine(buf->slot_out, buf->slot_fmt, buf->combine_w, buf->shared_out, y_dt, Ti, H,
-                                         k, y, s),
+                                         k, y, s, buf->res_in, buf->res_out, dt),
                     __func__);
 }
 

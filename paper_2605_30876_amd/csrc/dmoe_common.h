@@ -176,6 +176,7 @@ bool route_fused_fits(int T, int E, int k, int gs, bool block);
 
 // 16-byte chunks: elements of one chunk of the chunk-major activation layout.
 inline int chunk_elems(dmoe_dtype dt) { return dt == DMOE_F32 ? 4 : 8; }
+inline size_t dtype_bytes(dmoe_dtype dt) { return dt == DMOE_F32 ? 4 : 2; }
 
 hipError_t launch_pack_weights(const void* wg, const void* wu, const void* wd, dmoe_dtype dt, int E,
                                int H, int I, void* w13, void* w2, hipStream_t s);
@@ -226,12 +227,16 @@ struct LayerArgs {
   void* workspace;  // layer_fused_workspace_bytes
   void* y;
   dmoe_dtype y_dt;
+  const void* res_in;  // residual: res_out = bf16(res_in + y), or nullptr
+  void* res_out;
 };
 bool layer_fused_fits(dmoe_dtype dt, int n_blocks, int T, int H, int E, int I, int I_s, int k);
 size_t layer_fused_workspace_bytes(int T, int E, int I, int I_s, int k);
 hipError_t launch_layer_fused(const LayerArgs& a, hipStream_t s);
 
+// res_out (optional): res_out = round_res_dt(res_in + y) from the fp32 sum.
 hipError_t launch_combine(const void* slot_out, dmoe_slot_format slot_fmt, const float* w,
-                          const float* shared_out, dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s);
+                          const float* shared_out, dmoe_dtype dt, int T, int H, int k, void* y, hipStream_t s,
+                          const void* res_in = nullptr, void* res_out = nullptr, dmoe_dtype res_dt = DMOE_BF16);
 
 }  // namespace dmoe

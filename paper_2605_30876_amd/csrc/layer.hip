@@ -31,6 +31,8 @@
 //     the j-th expert's intermediate units (the last wave over the shared
 //     expert's), and the waves' partial tiles are added in wave order, so y
 //     is deterministic and there is no per-slot output and no combine launch.
+//     With a residual the same epilogue writes res_in + y (the next layer's
+//     input) as well.
 //
 // Activations between the launches are chunk-major over the concatenated
 // reduction index: hk[(kk/8)*T + t][kk%8], kk = j*I + i for routed slot j and
@@ -75,6 +77,8 @@ struct LayerParams {
   float* gap;          // [1] or nullptr
   dmoe_schedule sched;
   void* y;             // [T][H], float32 or bf16
+  const bf16_t* res_in;  // [T][H] or nullptr: res_out = bf16(res_in + y), y in fp32
+  bf16_t* res_out;
 };
 
 // ---- launch 1: router tiles and the shared expert's gate/up -----------------
@@ -529,6 +533,16 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
   }
   const bf16_t* W = shared ? p.ws2 : p.w2 + static_cast<size_t>(p.experts[wave]) * H * p.I;
   const bf16_t* pa = W + static_cast<size_t>(jt) * ksteps * kFrag + lane * 8;
+  // the residual's four inputs of this lane (wave 0 writes the outputs),
+  // loaded before the product so that their latency is hidden
+  uint2 rin[NT];
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    rin[ct] = make_uint2(0u, 0u);
+    const int tok = min((tt + ct) * kTok + c, T - 1);
+    if (p.res_out && wave == 0)
+      rin[ct] = *reinterpret_cast<const uint2*>(p.res_in + static_cast<size_t>(tok) * H + jt * 16 + 4 * q);
+  }
   f32x4 acc[1][NT];
   fdev::zero(acc);
   fdev::WaveOps<NT, 16, kTokChunk<NT>, 1> w;
@@ -546,7 +560,15 @@ __global__ __launch_bounds__(kMaxSegments * kWave) void layer_down_combine_kerne
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
     const int col = (tt + ct) * kTok + c;
-    if (col < T) store_y(y + static_cast<size_t>(col) * H + jt * 16 + 4 * q, acc[0][ct]);
+    if (col >= T) continue;
+    store_y(y + static_cast<size_t>(col) * H + jt * 16 + 4 * q, acc[0][ct]);
+    if (p.res_out) {
+      const f32x4 r = {bf16_to_f32(static_cast<bf16_t>(rin[ct].x & 0xFFFFu)),
+                       bf16_to_f32(static_cast<bf16_t>(rin[ct].x >> 16)),
+                       bf16_to_f32(static_cast<bf16_t>(rin[ct].y & 0xFFFFu)),
+                       bf16_to_f32(static_cast<bf16_t>(rin[ct].y >> 16))};
+      store_y(p.res_out + static_cast<size_t>(col) * H + jt * 16 + 4 * q, r + acc[0][ct]);
+    }
   }
 }
 
@@ -596,7 +618,8 @@ hipError_t launch_layer_fused(const LayerArgs& a, hipStream_t s) {
                 a.k, static_cast<float*>(a.workspace), router_slices(a.H, a.E),
                 static_cast<bf16_t*>(a.x_chunked),
                 reinterpret_cast<bf16_t*>(static_cast<char*>(a.workspace) + zb), a.logits, a.probs, a.block_scores,
-                a.experts, a.combine_w, a.gap, a.sched, a.y};
+                a.experts, a.combine_w, a.gap, a.sched, a.y, static_cast<const bf16_t*>(a.res_in),
+                static_cast<bf16_t*>(a.res_out)};
   if (a.T <= kTok) return launch_nt<1>(p, a.y_dt, s);
   if (a.T <= 2 * kTok) return launch_nt<2>(p, a.y_dt, s);
   return launch_nt<4>(p, a.y_dt, s);

@@ -195,14 +195,18 @@ class MoELayer:
                          stream)
 
     def forward(self, x, w: dict, routing: str = "block", stream=None, fused_routing: bool = True,
-                chained: bool = False) -> torch.Tensor:
+                chained: bool = False, residual=None) -> torch.Tensor:
         """Whole layer on hidden states x[T, H] with weights from
         :func:`pack_weights`; returns (a view of) y[T, H].
 
         By default one dmoe_moe_forward call (three kernels for a block-routed
         single block, else the chain below inside the library).  chained=True
         (or overlap_shared) enqueues the routing, expert FFN and combine entry
-        points one by one instead."""
+        points one by one instead.  residual=(base, out): the same call also
+        writes out = base + y, rounded once to the layer's type (one-call
+        forward only)."""
+        if residual is not None and (chained or self.overlap_shared or not fused_routing):
+            raise ValueError("a residual output needs the one-call forward")
         if not chained and not self.overlap_shared and fused_routing:
             self._x = x
             lib.dmoe_moe_forward(x, w["w_router"], w.get("bias"), w["w13"], w["w2"], w.get("ws13"), w.get("ws2"),
@@ -210,7 +214,7 @@ class MoELayer:
                                  self.min_coreset, self.logits, self.probs, self.x_chunked,
                                  self.block_scores, self.experts(routing), self.combine_w, self.gaps(routing),
                                  self.coreset, self.coreset_size, self.sched, self.slot_out, self.shared_out,
-                                 self.layer_ws, self.y, stream)
+                                 self.layer_ws, self.y, stream, *(residual if residual is not None else (None, None)))
             return self.y
         main = stream if stream is not None else torch.cuda.current_stream()
         if self.overlap_shared:
@@ -252,11 +256,10 @@ def decode_step(layers: list, weights: list, xs: list, routing: str = "block", s
     ``layers`` are MoELayer objects of one shape, ``weights`` their packed
     weights, ``xs`` len(layers) preallocated [T, H] tensors of the storage
     type with xs[0] the step's input.  Returns the last layer's output y.
-    The add is one torch kernel per layer boundary; everything else runs in
-    libdmoe."""
+    Each layer's call writes the next layer's input itself (the add is
+    fused into its last kernel), so the step runs in libdmoe only."""
     y = None
+    L = len(layers)
     for l, (m, w) in enumerate(zip(layers, weights)):
-        y = m.forward(xs[l], w, routing, stream)
-        if l + 1 < len(layers):
-            torch.add(xs[0], y, out=xs[l + 1])
+        y = m.forward(xs[l], w, routing, stream, residual=(xs[0], xs[l + 1]) if l + 1 < L else None)
     return y

@@ -64,7 +64,8 @@ class dmoe_layer_buffers(ctypes.Structure):
                 ("gap", ctypes.c_void_p), ("coreset", ctypes.c_void_p), ("coreset_size", ctypes.c_void_p),
                 ("sched", dmoe_schedule), ("slot_out", ctypes.c_void_p), ("slot_fmt", ctypes.c_int),
                 ("shared_out", ctypes.c_void_p),
-                ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t)]
+                ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
+                ("res_in", ctypes.c_void_p), ("res_out", ctypes.c_void_p)]
 
 
 _P = ctypes.c_void_p
@@ -329,12 +330,15 @@ def dmoe_moe_forward_fused(dt, n_blocks, block_size, H, E, I, I_s, k, routing: s
 
 def dmoe_moe_forward(x, w_router, bias, w13, w2, ws13, ws2, n_blocks, block_size, H, E, I, I_s, k, routing: str,
                      top_p, min_coreset, logits, probs, x_chunked, block_scores, experts, combine_w, gap, coreset,
-                     coreset_size, sched: Schedule, slot_out, shared_out, workspace, y, stream=None):
+                     coreset_size, sched: Schedule, slot_out, shared_out, workspace, y, stream=None, res_in=None,
+                     res_out=None):
     """One MoE layer forward; ``routing`` is "block", "token" or "topp"; the
-    buffers are gathered into a dmoe_layer_buffers (a host struct)."""
+    buffers are gathered into a dmoe_layer_buffers (a host struct).  With
+    res_out, also res_out = round(res_in + y) (the next layer's input)."""
     buf = dmoe_layer_buffers(ptr(logits), ptr(probs), ptr(x_chunked), ptr(block_scores), ptr(experts),
                              ptr(combine_w), ptr(gap), ptr(coreset), ptr(coreset_size), sched.as_c(), ptr(slot_out),
-                             slot_format_code(slot_out), ptr(shared_out), ptr(workspace), _nbytes(workspace))
+                             slot_format_code(slot_out), ptr(shared_out), ptr(workspace), _nbytes(workspace),
+                             ptr(res_in), ptr(res_out))
     _check(load().dmoe_moe_forward(ptr(x), ptr(w_router), ptr(bias), ptr(w13), ptr(w2), ptr(ws13), ptr(ws2),
                                    dtype_code(x), n_blocks, block_size, H, E, I, I_s, k, ROUTING[routing],
                                    float(top_p), min_coreset, ctypes.byref(buf), ptr(y), dtype_code(y),

@@ -389,12 +389,14 @@ def test_ffn_noalloc_validation(L, buf):
 def _moe(L, p, ws_bytes=1 << 30, **kw):
     a = dict(x=p, wr=p, bias=None, w13=p, w2=p, ws13=p, ws2=p, dt=lib.DMOE_BF16, NB=1, bs=32, H=2048, E=256, I=512,
              I_s=512, k=8, routing=lib.DMOE_ROUTE_BLOCK, top_p=0.6, min_c=8, y=p, y_dt=lib.DMOE_F32)
-    bufkw = {f: kw.pop(f) for f in list(kw) if f in ("probs", "coreset", "shared_out", "workspace", "slot_fmt")}
+    bufkw = {f: kw.pop(f) for f in list(kw)
+             if f in ("probs", "coreset", "shared_out", "workspace", "slot_fmt", "res_in", "res_out")}
     a.update(kw)
     sched = lib.dmoe_schedule(p, p, p, p, p, p, p, None)
     buf = lib.dmoe_layer_buffers(None, bufkw.get("probs", p), p, None, p, p, None, bufkw.get("coreset", None), None,
                                  sched, p, bufkw.get("slot_fmt", lib.DMOE_SLOT_F16S), bufkw.get("shared_out", p),
-                                 bufkw.get("workspace", p), ws_bytes)
+                                 bufkw.get("workspace", p), ws_bytes, bufkw.get("res_in", None),
+                                 bufkw.get("res_out", None))
     return status(L, "dmoe_moe_forward", a["x"], a["wr"], a["bias"], a["w13"], a["w2"], a["ws13"], a["ws2"],
                   a["dt"], a["NB"], a["bs"], a["H"], a["E"], a["I"], a["I_s"], a["k"], a["routing"], a["top_p"],
                   a["min_c"], ctypes.byref(buf), a["y"], a["y_dt"], None)
@@ -417,6 +419,16 @@ def test_moe_forward_validation(L, buf):
     assert _moe(L, p, E=600)[0] == UNS
     assert _moe(L, p, slot_fmt=3)[0] == INV
     assert _moe(L, p, dt=lib.DMOE_F32, H=256, I=128, I_s=128)[0] == UNS  # scaled-half slots in an fp32 layer
+    # the residual output: needs its input, must not overlap y or x, aligned
+    T, H = 32, 2048
+    far = p + (1 << 28)
+    st, msg = _moe(L, p, y=far, x=far + (1 << 24), res_out=p + (1 << 26))
+    assert st == INV and "res_in" in msg
+    assert _moe(L, p, y=far, x=far + (1 << 24), res_in=p + (1 << 25), res_out=far + 256)[0] == INV  # overlaps y
+    assert _moe(L, p, y=far, x=far + (1 << 24), res_in=far, res_out=p + (1 << 26))[0] == INV  # res_in overlaps y
+    assert _moe(L, p, y=far, x=far + (1 << 24), res_in=p + (1 << 25), res_out=far + (1 << 24) + 64)[0] == INV
+    assert _moe(L, p, y=far, x=far + (1 << 24), res_in=p + (1 << 25) + 2, res_out=p + (1 << 26))[0] == INV
+    del T, H
     st = L.dmoe_moe_forward(p, p, None, p, p, p, p, lib.DMOE_BF16, 1, 32, 2048, 256, 512, 512, 8, 0, 0.6, 8, None, p,
                             lib.DMOE_F32, None)
     assert st == INV  # buf is NULL

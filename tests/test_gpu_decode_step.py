@@ -60,6 +60,20 @@ def test_decode_step_graph_equals_eager(gpu_lib, chain, routing):
 
 
 @pytest.mark.parametrize("routing", ["block", "token", "topp"])
+def test_decode_step_residual_is_the_rounded_sum(gpu_lib, chain, routing):
+    """Each layer's call writes the next layer's input, base + y rounded once
+    to bf16 (the one-block path from the down projection's epilogue, the
+    chained path from the combine): bitwise torch's fp32 add and cast."""
+    cfg, ds, ws, ms, xs = chain
+    print("case", routing, flush=True)
+    decode_step(ms, ws, xs, routing)
+    torch.cuda.synchronize()
+    for l in range(L - 1):
+        ref = (xs[0].float() + ms[l].y.float()).to(torch.bfloat16)
+        assert torch.equal(xs[l + 1], ref), f"layer {l}: residual output differs"
+
+
+@pytest.mark.parametrize("routing", ["block", "token", "topp"])
 def test_decode_step_layers_match_oracle(gpu_lib, chain, routing):
     """Every layer under block routing, the first, middle and last under token
     and Top-P routing (the oracle's token-routed layer costs more)."""
