@@ -90,3 +90,23 @@ def test_decode_step_layers_match_oracle(gpu_lib, chain, routing):
         else:
             rep = run_and_check(cfg, d, routing, ms[l], check_determinism=False, packed=ws[l])
         print("  layer", l, routing, "n_unique", rep["n_unique"], "y_err", round(rep["y_err_rms"], 5), flush=True)
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16"])
+@pytest.mark.parametrize("routing", ["block", "token", "topp"])
+def test_residual_output_other_layers(gpu_lib, name, routing):
+    """The residual output of an fp32 layer (base + y in fp32) and of a
+    several-block bf16 layer (the chained path's combine), against torch."""
+    cfg = get_config(name)
+    print("case", name, routing, flush=True)
+    d = make_inputs(cfg, seed=9, device="cuda")
+    w = pack_weights(d)
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    m = MoELayer(cfg.H, cfg.E, cfg.I, cfg.I_s, cfg.k, cfg.NB, cfg.bs, dtype=dt, device="cuda")
+    base = torch.randn_like(d["x"], dtype=torch.float32).to(dt)
+    out = torch.full_like(d["x"], float("nan"))
+    y = m.forward(d["x"], w, routing, residual=(base, out))
+    torch.cuda.synchronize()
+    assert torch.equal(out, (base.float() + y.float()).to(dt))
+    with pytest.raises(ValueError):
+        m.forward(d["x"], w, routing, chained=True, residual=(base, out))
