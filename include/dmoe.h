@@ -483,7 +483,8 @@ dmoe_status dmoe_combine(const void* slot_out, dmoe_slot_format slot_fmt, const 
  * stream plus this layer's output): with res_out set, the forward also
  * writes res_out[t][h] = round_dt(res_in[t][h] + y[t][h]), y taken in
  * float32 before its own rounding to y_dt, both [T][H] of type dt; res_in
- * must then be set too, and neither may overlap y or x.  The three-kernel
+ * must then be set too.  res_out may overlap neither x nor y (it is written
+ * while they are read); res_in may be x itself but must not overlap y.  The three-kernel
  * path writes it from the down projection's epilogue and the chained path
  * from the combine, so no further kernel runs.  res_out NULL: not written.
  * Limits: those of the chained entry points (E <= 512; bf16: H, I, I_s

@@ -619,7 +619,7 @@ dmoe_status dmoe_moe_forward(const void* x, const void* w_router, const float* b
   REQUIRE(buf->ws_bytes >= need, "workspace of %zu bytes is smaller than the %zu bytes needed", buf->ws_bytes, need);
   REQUIRE(!buf->res_out || buf->res_in, "res_out needs res_in");
   {
-    // the residual's arrays are [T][H] of dt and overlap neither x nor y
+    // the residual's arrays are [T][H] of dt; res_out overlaps neither x nor y, res_in not y (it may be x)
     const size_t rb = static_cast<size_t>(T) * H * dmoe::dtype_bytes(dt);
     const size_t yb = static_cast<size_t>(T) * H * dmoe::dtype_bytes(y_dt);
     auto overlaps = [](const void* a, size_t na, const void* b, size_t nb) {
