@@ -141,3 +141,38 @@ def test_single_block_logits_output(gpu_lib, base, kw):
     err = float(np.abs(got - ref).max())
     print("  logits max|err|", err, "max|z|", float(np.abs(ref).max()), flush=True)
     assert err <= 1e-4 * max(1.0, float(np.abs(ref).max()))
+
+
+@pytest.mark.parametrize("E,k", [(64, 8), (256, 8), (256, 12), (8, 8)])
+def test_single_block_layer_exact_ties(gpu_lib, E, k):
+    """Router rows repeated in groups of 4 (2 for E = 8) make experts with
+    identical logits, so the block means tie exactly: the one-block path's
+    selection is the oracle's (score desc, id asc) order of its own block
+    scores, k distinct ids, and bitwise that of the chained entry points."""
+    import oracle as O
+
+    H, I, NB, bs = 256, 128, 1, 32
+    rep = 4 if E >= 16 else 2
+    g = torch.Generator().manual_seed(7 + E + k)
+    base = (0.02 * torch.randn((E // rep, H), generator=g)).to(torch.bfloat16)
+    w_router = base.repeat_interleave(rep, dim=0)
+    x = torch.randn((NB * bs, H), generator=g).to(torch.bfloat16)
+    wg, wu = ((0.02 * torch.randn((E, I, H), generator=g)).to(torch.bfloat16) for _ in range(2))
+    wd = (0.02 * torch.randn((E, H, I), generator=g)).to(torch.bfloat16)
+    d = {"x": x.cuda(), "w_router": w_router.cuda(), "bias": None, "w_gate": wg.cuda(), "w_up": wu.cuda(),
+         "w_down": wd.cuda()}
+    w = pack_weights(d)
+    one = MoELayer(H, E, I, 0, k, NB, bs, device="cuda")
+    ch = MoELayer(H, E, I, 0, k, NB, bs, device="cuda")
+    assert one.fused("block")
+    print("case", E, k, flush=True)
+    y1 = one.forward(d["x"], w, "block").clone()
+    y2 = ch.forward(d["x"], w, "block", chained=True).clone()
+    torch.cuda.synchronize()
+    S = one.block_scores.cpu().numpy()
+    assert np.array_equal(S[0][0::rep], S[0][1::rep])  # the ties are real
+    sel = one.block_experts[0].cpu().tolist()
+    assert sel == O.topk(S[0], k)[0].tolist()
+    assert len(set(sel)) == k
+    assert torch.equal(one.block_experts, ch.block_experts)
+    assert float((y1 - y2).abs().max()) <= 2e-2 * float(y2.pow(2).mean().sqrt())
