@@ -717,17 +717,21 @@ hipError_t launch_bf16(const FfnParams& p, int ldh, int groups, hipStream_t s) {
 // halve the LDS reads per weight byte; one tile per wave doubles the
 // workgroups.  A gate/up grid of fewer than two rounds of the chip (three
 // resident workgroups on each of 256 CUs) ends in a long partial round, which
-// the finer split shortens; both halves of the FFN take the gate/up choice.
+// the finer split shortens.  The down projection always takes two tiles per
+// wave: its reduction (I) is short, and at one tile per wave a workgroup
+// reads twice as many token bytes as weight bytes.
 constexpr long kTileRound = 3L * 256;
 template <bool kGateUp>
 hipError_t launch_tile_bf16(const FfnParams& p, int ldh, int items, hipStream_t s) {
-  const bool fine = static_cast<long>(ldh / 64) * items < 2 * kTileRound;
   const int tiles = kGateUp ? ldh / 8 : p.H / 16;  // packed 16-row tiles
   const int items8 = (items + 7) / 8 * 8;
-  if (fine)
-    ffn_tile_bf16_kernel<kGateUp, 1><<<dim3(tiles / 4 * items8), kThreads, 0, s>>>(p, tiles / 4);
-  else
-    ffn_tile_bf16_kernel<kGateUp, 2><<<dim3(tiles / 8 * items8), kThreads, 0, s>>>(p, tiles / 8);
+  if constexpr (kGateUp) {
+    if (static_cast<long>(ldh / 64) * items < 2 * kTileRound) {
+      ffn_tile_bf16_kernel<true, 1><<<dim3(tiles / 4 * items8), kThreads, 0, s>>>(p, tiles / 4);
+      return hipGetLastError();
+    }
+  }
+  ffn_tile_bf16_kernel<kGateUp, 2><<<dim3(tiles / 8 * items8), kThreads, 0, s>>>(p, tiles / 8);
   return hipGetLastError();
 }
 
