@@ -206,6 +206,21 @@ def cmd_mfma(a):
         print(f"| `{pat}` | {n} | {m:.0f} | {gflop:.1f} | {us if us else '—'} | {rate} |")
 
 
+def cmd_stalls(a):
+    """Where the waves of each kernel spend their cycles: SQ wave-cycle
+    counters as fractions of SQ_WAVE_CYCLES (all counted in the same units)."""
+    names = ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS")
+    rows = {c: read_counters(a.csv, c) for c in ("SQ_WAVE_CYCLES",) + names}
+    print("| kernel | dispatches | wave-cycles per dispatch | waiting (any) | waiting to issue | issuing | issuing LDS "
+          "| waiting to issue LDS |\n|---|---|---|---|---|---|---|---|")
+    for pat in a.kernel:
+        w, n = mean_per_dispatch(rows["SQ_WAVE_CYCLES"], pat)
+        if not w:
+            continue
+        fr = [mean_per_dispatch(rows[c], pat)[0] / w for c in names]
+        print(f"| `{pat}` | {n} | {w:.3g} | " + " | ".join(f"{100 * f:.1f}%" for f in fr) + " |")
+
+
 def cmd_sweep(a):
     with open(a.json) as fh:
         sw = json.loads(fh.read().strip().splitlines()[-1])["sweep"]
@@ -281,6 +296,10 @@ def main(argv=None):
     m.add_argument("--simds", type=int, default=1024, help="SIMDs on the chip (256 CUs x 4)")
     m.add_argument("--avg-us", type=float, nargs="*", help="average duration of each --kernel (kernel trace)")
     m.set_defaults(fn=cmd_mfma)
+    st = sub.add_parser("stalls")
+    st.add_argument("--csv", required=True)
+    st.add_argument("--kernel", nargs="+", required=True)
+    st.set_defaults(fn=cmd_stalls)
     c = sub.add_parser("configs")
     c.add_argument("--json", nargs="+", required=True)
     c.add_argument("--cmd", required=True)
