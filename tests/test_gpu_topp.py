@@ -128,3 +128,42 @@ def test_topp_direct_shapes(gpu_lib, E, k, bs, nb, p):
             gw = dict(zip(ex_h[b * bs + t].tolist(), w_h[b * bs + t].tolist()))
             assert max(abs(gw[e] - r) for e, r in zip(acc[t].tolist(), ref.tolist())) <= 1e-6
     print("   near-ties", len(log), "coreset sizes", size.cpu().tolist(), flush=True)
+
+
+# Single blocks of several expert counts, slot counts and block sizes (one
+# token up to 256), p from 0.4 to 1, and a minimum coreset of every expert.
+ONE_BLOCK = [(256, 64, 4, 5, 0.6, None), (256, 256, 8, 32, 0.4, None), (512, 300, 11, 17, 0.8, None),
+             (256, 8, 2, 1, 0.6, None), (256, 512, 8, 64, 0.9, None), (256, 64, 4, 24, 1.0, None),
+             (256, 64, 4, 24, 0.3, 64), (256, 256, 8, 256, 0.6, None)]
+
+
+@pytest.mark.parametrize("H,E,k,bs,p,min_c", ONE_BLOCK)
+def test_topp_one_block_equals_separate_kernels(gpu_lib, H, E, k, bs, p, min_c):
+    """The one-call Top-P routing of a single block gives bitwise what the
+    separate entry points give (router, dmoe_block_topp_route, then the
+    token-level schedule), and its layer forward matches the oracle."""
+    cfg = get_config("small_bf16").with_(name=f"topp1_e{E}_k{k}_bs{bs}", H=H, E=E, k=k, NB=1, bs=bs, I=128, I_s=128)
+    print("case", cfg.name, p, min_c, flush=True)
+    d = make_inputs(cfg, seed=13, device="cuda")
+    one, sep = _layer(cfg, p, min_c), _layer(cfg, p, min_c)
+    one.route(d["x"], d["w_router"], d.get("bias"), "topp", fused=True)
+    sep.route(d["x"], d["w_router"], d.get("bias"), "topp", fused=False)
+    torch.cuda.synchronize()
+    assert torch.equal(one.probs, sep.probs)
+    assert torch.equal(one.block_scores, sep.block_scores)
+    n = int(sep.coreset_size[0])
+    assert int(one.coreset_size[0]) == n
+    assert torch.equal(one.coreset[0, :n], sep.coreset[0, :n])
+    assert torch.equal(one.token_experts, sep.token_experts)
+    assert torch.equal(one.combine_w, sep.combine_w)
+    assert torch.equal(one.token_gap, sep.token_gap)
+    a, b = one.sched, sep.sched
+    nu = int(b.n_unique[0])
+    assert int(a.n_unique[0]) == nu
+    assert torch.equal(a.unique[:nu], b.unique[:nu]) and torch.equal(a.offsets[:nu + 1], b.offsets[:nu + 1])
+    assert torch.equal(a.row_token[:bs * k], b.row_token[:bs * k])
+    assert torch.equal(a.row_slot[:bs * k], b.row_slot[:bs * k])
+    nw = int(b.n_work[0])
+    assert int(a.n_work[0]) == nw and torch.equal(a.work[:nw], b.work[:nw])
+    if E <= 512:
+        run_and_check_topp(cfg, d, _layer(cfg, p, min_c))
