@@ -21,6 +21,11 @@
         GRBM_GUI_ACTIVE`` run) and, given each kernel's average duration from
         a kernel trace, the achieved TFLOP/s against the dense bf16 peak.
 
+    python -m paper_2605_30876_amd.prof_summary stalls --csv CSV --kernel PATTERN ...
+        Where each kernel's waves spend their resident cycles (SQ_WAIT_ANY,
+        SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_ANY, SQ_ACTIVE_INST_LDS and
+        SQ_WAIT_INST_LDS over SQ_WAVE_CYCLES, per dispatch).
+
     python -m paper_2605_30876_amd.prof_summary sweep --json OUT.json --cmd C
         The JSON line of ``bench.py --sweep`` as markdown tables.
 
