@@ -183,6 +183,18 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
 
   __shared__ f32x4 red[3][RT][NT][kWave];
   WaveOps<NT, KMAX, BC, RT> w;  // a one-burst weight slice stays here across passes
+  // At two token tiles (items of whole blocks) a one-burst slice is loaded
+  // before the token rows are known: the weights wait only for the work
+  // item, not for its row list and then x.  With one token tile (many small
+  // items) the token fragments going first measured faster.
+  bool a_held = false;
+  if constexpr (NT == 2) {
+    if (steps <= KMAX) {
+      issue_a<true>(w, pa, tstride, steps);
+      a_held = true;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
   for (int p0 = 0; p0 < g.n; p0 += 16 * NT) {
     const bf16_t* pb[NT];
     int tok[NT];
@@ -199,7 +211,7 @@ __global__ __launch_bounds__(kThreads, MINW) void ffn_gateup_bf16_kernel(FfnPara
                         : p.xk + (static_cast<size_t>(chunk0) * p.T + tok[ct]) * 8;
     f32x4 acc[RT][NT];
     zero(acc);
-    wave_dot<true>(w, pa, tstride, pb, gathered ? 32 : bstep, steps, acc, p0 > 0 && steps <= KMAX);
+    wave_dot<true>(w, pa, tstride, pb, gathered ? 32 : bstep, steps, acc, a_held || (p0 > 0 && steps <= KMAX));
     reduce_waves(acc, red, wave, lane);
     if (wave == 0) {
 #pragma unroll
